@@ -1,0 +1,81 @@
+/*
+ * CIERA reference oracle: plain, slow, scalar C on host buffers.
+ *
+ * TEST INFRASTRUCTURE ONLY. Nothing in the product path may include, link or
+ * call this file: only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it. It shares no code, header, table or helper with the
+ * HIP library; it defines its own copy of every constant it needs.
+ *
+ * What it computes follows the paper (CIERA, "Cross-Iteration Exponent Reuse
+ * for Lossless Allgather in Sharded MoE Training"):
+ *   - Section 3.1 and Algorithm 1 (appendix): split every value into exponent
+ *     and sign+mantissa, mark the blocks whose exponents changed in a
+ *     one-bit-per-block bitmap, send the changed blocks' exponents, and on the
+ *     receiver patch the exponent cache and merge.
+ *   - Section 3.2: the size definitions S, S_e, S_{s+m}, S_b, S_bm, the
+ *     expected payload S_{s+m} + S_bm + q S_e, the gain g_i and the
+ *     benefit-to-memory ranking.
+ * Readings where the paper is silent (exact compare instead of a block hash,
+ * no entropy coder on the exceptions, the wire header and alignment) are
+ * stated next to the code that takes them.
+ *
+ * Parity pins: every function here is pinned by tests that do not re-use
+ * this code (IEEE-semantics exponent extraction, brute force over all bf16
+ * patterns, closed-form sizes, the reuse model (1-c)^B, hand-computed gains).
+ */
+#ifndef CIERA_ORACLE_H
+#define CIERA_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Worst-case encoded size in bytes of an n-element shard at block size B. */
+uint64_t oracle_encoded_bound(uint64_t n, uint64_t B);
+
+/* Split (Algorithm 1, SplitExpMant): e[k] = biased exponent field,
+ * sm[k] = sign bit in bit 7, the 7 mantissa bits in bits 6..0. */
+void oracle_split(const uint16_t *w, uint64_t n, uint8_t *e, uint8_t *sm);
+
+/* Encode one shard. raw != 0 emits the uncompressed form (cache unused, may be
+ * NULL). Returns the total encoded size in bytes, or 0 on error (bad B, buffer
+ * too small). out must hold oracle_encoded_bound(n, B) bytes. */
+uint64_t oracle_encode(const uint16_t *w, const uint8_t *cache, uint64_t n,
+                       uint64_t B, int raw, uint8_t *out, uint64_t out_cap);
+
+/* Decode one encoded shard of n elements against cache (updated in place to
+ * the exponents of the decoded values). Returns 0, or a negative code when
+ * the header does not describe an n-element shard. */
+int oracle_decode(const uint8_t *enc, uint64_t n, uint8_t *cache, uint16_t *out);
+
+/* Decode R shards found at gathered + offsets[j]; shard j writes
+ * out[j*n_s ..] and updates cache[j*n_s ..]. Returns 0 or the first error. */
+int oracle_decode_gathered(const uint8_t *gathered, const uint64_t *offsets,
+                           uint64_t R, uint64_t n_s, uint16_t *out,
+                           uint8_t *cache);
+
+/* Apply an encoded shard's changed blocks to a cache (the receiver's
+ * ExpCache patch of Algorithm 1 without the merge). RAW shards set the whole
+ * cache. Returns 0 or a negative code. */
+int oracle_update_cache(uint8_t *cache, const uint8_t *enc, uint64_t n);
+
+/* Section 3.2 gain in seconds with the alpha-beta link model
+ * Comm(x) = alpha + (R-1) x / bw. */
+double oracle_gain(uint64_t n, uint64_t B, double q, uint64_t R, double alpha_s,
+                   double bw_Bps, double t_hash_s, double t_cmp_s,
+                   double t_decmp_s, int overlapped, double header_bytes);
+
+/* Section 3.2 ranking: keep shards with g > 0, sort by g/M descending (ties by
+ * index), take them greedily while the cache budget allows. Writes 1/0 into
+ * selected[i]; returns the number selected. stop_at_first_misfit != 0 stops
+ * at the first shard that does not fit instead of skipping it. */
+uint64_t oracle_select(const double *gain, const double *mem, uint64_t count,
+                       double budget, int stop_at_first_misfit,
+                       uint8_t *selected);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,53 @@
+"""Exponent / sign / mantissa of bf16 values derived from their *value*.
+
+Used by the tests to pin the oracle to something other than itself: the
+oracle extracts fields with bit masks; here the fields come from IEEE-754
+semantics (bf16 is binary32 with the low 16 bits dropped) through frexp and
+magnitude comparisons. A transposed shift, a wrong mask or a wrong packing
+order in the oracle disagrees with these on some value.
+"""
+import numpy as np
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    b = np.asarray(bits).astype(np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32)
+
+
+def exponent_field(bits: np.ndarray) -> np.ndarray:
+    """Biased 8-bit exponent: 0 for zero and subnormals, 255 for Inf/NaN,
+    otherwise floor(log2|x|) + 127 (frexp returns |m| in [0.5, 1))."""
+    x = bf16_to_f32(bits).astype(np.float64)
+    out = np.zeros(x.shape, np.int64)
+    special = ~np.isfinite(x)
+    out[special] = 255
+    ax = np.abs(np.where(special, 0.0, x))
+    normal = ax >= 2.0 ** -126
+    _, ex = np.frexp(ax[normal])
+    out[normal] = ex + 126
+    return out.astype(np.uint8)
+
+
+def sign_bit(bits: np.ndarray) -> np.ndarray:
+    return np.signbit(bf16_to_f32(bits)).astype(np.uint8)
+
+
+def mantissa7(bits: np.ndarray) -> np.ndarray:
+    """The 7 stored fraction bits of finite values, from the magnitude:
+    normal |x| = (1 + m/128) 2^(e-127), subnormal |x| = (m/128) 2^-126.
+    Non-finite values return -1 (their payload is not a magnitude)."""
+    x = bf16_to_f32(bits).astype(np.float64)
+    out = np.full(x.shape, -1, np.int64)
+    fin = np.isfinite(x)
+    ax = np.abs(np.where(fin, x, 0.0))
+    e = exponent_field(bits).astype(np.int64)
+    normal = fin & (e > 0)
+    sub = fin & (e == 0)
+    out[normal] = np.rint((ax[normal] / np.exp2(e[normal] - 127.0) - 1.0)
+                          * 128.0).astype(np.int64)
+    out[sub] = np.rint(ax[sub] * 2.0 ** 133).astype(np.int64)
+    return out
+
+
+def all_bf16_patterns() -> np.ndarray:
+    return np.arange(65536, dtype=np.uint32).astype(np.uint16)
