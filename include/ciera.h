@@ -1,0 +1,190 @@
+/*
+ * libciera: the CIERA exponent-reuse codec for bf16 weight shards on MI355X
+ * (gfx950).
+ *
+ * The method (CIERA, "Cross-Iteration Exponent Reuse for Lossless Allgather
+ * in Sharded MoE Training", Section 3.1 and Algorithm 1 in its appendix):
+ * before each Allgather, every rank splits its bf16 shard into 8-bit
+ * exponents and sign+mantissa bytes, compares the exponents with a cache of
+ * the previous iteration's, marks each block of B values whose exponents
+ * changed in a one-bit-per-block bitmap, and sends the sign+mantissa bytes of
+ * all values, the bitmap and the exponents of the changed blocks. Every
+ * receiver patches its exponent cache with those blocks and merges cache and
+ * sign+mantissa back into the exact bf16 values. Section 3.2 decides per
+ * tensor whether compression pays off at all.
+ *
+ * Differences from the paper's own implementation, all lossless:
+ *   - change detection compares each exponent with the cached byte exactly
+ *     instead of comparing a 128-bit hash per block (same result without the
+ *     2^-128 collision chance);
+ *   - the changed blocks' exponents travel raw (no entropy coder);
+ *   - B is a parameter: 1 (one exception per changed value) or a power of two
+ *     from 16 to 4096 (the paper's default is 512).
+ *
+ * ---------------------------------------------------------------- wire ----
+ * An encoded shard starts with a 64-byte little-endian header:
+ *    0 magic u32 0x52454943 ("CIER")  4 version u16 = 1  6 mode u16
+ *      (0 compressed, 1 raw)          8 B u32           12 reserved u32 = 0
+ *   16 n u64 (values)   24 changed blocks u64   32 exception bytes E u64
+ *   40 payload bytes P u64   48 total bytes u64   56 reserved u64 = 0
+ * compressed body: sign+mantissa plane (n bytes: sign in bit 7, mantissa in
+ *   bits 6..0), bitmap (ceil(ceil(n/B)/8) bytes, block b in bit b%8 of byte
+ *   b/8), exceptions (E bytes: the exponents of every changed block, block
+ *   order); each section starts on a 16-byte boundary, padding bytes are 0;
+ *   P = n + bitmap bytes + E, the paper's S_{s+m} + S_bm + q S_e.
+ * raw body: the n values as little-endian 16-bit words (P = 2n).
+ * total = 64 + the padded sections, always a multiple of 16, so shards
+ * placed back to back keep every shard 16-byte aligned.
+ *
+ * ---------------------------------------------------------- conventions ----
+ * All buffers are device memory unless marked (host); the caller owns every
+ * buffer. GPU calls validate their arguments on the host, enqueue on
+ * `stream`, and return at once: they never allocate, free or synchronise. A
+ * negative return means nothing was enqueued. Errors that only the device can
+ * see (a shard whose header does not match the call, a shard offset that is
+ * not 16-byte aligned, an exception index past the shard's list) set bits in
+ * the error word at the start of the workspace; the shard concerned is skipped
+ * (header errors) or its output is unspecified (inconsistent bitmap), and no
+ * access leaves the shard's `total` bytes. The word is sticky: read it with
+ * ciera_workspace_error after the stream has run.
+ *
+ * The workspace is caller memory of at least ciera_workspace_bytes(); prepare
+ * it once with ciera_workspace_init. Every call leaves it ready for the next.
+ * Calls that share one workspace must be ordered (one stream); calls that
+ * overlap in time need separate workspaces. The library keeps no state.
+ */
+#ifndef CIERA_H
+#define CIERA_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum ciera_status {
+  CIERA_OK = 0,
+  CIERA_EINVAL = -1,       /* null pointer, bad size or flag */
+  CIERA_ENOSPC = -2,       /* output or workspace smaller than required */
+  CIERA_EUNSUPPORTED = -3, /* block size not in {1, 16, 32, ..., 4096} */
+  CIERA_EFORMAT = -4,      /* malformed encoded shard (host-side checks) */
+  CIERA_EHIP = -5          /* the HIP runtime refused a launch or copy */
+};
+
+/* Device error word bits (see ciera_workspace_error). */
+#define CIERA_DEVERR_FORMAT 0x1u   /* header magic/version/mode/n/B mismatch */
+#define CIERA_DEVERR_ALIGN 0x2u    /* a shard offset not 16-byte aligned */
+#define CIERA_DEVERR_BOUNDS 0x4u   /* bitmap flags more blocks than E holds */
+#define CIERA_DEVERR_TIMEOUT 0x8u  /* a scan step waited past its bound */
+
+/* ciera_encode flags */
+#define CIERA_ENC_RAW 0x1u /* emit the uncompressed form (first gather after
+                              warm-up; tensors the selection rule leaves out) */
+
+/* Largest encoded size of an n-value shard at block size B (host). It covers
+ * both the compressed form with every block changed and the raw form. */
+uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems);
+
+/* Workspace bytes for encoding an n-value shard and for decoding (or cache
+ * updating) `nshards` such shards at block size B (host). */
+uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
+                               uint32_t block_elems);
+
+/* Zero the workspace (a fill kernel on `stream`, capturable). Required once
+ * before the first call that uses the workspace. */
+int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
+                         hipStream_t stream);
+
+/* Copy the device error word to *err (host) and, if clear != 0, reset it.
+ * Synchronises `stream` (the only call that does). */
+int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
+                          hipStream_t stream);
+
+/* Sender side of Algorithm 1 for one shard (Section 3.1).
+ *   w_new      n bf16 values as 16-bit patterns.
+ *   exp_cache  n exponent bytes from the previous iteration (read only; NULL
+ *              allowed only with CIERA_ENC_RAW).
+ *   out        at least ciera_encoded_bound(n, B) bytes; receives the encoded
+ *              shard (header + sections + zero padding).
+ *   out_bytes  optional device u64 that receives the total encoded size (the
+ *              same value as the header's `total`); may be NULL.
+ * Encoding is a pure function of (w_new, exp_cache, B, flags): calling it
+ * twice gives identical bytes. The sender's own cache is brought forward
+ * separately (ciera_update_cache), or is the own-rank slot of the caches
+ * ciera_decode_gathered updates. n_elems must be below 2^32. */
+int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
+                 uint64_t n_elems, uint32_t block_elems, uint32_t flags,
+                 void *out, uint64_t out_capacity, uint64_t *out_bytes,
+                 void *workspace, uint64_t workspace_bytes,
+                 hipStream_t stream);
+
+/* Receiver side of Algorithm 1 for the Allgather output: `nshards` encoded
+ * shards of `shard_elems` values each, shard j starting at
+ * gathered + shard_offsets[j] (device u64 array, offsets 16-byte aligned).
+ * For every shard j it patches exp_cache[j*shard_elems ...] with the changed
+ * blocks' exponents and writes the exact values to out[j*shard_elems ...]
+ * (the Merge step); raw shards are copied and seed the cache. Compressed
+ * shards must have been encoded with block_elems. Decoding is idempotent: a
+ * second call with the same gathered buffer gives the same out and cache. */
+int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
+                          uint32_t nshards, uint64_t shard_elems,
+                          uint32_t block_elems, uint16_t *out,
+                          uint8_t *exp_cache, void *workspace,
+                          uint64_t workspace_bytes, hipStream_t stream);
+
+/* The ExpCache patch of Algorithm 1 alone for one encoded shard: afterwards
+ * exp_cache holds the exponents of the values that were encoded (changed
+ * blocks are overwritten from the exception list; a raw shard sets every
+ * byte). This is how a sender brings its own cache forward. */
+int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
+                       uint64_t n_elems, uint32_t block_elems,
+                       void *workspace, uint64_t workspace_bytes,
+                       hipStream_t stream);
+
+/* ---------------------------------------------- selection (Section 3.2) ----
+ * Per-shard gain with an alpha-beta Allgather model
+ *   Comm(x) = alpha + (R - 1) x / bw
+ *   g = Comm(S) - (Comm(S_{s+m} + S_bm + q S_e + header) + T_hash + T_cmp
+ *                  + T_decmp)
+ * with S = 2n, S_e = S_{s+m} = n bytes for bf16, S_bm = ceil(ceil(n/B)/8).
+ * T_hash and T_cmp count as zero when `overlapped` (compression runs on its
+ * own stream beside the Allgather). A shard is compressed iff g > 0. */
+typedef struct {
+  uint64_t n_elems;     /* values in one rank's shard */
+  uint32_t block_elems; /* B */
+  double q;             /* measured fraction of changed blocks, in [0, 1] */
+} ciera_shard_stats;
+
+typedef struct {
+  uint32_t world_size; /* R >= 1 */
+  double alpha_s;      /* per-Allgather latency */
+  double bus_bw_Bps;   /* bytes per second per rank-to-rank transfer */
+  double t_hash_s;     /* sender change detection */
+  double t_cmp_s;      /* sender packing */
+  double t_decmp_s;    /* receiver decode of all R shards (critical path) */
+  double header_bytes; /* fixed bytes per compressed shard (64 here) */
+  int overlapped;      /* nonzero: T_hash and T_cmp are hidden */
+} ciera_cost_model;
+
+/* Host only. Returns 1 (compress), 0 (send raw) or a negative status; the
+ * gain in seconds goes to *gain_s when non-NULL. */
+int ciera_should_compress(const ciera_shard_stats *stats,
+                          const ciera_cost_model *model, double *gain_s);
+
+/* Host only. Section 3.2 ranking: among shards with gain[i] > 0, in order of
+ * gain[i] / mem[i] descending (ties by lower index), mark selected[i] = 1
+ * while the summed mem fits in budget_bytes. A shard that does not fit is
+ * skipped and the scan continues, unless CIERA_SELECT_STOP_AT_MISFIT is set.
+ * mem[i] is the shard's exponent-cache footprint (R * n bytes here). Returns
+ * the number selected or a negative status. */
+#define CIERA_SELECT_STOP_AT_MISFIT 0x1u
+int ciera_select(const double *gain, const double *mem, uint64_t count,
+                 double budget_bytes, uint32_t flags, uint8_t *selected);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CIERA_H */

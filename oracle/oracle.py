@@ -151,10 +151,10 @@ def update_cache(cache: np.ndarray, enc: np.ndarray, n: int) -> None:
         raise ValueError(f"oracle_update_cache: bad shard ({rc})")
 
 
-def gain(n: int, B: int, q: float, R: int, alpha_s: float, bw_Bps: float,
+def gain(n: int, B: int, q: float, R: int, alpha_s: float, bus_bw_Bps: float,
          t_hash_s: float = 0.0, t_cmp_s: float = 0.0, t_decmp_s: float = 0.0,
          overlapped: bool = True, header_bytes: float = HEADER_BYTES) -> float:
-    return float(_load().oracle_gain(n, B, q, R, alpha_s, bw_Bps, t_hash_s,
+    return float(_load().oracle_gain(n, B, q, R, alpha_s, bus_bw_Bps, t_hash_s,
                                      t_cmp_s, t_decmp_s, int(overlapped),
                                      header_bytes))
 

@@ -1,0 +1,210 @@
+"""ctypes binding of libciera (the C ABI in include/ciera.h).
+
+Argument marshalling only: every function forwards to the library call of the
+same name, and every step of the codec runs in the library's HIP kernels. The
+``*_t`` helpers accept torch tensors and pass their device pointers and the
+current HIP stream. Opening the library fails loudly when it is not built;
+there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libciera.so")
+
+OK, EINVAL, ENOSPC, EUNSUPPORTED, EFORMAT, EHIP = 0, -1, -2, -3, -4, -5
+DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS, DEVERR_TIMEOUT = 1, 2, 4, 8
+ENC_RAW = 0x1
+SELECT_STOP_AT_MISFIT = 0x1
+HEADER_BYTES = 64
+STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOSPC: "ENOSPC",
+                EUNSUPPORTED: "EUNSUPPORTED", EFORMAT: "EFORMAT",
+                EHIP: "EHIP"}
+
+
+class CieraError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} returned {STATUS_NAMES.get(code, code)}")
+        self.code = code
+
+
+class ShardStats(ctypes.Structure):
+    _fields_ = [("n_elems", ctypes.c_uint64), ("block_elems", ctypes.c_uint32),
+                ("q", ctypes.c_double)]
+
+
+class CostModel(ctypes.Structure):
+    _fields_ = [("world_size", ctypes.c_uint32), ("alpha_s", ctypes.c_double),
+                ("bus_bw_Bps", ctypes.c_double), ("t_hash_s", ctypes.c_double),
+                ("t_cmp_s", ctypes.c_double), ("t_decmp_s", ctypes.c_double),
+                ("header_bytes", ctypes.c_double), ("overlapped", ctypes.c_int)]
+
+
+_vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
+_SIGS = {
+    "ciera_encoded_bound": (_u64, [_u64, _u32]),
+    "ciera_workspace_bytes": (_u64, [_u64, _u32, _u32]),
+    "ciera_workspace_init": (_i32, [_vp, _u64, _vp]),
+    "ciera_workspace_error": (_i32, [_vp, ctypes.POINTER(_u32), _i32, _vp]),
+    "ciera_encode": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64, _vp, _vp,
+                            _u64, _vp]),
+    "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _vp, _vp, _vp,
+                                     _u64, _vp]),
+    "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _vp, _u64, _vp]),
+    "ciera_should_compress": (_i32, [ctypes.POINTER(ShardStats),
+                                     ctypes.POINTER(CostModel),
+                                     ctypes.POINTER(ctypes.c_double)]),
+    "ciera_select": (_i32, [ctypes.POINTER(ctypes.c_double),
+                            ctypes.POINTER(ctypes.c_double), _u64,
+                            ctypes.c_double, _u32,
+                            ctypes.POINTER(ctypes.c_uint8)]),
+}
+EXPORTED = tuple(_SIGS)
+
+_lib = None
+
+
+def lib():
+    """Open libciera.so (once). Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2609_04609_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(handle, name)
+            f.restype, f.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def _check(fn, rc):
+    if rc < 0:
+        raise CieraError(fn, rc)
+    return rc
+
+
+# ---- the C ABI, name for name (pointers and the stream as integers) ----
+
+def ciera_encoded_bound(n_elems, block_elems):
+    return lib().ciera_encoded_bound(n_elems, block_elems)
+
+
+def ciera_workspace_bytes(n_elems, nshards, block_elems):
+    return lib().ciera_workspace_bytes(n_elems, nshards, block_elems)
+
+
+def ciera_workspace_init(workspace, workspace_bytes, stream):
+    return lib().ciera_workspace_init(workspace, workspace_bytes, stream)
+
+
+def ciera_workspace_error(workspace, clear, stream):
+    err = _u32(0)
+    rc = lib().ciera_workspace_error(workspace, ctypes.byref(err), clear, stream)
+    _check("ciera_workspace_error", rc)
+    return err.value
+
+
+def ciera_encode(w_new, exp_cache, n_elems, block_elems, flags, out,
+                 out_capacity, out_bytes, workspace, workspace_bytes, stream):
+    return lib().ciera_encode(w_new, exp_cache, n_elems, block_elems, flags,
+                              out, out_capacity, out_bytes, workspace,
+                              workspace_bytes, stream)
+
+
+def ciera_decode_gathered(gathered, shard_offsets, nshards, shard_elems,
+                          block_elems, out, exp_cache, workspace,
+                          workspace_bytes, stream):
+    return lib().ciera_decode_gathered(gathered, shard_offsets, nshards,
+                                       shard_elems, block_elems, out,
+                                       exp_cache, workspace, workspace_bytes,
+                                       stream)
+
+
+def ciera_update_cache(exp_cache, encoded, n_elems, block_elems, workspace,
+                       workspace_bytes, stream):
+    return lib().ciera_update_cache(exp_cache, encoded, n_elems, block_elems,
+                                    workspace, workspace_bytes, stream)
+
+
+def ciera_should_compress(n_elems, block_elems, q, world_size, alpha_s,
+                          bus_bw_Bps, t_hash_s=0.0, t_cmp_s=0.0, t_decmp_s=0.0,
+                          header_bytes=float(HEADER_BYTES), overlapped=True):
+    """Returns (decision 0/1, gain in seconds)."""
+    st = ShardStats(n_elems, block_elems, q)
+    cm = CostModel(world_size, alpha_s, bus_bw_Bps, t_hash_s, t_cmp_s,
+                   t_decmp_s, header_bytes, int(overlapped))
+    g = ctypes.c_double(0.0)
+    rc = lib().ciera_should_compress(ctypes.byref(st), ctypes.byref(cm),
+                                     ctypes.byref(g))
+    _check("ciera_should_compress", rc)
+    return rc, g.value
+
+
+def ciera_select(gains, mems, budget_bytes, flags=0):
+    n = len(gains)
+    G = (ctypes.c_double * n)(*gains)
+    M = (ctypes.c_double * n)(*mems)
+    S = (ctypes.c_uint8 * n)()
+    rc = lib().ciera_select(G, M, n, budget_bytes, flags, S)
+    _check("ciera_select", rc)
+    return [bool(x) for x in S]
+
+
+# ---- tensor-level marshalling ----
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t):
+    return 0 if t is None else t.data_ptr()
+
+
+class Workspace:
+    """Device workspace sized for a shard size, shard count and B."""
+
+    def __init__(self, n_elems, nshards, block_elems, device="cuda"):
+        self.nbytes = int(ciera_workspace_bytes(n_elems, nshards, block_elems))
+        if self.nbytes == 0:
+            raise CieraError("ciera_workspace_bytes", EUNSUPPORTED)
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        _check("ciera_workspace_init",
+               ciera_workspace_init(self.buf.data_ptr(), self.nbytes,
+                                    _stream()))
+
+    @property
+    def ptr(self):
+        return self.buf.data_ptr()
+
+    def error(self, clear=True):
+        return ciera_workspace_error(self.ptr, int(clear), _stream())
+
+
+def encode_t(w_bits, cache, block_elems, ws, out, raw=False, out_bytes=None):
+    """Encode a 1-D int16 bit tensor into ``out`` (uint8, bound-sized)."""
+    n = w_bits.numel()
+    rc = ciera_encode(_ptr(w_bits), _ptr(cache), n, block_elems,
+                      ENC_RAW if raw else 0, _ptr(out), out.numel(),
+                      _ptr(out_bytes), ws.ptr, ws.nbytes, _stream())
+    return _check("ciera_encode", rc)
+
+
+def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,
+                      ws):
+    rc = ciera_decode_gathered(_ptr(gathered), _ptr(offsets), offsets.numel(),
+                               shard_elems, block_elems, _ptr(out),
+                               _ptr(cache), ws.ptr, ws.nbytes, _stream())
+    return _check("ciera_decode_gathered", rc)
+
+
+def update_cache_t(cache, encoded, n_elems, block_elems, ws):
+    rc = ciera_update_cache(_ptr(cache), _ptr(encoded), n_elems, block_elems,
+                            ws.ptr, ws.nbytes, _stream())
+    return _check("ciera_update_cache", rc)

@@ -1,0 +1,171 @@
+// C ABI of libciera: host-side argument checks, workspace carving and kernel
+// launches. Declarations and the contract of every entry point are in
+// include/ciera.h.
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "ciera.h"
+#include "ciera_internal.h"
+
+namespace {
+
+using namespace ciera;
+
+// B = 1 or a power of two in [16, 4096]; returns log2(B) or -1.
+int log2_block(uint32_t B) {
+  if (B == 1) return 0;
+  for (int k = 4; k <= 12; ++k)
+    if (B == (1u << k)) return k;
+  return -1;
+}
+
+bool aligned(const void *p, uintptr_t a) {
+  return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+uint64_t status_words(uint64_t workspace_bytes) {
+  return workspace_bytes > kWsCtlBytes ? (workspace_bytes - kWsCtlBytes) / 8
+                                       : 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return 0;
+  const uint64_t compressed = kHeaderBytes + pad16(n_elems) +
+                              pad16(bitmap_bytes(n_elems, uint32_t(l))) +
+                              pad16(n_elems);
+  const uint64_t raw = kHeaderBytes + pad16(2 * n_elems);
+  return compressed > raw ? compressed : raw;
+}
+
+uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
+                               uint32_t block_elems) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return 0;
+  (void)nshards;  // decode needs only the control block at B >= 16
+  const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
+  return kWsCtlBytes + 8 * (tiles + 64);
+}
+
+int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
+                         hipStream_t stream) {
+  if (!workspace || workspace_bytes < kWsCtlBytes || !aligned(workspace, 8))
+    return CIERA_EINVAL;
+  return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream) ==
+                 hipSuccess
+             ? CIERA_OK
+             : CIERA_EHIP;
+}
+
+int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
+                          hipStream_t stream) {
+  if (!workspace || !err) return CIERA_EINVAL;
+  if (hipMemcpyAsync(err, workspace, sizeof(uint32_t), hipMemcpyDeviceToHost,
+                     stream) != hipSuccess)
+    return CIERA_EHIP;
+  if (clear && launch_fill_zero(workspace, sizeof(uint32_t), stream) !=
+                   hipSuccess)
+    return CIERA_EHIP;
+  return hipStreamSynchronize(stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
+                 uint64_t n_elems, uint32_t block_elems, uint32_t flags,
+                 void *out, uint64_t out_capacity, uint64_t *out_bytes,
+                 void *workspace, uint64_t workspace_bytes,
+                 hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return CIERA_EUNSUPPORTED;
+  if (flags & ~CIERA_ENC_RAW) return CIERA_EINVAL;
+  const bool raw = flags & CIERA_ENC_RAW;
+  if (!out || (n_elems && !w_new) || (!raw && n_elems && !exp_cache))
+    return CIERA_EINVAL;
+  if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(out, 16)) return CIERA_EINVAL;
+  if (out_capacity < ciera_encoded_bound(n_elems, block_elems))
+    return CIERA_ENOSPC;
+  uint8_t *o = static_cast<uint8_t *>(out);
+  if (raw) {
+    const bool vec = aligned(w_new, 16);
+    return launch_encode_raw(w_new, n_elems, block_elems, o, out_bytes, vec,
+                             stream) == hipSuccess
+               ? CIERA_OK
+               : CIERA_EHIP;
+  }
+  if (l == 0) return CIERA_EUNSUPPORTED;  // element-level path: not yet built
+  if (!workspace || !aligned(workspace, 8)) return CIERA_EINVAL;
+  const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
+  if (status_words(workspace_bytes) < tiles) return CIERA_ENOSPC;
+  EncArgs a;
+  a.w = w_new;
+  a.cache = exp_cache;
+  a.n = n_elems;
+  a.log2B = uint32_t(l);
+  a.num_tiles = uint32_t(tiles);
+  a.out = o;
+  a.out_bytes = out_bytes;
+  a.ctl = static_cast<WsCtl *>(workspace);
+  a.status = reinterpret_cast<uint64_t *>(static_cast<uint8_t *>(workspace) +
+                                          kWsCtlBytes);
+  a.status_cap = status_words(workspace_bytes);
+  const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
+  return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
+                          uint32_t nshards, uint64_t shard_elems,
+                          uint32_t block_elems, uint16_t *out,
+                          uint8_t *exp_cache, void *workspace,
+                          uint64_t workspace_bytes, hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return CIERA_EUNSUPPORTED;
+  if (l == 0) return CIERA_EUNSUPPORTED;
+  if (!gathered || !shard_offsets || !out || !exp_cache || !workspace)
+    return CIERA_EINVAL;
+  if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
+  if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(gathered, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
+  if (workspace_bytes < kWsCtlBytes) return CIERA_ENOSPC;
+  DecArgs a;
+  a.gathered = static_cast<const uint8_t *>(gathered);
+  a.offsets = shard_offsets;
+  a.n = shard_elems;
+  a.log2B = uint32_t(l);
+  a.nshards = nshards;
+  a.out = out;
+  a.cache = exp_cache;
+  a.ctl = static_cast<WsCtl *>(workspace);
+  const bool vec =
+      (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
+  return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
+                       uint64_t n_elems, uint32_t block_elems, void *workspace,
+                       uint64_t workspace_bytes, hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return CIERA_EUNSUPPORTED;
+  if (l == 0) return CIERA_EUNSUPPORTED;
+  if (!encoded || (n_elems && !exp_cache) || !workspace) return CIERA_EINVAL;
+  if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(encoded, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
+  if (workspace_bytes < kWsCtlBytes) return CIERA_ENOSPC;
+  DecArgs a;
+  a.gathered = static_cast<const uint8_t *>(encoded);
+  a.offsets = nullptr;
+  a.n = n_elems;
+  a.log2B = uint32_t(l);
+  a.nshards = 1;
+  a.out = nullptr;
+  a.cache = exp_cache;
+  a.ctl = static_cast<WsCtl *>(workspace);
+  const bool vec = aligned(exp_cache, 8);
+  return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,96 @@
+// Internal declarations shared by the C ABI (ciera_api.cpp) and the kernels
+// (ciera_kernels.hip). Not installed; include/ciera.h is the public surface.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace ciera {
+
+// ---- wire format (documented in include/ciera.h) ----
+constexpr uint32_t kMagic = 0x52454943u;  // "CIER" little-endian
+constexpr uint32_t kVersion = 1u;
+constexpr uint32_t kModeCompressed = 0u;
+constexpr uint32_t kModeRaw = 1u;
+constexpr uint64_t kHeaderBytes = 64u;
+
+__host__ __device__ constexpr inline uint64_t pad16(uint64_t x) {
+  return (x + 15u) & ~uint64_t(15);
+}
+__host__ __device__ constexpr inline uint64_t blocks_of(uint64_t n,
+                                                       uint32_t log2B) {
+  return (n + (uint64_t(1) << log2B) - 1) >> log2B;
+}
+__host__ __device__ constexpr inline uint64_t bitmap_bytes(uint64_t n,
+                                                          uint32_t log2B) {
+  return (blocks_of(n, log2B) + 7u) >> 3;
+}
+
+// ---- workspace ----
+// [0, 256): control words; [256, ...): one 64-bit scan status per encode
+// tile, or one 32-bit count per decode tile for B = 1.
+struct WsCtl {
+  uint32_t err;     // sticky device error bits (CIERA_DEVERR_*)
+  uint32_t epoch;   // tags scan status words of the current encode call
+  uint32_t ticket;  // next encode tile id (dispatch order)
+  uint32_t done;    // encode tiles finished in the current call
+  uint32_t reserved[60];
+};
+static_assert(sizeof(WsCtl) == 256, "control block is 256 bytes");
+constexpr uint64_t kWsCtlBytes = 256;
+
+// ---- tiling ----
+constexpr int kThreads = 256;  // 4 wave64 per workgroup
+// An "octet" is 8 consecutive values: 16 bytes of bf16, 8 bytes of exponent
+// or sign+mantissa. A lane handles `kOct` octets of a tile per pass.
+constexpr int kEncOct = 8;                           // encode: 16384 values
+constexpr int kEncTile = kThreads * 8 * kEncOct;
+constexpr int kEncOctWide = 16;                      // B = 4096: 32768 values
+constexpr int kEncTileWide = kThreads * 8 * kEncOctWide;
+constexpr int kDecOct = 8;                           // decode: 16384 values
+constexpr int kDecTile = kThreads * 8 * kDecOct;
+
+inline uint64_t enc_tile_elems(uint32_t log2B) {
+  // a tile must hold whole bitmap bytes: a multiple of 8 blocks
+  return (log2B <= 11) ? uint64_t(kEncTile) : uint64_t(kEncTileWide);
+}
+inline uint64_t enc_tiles(uint64_t n, uint32_t log2B) {
+  uint64_t T = enc_tile_elems(log2B);
+  uint64_t t = (n + T - 1) / T;
+  return t ? t : 1;
+}
+
+struct EncArgs {
+  const uint16_t *w;
+  const uint8_t *cache;
+  uint64_t n;
+  uint32_t log2B;
+  uint32_t num_tiles;
+  uint8_t *out;
+  uint64_t *out_bytes;
+  WsCtl *ctl;
+  uint64_t *status;
+  uint64_t status_cap;  // status words available (for the epoch wrap clear)
+};
+
+struct DecArgs {
+  const uint8_t *gathered;
+  const uint64_t *offsets;  // nullptr: one shard at gathered + 0
+  uint64_t n;               // values per shard
+  uint32_t log2B;
+  uint32_t nshards;
+  uint16_t *out;            // nullptr for the cache-update-only pass
+  uint8_t *cache;
+  WsCtl *ctl;
+};
+
+// Launchers (ciera_kernels.hip). Each returns the launch status.
+hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
+hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
+                             uint8_t *out, uint64_t *out_bytes, bool vec,
+                             hipStream_t s);
+hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s);
+hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s);
+
+}  // namespace ciera

@@ -1,0 +1,262 @@
+"""GPU path vs the CPU oracle, byte for byte (tolerance 0: the codec is
+integer bit manipulation). Encode is compared over the whole encoded buffer
+(header, sections, padding); decode over the rebuilt values and the updated
+caches. All calls go through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+# sizes that span several tiles and leave ragged tails (tile = 16384 values
+# at B <= 2048, 32768 at B = 4096)
+SIZES = [1, 7, 8, 9, 100, 511, 4097, 16383, 16384, 16385, 40000,
+         3 * 16384 + 17, 32768 * 3 + 8, 262147]
+BLOCKS = [16, 32, 64, 128, 512, 2048, 4096]
+
+
+@pytest.fixture(scope="module")
+def gu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_util
+    from paper_2609_04609_amd import ciera
+    ciera.lib()
+    return gpu_util
+
+
+@pytest.mark.parametrize("B", BLOCKS)
+def test_encode_matches_oracle(gu, orc, B):
+    ws = None
+    for i, n in enumerate(SIZES):
+        w, w2 = gu.pair(n, 100 * B + i, c=0.002 * (1 + i % 4))
+        cache_h, _ = orc.split(gu.host_u16(w))
+        cache = gu.dev_u8(cache_h)
+        from paper_2609_04609_amd import ciera
+        ws = ws if ws is not None and ws.nbytes >= ciera.ciera_workspace_bytes(
+            n, 1, B) else ciera.Workspace(max(n, 262147), 1, B)
+        out, total, ws = gu.gpu_encode(w2, cache, B, ws)
+        expect = orc.encode(gu.host_u16(w2), cache_h, B)
+        got = gu.host_u8(out)
+        assert total == expect.size, (n, B)
+        np.testing.assert_array_equal(got[:total], expect, err_msg=f"n={n} B={B}")
+        # nothing written past the encoded size
+        assert np.all(got[total:] == 0xA5)
+        assert ws.error() == 0
+
+
+def test_encode_edge_cases(gu, orc):
+    from paper_2609_04609_amd import ciera
+    B = 512
+    ws = ciera.Workspace(1 << 20, 1, B)
+    rng = np.random.default_rng(5)
+    n = 70001
+    w, _ = gu.pair(n, 77)
+    wh = gu.host_u16(w)
+    e_h, _ = orc.split(wh)
+    cases = {
+        "no_change": e_h.copy(),
+        "all_change": (e_h + 1).astype(np.uint8),
+        "random_cache": rng.integers(0, 256, n, dtype=np.uint8),
+    }
+    for name, cache_h in cases.items():
+        out, total, _ = gu.gpu_encode(w, gu.dev_u8(cache_h), B, ws)
+        expect = orc.encode(wh, cache_h, B)
+        np.testing.assert_array_equal(gu.host_u8(out)[:total], expect,
+                                      err_msg=name)
+    # n = 0: header only
+    out, total, _ = gu.gpu_encode(torch.zeros(0, dtype=torch.int16,
+                                              device="cuda"),
+                                  torch.zeros(0, dtype=torch.uint8,
+                                              device="cuda"), B, ws)
+    expect = orc.encode(np.zeros(0, np.uint16), np.zeros(0, np.uint8), B)
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    # raw form
+    for n in [0, 1, 9, 16385]:
+        w, _ = gu.pair(n, 90 + n)
+        out, total, _ = gu.gpu_encode(w, None, B, ws, raw=True)
+        expect = orc.encode(gu.host_u16(w), None, B, raw=True)
+        np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    assert ws.error() == 0
+
+
+def test_encode_unaligned_pointers(gu, orc):
+    """Inputs that are not 16-byte aligned take the element-wise path."""
+    from paper_2609_04609_amd import ciera
+    B, n = 64, 50001
+    w_all, w2_all = gu.pair(n + 1, 31)
+    w, w2 = w_all[1:], w2_all[1:]            # 2-byte offset
+    cache_all = gu.dev_u8(np.concatenate(
+        [[0], orc.split(gu.host_u16(w))[0]]))
+    cache = cache_all[1:]                    # 1-byte offset
+    ws = ciera.Workspace(n, 1, B)
+    out, total, _ = gu.gpu_encode(w2, cache, B, ws)
+    expect = orc.encode(gu.host_u16(w2), gu.host_u8(cache), B)
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+
+
+def test_encode_repeats_and_epoch_wrap(gu, orc):
+    """The workspace is reused call after call (epoch-tagged scan state); the
+    bytes never change, also across the 30-bit epoch wrap."""
+    from paper_2609_04609_amd import ciera
+    B, n = 512, 300000
+    w, w2 = gu.pair(n, 41, c=0.001)
+    cache_h, _ = orc.split(gu.host_u16(w))
+    cache = gu.dev_u8(cache_h)
+    expect = orc.encode(gu.host_u16(w2), cache_h, B)
+    ws = ciera.Workspace(n, 1, B)
+    for _ in range(20):
+        out, total, _ = gu.gpu_encode(w2, cache, B, ws)
+        np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    # move the epoch to the last value before the wrap
+    ws.buf[4:8].copy_(torch.tensor([0x3FFFFFFF], dtype=torch.int32)
+                      .view(torch.uint8).to("cuda"))
+    for _ in range(3):
+        out, total, _ = gu.gpu_encode(w2, cache, B, ws)
+        np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    assert ws.error() == 0
+
+
+def _decode_case(gu, orc, R, n_s, B, raw_mask, seed):
+    """Encode R shards with the oracle, gather them, decode on the GPU."""
+    from paper_2609_04609_amd import synth
+    encs, caches, values = [], [], []
+    for j in range(R):
+        w = synth.normal_bf16_bits(n_s, 0.02, seed + j).numpy().view(np.uint16)
+        w2 = synth.forced_bernoulli_bits(
+            torch.from_numpy(w.view(np.int16)), 0.003, seed + 100 + j
+        ).numpy().view(np.uint16)
+        c, _ = orc.split(w)
+        encs.append(orc.encode(w2, None if raw_mask[j] else c, B,
+                               raw=bool(raw_mask[j])))
+        caches.append(c)
+        values.append(w2)
+    gathered, offs = gu.gather(encs)
+    cache0 = np.concatenate(caches)
+    return gathered, offs, cache0, np.concatenate(values)
+
+
+@pytest.mark.parametrize("B", [16, 64, 512, 4096])
+@pytest.mark.parametrize("R,n_s", [(1, 1), (3, 16385), (4, 40000),
+                                   (5, 7777), (16, 16384), (2, 100003)])
+def test_decode_gathered_matches_oracle(gu, orc, B, R, n_s):
+    from paper_2609_04609_amd import ciera
+    raw_mask = [(j % 3) == 2 for j in range(R)]
+    gathered, offs, cache0, values = _decode_case(gu, orc, R, n_s, B,
+                                                  raw_mask, 1000 * B + R)
+    cache_o = cache0.copy()
+    expect = orc.decode_gathered(gathered, offs, n_s, cache_o)
+    np.testing.assert_array_equal(expect, values)  # oracle round trip
+    g = gu.dev_u8(gathered)
+    o = torch.from_numpy(offs.view(np.int64)).to("cuda")
+    out = torch.empty(R * n_s, dtype=torch.int16, device="cuda")
+    cache = gu.dev_u8(cache0)
+    ws = ciera.Workspace(n_s, R, B)
+    ciera.decode_gathered_t(g, o, n_s, B, out, cache, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u16(out), expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+    # idempotent
+    ciera.decode_gathered_t(g, o, n_s, B, out, cache, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u16(out), expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+    assert ws.error() == 0
+
+
+@pytest.mark.parametrize("B", [16, 512, 4096])
+def test_update_cache_matches_oracle(gu, orc, B):
+    from paper_2609_04609_amd import ciera
+    for n, raw in [(1, False), (16385, False), (100003, False), (5000, True)]:
+        gathered, offs, cache0, values = _decode_case(gu, orc, 1, n, B,
+                                                      [raw], 7 * n + B)
+        cache_o = cache0.copy()
+        orc.update_cache(cache_o, gathered, n)
+        cache = gu.dev_u8(cache0)
+        ws = ciera.Workspace(n, 1, B)
+        ciera.update_cache_t(cache, gu.dev_u8(gathered), n, B, ws)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+        assert ws.error() == 0
+
+
+def test_decode_unaligned_and_bad_shards(gu, orc):
+    from paper_2609_04609_amd import ciera
+    B, R, n_s = 64, 3, 5003          # n_s % 8 != 0: element-wise stores
+    gathered, offs, cache0, values = _decode_case(gu, orc, R, n_s, B,
+                                                  [False] * R, 555)
+    cache_o = cache0.copy()
+    expect = orc.decode_gathered(gathered, offs, n_s, cache_o)
+    g = gu.dev_u8(gathered)
+    o = torch.from_numpy(offs.view(np.int64)).to("cuda")
+    out = torch.empty(R * n_s, dtype=torch.int16, device="cuda")
+    cache = gu.dev_u8(cache0)
+    ws = ciera.Workspace(n_s, R, B)
+    ciera.decode_gathered_t(g, o, n_s, B, out, cache, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u16(out), expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+    # corrupt shard 1's magic: device reports FORMAT, shard 1 left untouched
+    bad = gathered.copy()
+    bad[int(offs[1])] ^= 0xFF
+    out2 = torch.full((R * n_s,), 7, dtype=torch.int16, device="cuda")
+    cache2 = gu.dev_u8(cache0)
+    ciera.decode_gathered_t(gu.dev_u8(bad), o, n_s, B, out2, cache2, ws)
+    torch.cuda.synchronize()
+    assert ws.error() & ciera.DEVERR_FORMAT
+    got = gu.host_u16(out2)
+    np.testing.assert_array_equal(got[:n_s], expect[:n_s])
+    assert np.all(got[n_s:2 * n_s] == 7)
+    np.testing.assert_array_equal(gu.host_u8(cache2)[n_s:2 * n_s],
+                                  cache0[n_s:2 * n_s])
+    # a shard offset that is not 16-byte aligned
+    o_bad = o.clone()
+    o_bad[2] += 8
+    ciera.decode_gathered_t(g, o_bad, n_s, B, out2, cache2, ws)
+    torch.cuda.synchronize()
+    assert ws.error() & ciera.DEVERR_ALIGN
+    # a compressed shard decoded with the wrong block size
+    ciera.decode_gathered_t(g, o, n_s, 128, out2, cache2, ws)
+    torch.cuda.synchronize()
+    assert ws.error() & ciera.DEVERR_FORMAT
+
+
+def test_round_trip_chain_on_gpu(gu, orc):
+    """T iterations of encode -> gather -> decode entirely on the GPU: every
+    shard decodes to its exact values, the sender caches (brought forward by
+    ciera_update_cache) equal the receiver caches, and the oracle agrees on
+    every encoded byte."""
+    from paper_2609_04609_amd import ciera, synth
+    R, n, B, T = 4, 33333, 512, 4
+    ws_e = ciera.Workspace(n, 1, B)
+    ws_d = ciera.Workspace(n, R, B)
+    ws = [synth.normal_bf16_bits(n, 0.02, 300 + j, "cuda") for j in range(R)]
+    send_cache = [torch.zeros(n, dtype=torch.uint8, device="cuda")
+                  for _ in range(R)]
+    recv_cache = torch.zeros(R * n, dtype=torch.uint8, device="cuda")
+    out = torch.empty(R * n, dtype=torch.int16, device="cuda")
+    for t in range(T):
+        encs = []
+        for j in range(R):
+            enc, total, _ = gu.gpu_encode(ws[j], send_cache[j], B, ws_e,
+                                          raw=(t == 0))
+            expect = orc.encode(gu.host_u16(ws[j]),
+                                None if t == 0 else gu.host_u8(send_cache[j]),
+                                B, raw=(t == 0))
+            np.testing.assert_array_equal(gu.host_u8(enc)[:total], expect)
+            ciera.update_cache_t(send_cache[j], enc, n, B, ws_e)
+            encs.append(gu.host_u8(enc)[:total])
+        gathered, offs = gu.gather(encs)
+        ciera.decode_gathered_t(gu.dev_u8(gathered),
+                                torch.from_numpy(offs.view(np.int64)).cuda(),
+                                n, B, out, recv_cache, ws_d)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(gu.host_u16(out),
+                                      np.concatenate([gu.host_u16(x)
+                                                      for x in ws]))
+        np.testing.assert_array_equal(gu.host_u8(recv_cache),
+                                      np.concatenate([gu.host_u8(c)
+                                                      for c in send_cache]))
+        ws = [synth.forced_bernoulli_bits(x, 0.002, 7000 + 10 * t + j)
+              for j, x in enumerate(ws)]
+    assert ws_e.error() == 0 and ws_d.error() == 0
