@@ -49,7 +49,8 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
   if (l < 0) return 0;
   (void)nshards;  // decode needs only the control block at B >= 16
   const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  return kWsCtlBytes + 8 * (tiles + 64);
+  // one scan word per tile and one per group of 64 tiles
+  return kWsCtlBytes + 8 * (tiles + (tiles + 63) / 64 + 32);
 }
 
 int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
@@ -100,7 +101,8 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
   if (l == 0) return CIERA_EUNSUPPORTED;  // element-level path: not yet built
   if (!workspace || !aligned(workspace, 8)) return CIERA_EINVAL;
   const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  if (status_words(workspace_bytes) < tiles) return CIERA_ENOSPC;
+  if (status_words(workspace_bytes) < tiles + (tiles + 63) / 64)
+    return CIERA_ENOSPC;
   EncArgs a;
   a.w = w_new;
   a.cache = exp_cache;

@@ -31,11 +31,10 @@ __host__ __device__ constexpr inline uint64_t bitmap_bytes(uint64_t n,
 // [0, 256): control words; [256, ...): one 64-bit scan status per encode
 // tile, or one 32-bit count per decode tile for B = 1.
 struct WsCtl {
-  uint32_t err;     // sticky device error bits (CIERA_DEVERR_*)
-  uint32_t epoch;   // tags scan status words of the current encode call
-  uint32_t ticket;  // next encode tile id (dispatch order)
-  uint32_t done;    // encode tiles finished in the current call
-  uint32_t reserved[60];
+  uint32_t err;    // sticky device error bits (CIERA_DEVERR_*)
+  uint32_t epoch;  // tags the scan words written by the current encode call
+  uint32_t done;   // tiles finished, counted only in the epoch-wrap call
+  uint32_t reserved[61];
 };
 static_assert(sizeof(WsCtl) == 256, "control block is 256 bytes");
 constexpr uint64_t kWsCtlBytes = 256;

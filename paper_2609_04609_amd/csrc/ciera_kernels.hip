@@ -9,9 +9,9 @@
 // Algorithm 1 (appendix of the paper) split into kernels:
 //   encode   SplitExpMant + change detection + bitmap + exception gather +
 //            payload layout, in one pass. The exception list is compacted in
-//            block order with a single-pass decoupled look-back scan over
-//            tiles (tile ids from a ticket counter so that every tile waits
-//            only on tiles that are already running).
+//            block order with a single-pass two-level scan over tiles (the
+//            wait is a constant number of memory round trips whatever the
+//            number of tiles).
 //   decode   for all R gathered shards at once: ExpCache patch + Merge. Each
 //            tile finds its first exception by counting the bitmap bits in
 //            front of it (the bitmap is 1/(8B) of the shard and stays in L2),
@@ -26,11 +26,12 @@ namespace ciera {
 
 namespace {
 
-constexpr uint64_t kFlagAgg = 1ull << 62;   // tile aggregate published
-constexpr uint64_t kFlagIncl = 2ull << 62;  // inclusive prefix published
+// A scan word: bit 62 = published, bits 61..32 = epoch of the call that
+// wrote it, bits 31..0 = value (changed blocks).
+constexpr uint64_t kFlagAgg = 1ull << 62;
 constexpr uint64_t kFlagMask = 3ull << 62;
 constexpr uint32_t kEpochMask = 0x3FFFFFFFu;  // 30-bit epoch in bits 61..32
-constexpr uint32_t kSpinLimit = 1u << 22;     // look-back waits before giving up
+constexpr uint32_t kSpinLimit = 1u << 22;     // scan waits before giving up
 
 // ------------------------------------------------------------ bit packing --
 // Four bf16 values held as two 32-bit words (a: values 0,1; b: values 2,3)
@@ -134,53 +135,87 @@ __device__ __forceinline__ uint64_t ld_status(uint64_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Decoupled look-back (run by one whole wave): publish this tile's count,
-// walk predecessors 64 at a time until an inclusive prefix is found, publish
-// the inclusive prefix, return the exclusive one. Tile ids come from the
-// ticket counter, so every predecessor is already resident and the walk ends.
-__device__ uint32_t lookback(uint64_t *status, uint32_t tile, uint32_t count,
-                             uint32_t epoch, WsCtl *ctl) {
-  const int lane = threadIdx.x & 63;
-  const uint64_t tag = uint64_t(epoch & kEpochMask) << 32;
-  if (tile == 0) {
-    if (lane == 0) st_status(&status[0], kFlagIncl | tag | count);
-    return 0u;
-  }
-  if (lane == 0) st_status(&status[tile], kFlagAgg | tag | count);
-  uint32_t excl = 0;
-  int64_t top = int64_t(tile) - 1;
-  uint32_t spins = 0;
-  while (true) {
-    const int64_t idx = top - lane;
-    const uint64_t s = idx >= 0 ? ld_status(&status[idx]) : (kFlagIncl | tag);
-    const bool ready = (s & kFlagMask) != 0 &&
-                       uint32_t((s >> 32) & kEpochMask) == (epoch & kEpochMask);
-    const bool incl = ready && (s & kFlagMask) == kFlagIncl;
-    const uint64_t im = __ballot(incl);
-    const uint64_t rm = __ballot(ready);
-    // lanes 0 .. first inclusive lane must all be ready (all 64 if none is)
-    const uint64_t need = im ? (((im & (~im + 1)) << 1) - 1) : ~0ull;
-    if ((rm & need) != need) {
+__device__ __forceinline__ bool status_ready(uint64_t s, uint32_t epoch) {
+  return (s & kFlagMask) != 0 &&
+         uint32_t((s >> 32) & kEpochMask) == (epoch & kEpochMask);
+}
+
+// Sum of the values in status words p[0, count), run by one whole wave. Each
+// word is polled until it carries the current epoch; up to 256 words are in
+// flight per round (4 per lane). A wait that exceeds the spin bound sets the
+// timeout bit and counts the missing words as 0, so the kernel always ends.
+__device__ uint32_t sum_published(uint64_t *p, uint32_t count, uint32_t epoch,
+                                  WsCtl *ctl) {
+  const uint32_t lane = threadIdx.x & 63;
+  uint32_t total = 0;
+  for (uint32_t base = 0; base < count; base += 256) {
+    uint64_t s[4];
+    bool ok[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t i = base + uint32_t(k) * 64u + lane;
+      ok[k] = i >= count;
+      s[k] = 0;
+    }
+    uint32_t spins = 0;
+    while (true) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t i = base + uint32_t(k) * 64u + lane;
+        if (!ok[k]) {
+          s[k] = ld_status(&p[i]);
+          ok[k] = status_ready(s[k], epoch);
+        }
+      }
+      const bool mine = ok[0] && ok[1] && ok[2] && ok[3];
+      if (__ballot(!mine) == 0) break;
       if (++spins > kSpinLimit) {
         if (lane == 0) set_error(ctl, CIERA_DEVERR_TIMEOUT);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
-      continue;
     }
-    const uint32_t v = ((need >> lane) & 1ull) ? uint32_t(s) : 0u;
-    excl += wave_sum(v);
-    if (im) break;
-    top -= 64;
+    uint32_t v = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t i = base + uint32_t(k) * 64u + lane;
+      if (i < count && ok[k]) v += uint32_t(s[k]);
+    }
+    total += wave_sum(v);
   }
-  if (lane == 0) st_status(&status[tile], kFlagIncl | tag | (excl + count));
-  return excl;
+  return total;
+}
+
+// Exclusive prefix of per-tile counts across the grid, run by one whole wave
+// of every tile. Two levels, so that the wait does not grow with the number
+// of tiles: a tile publishes its count, adds up the counts of the earlier
+// tiles of its group of 64, and the last tile of a group publishes the group
+// total; a tile then adds up the totals of the earlier groups. A tile waits
+// only on tiles with lower ids, and publishes before it waits on another
+// group. Workgroups are dispatched in increasing id order on every XCD, so
+// the lowest unfinished tile is always resident and can finish: the waits end.
+// (The spin bound turns any breach of that into an error bit, never a hang.)
+__device__ uint32_t tile_prefix(uint64_t *status, uint64_t *gstatus,
+                                uint32_t tile, uint32_t num_tiles,
+                                uint32_t count, uint32_t epoch, WsCtl *ctl) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t tag = uint64_t(epoch & kEpochMask) << 32;
+  const uint32_t g = tile >> 6, gbase = g << 6;
+  if (lane == 0) st_status(&status[tile], kFlagAgg | tag | count);
+  const uint32_t in_group =
+      sum_published(status + gbase, tile - gbase, epoch, ctl);
+  const bool group_last = (tile == gbase + 63u) || (tile == num_tiles - 1u);
+  if (group_last && lane == 0)
+    st_status(&gstatus[g], kFlagAgg | tag | (in_group + count));
+  return in_group + sum_published(gstatus, g, epoch, ctl);
 }
 
 // ================================================================ encode ==
-// One tile = kThreads * 8 * OCT values. Lane l of wave w handles octets
-// (w*OCT + u)*64 + l, u = 0..OCT-1, so each wave instruction covers 512
-// consecutive values (1 KiB of bf16, 512 B of exponents).
+// One tile = kThreads * 8 * OCT values; tile id = workgroup id. Lane l of
+// wave w handles octets (w*OCT + u)*64 + l, u = 0..OCT-1, so each wave
+// instruction covers 512 consecutive values (1 KiB of bf16, 512 B of
+// exponents). A whole tile issues every load before it touches any value;
+// only the ragged last tile (or unaligned input) goes element by element.
 template <int OCT, bool VEC>
 __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
   constexpr uint32_t T = kThreads * 8 * OCT;
@@ -189,23 +224,14 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
   __shared__ uint64_t s_oct[kOctWords];
   __shared__ uint64_t s_blk[kBlkWords];
   __shared__ uint32_t s_blk_pre[kBlkWords];
-  __shared__ uint32_t s_tile, s_epoch, s_prefix, s_count, s_last;
+  __shared__ uint32_t s_prefix, s_count, s_last;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid == 0) {
-    s_tile = __hip_atomic_fetch_add(&a.ctl->ticket, 1u, __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_AGENT);
-    s_epoch = __hip_atomic_load(&a.ctl->epoch, __ATOMIC_RELAXED,
-                                __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  const uint32_t tile = s_tile, epoch = s_epoch;
-  if (tile >= a.num_tiles) {
-    // only reachable with a workspace that was not prepared: do nothing that
-    // could write out of bounds, and let the error word say why
-    if (tid == 0) set_error(a.ctl, CIERA_DEVERR_TIMEOUT);
-    return;
-  }
+  const uint32_t tile = blockIdx.x;
+  // read before anything is published; consumed only after the data pass, so
+  // the load overlaps the tile's data loads
+  const uint32_t epoch = __hip_atomic_load(&a.ctl->epoch, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
   const uint64_t n = a.n;
   const uint32_t log2B = a.log2B;
   const uint32_t B = 1u << log2B;
@@ -219,25 +245,48 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
 
   // ---- pass 1: split, compare, pack sign|mantissa ----
   uint2 ev[OCT];
+  if (VEC && base + T <= n) {
+    uint4 wv[OCT];
+    uint2 cv[OCT];
 #pragma unroll
-  for (int u = 0; u < OCT; ++u) {
-    const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
-    const uint64_t elem = base + uint64_t(o) * 8u;
-    const uint32_t valid = octet_valid(elem, n);
-    bool changed = false;
-    ev[u] = make_uint2(0u, 0u);
-    if (valid) {
-      const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-      const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
+    for (int u = 0; u < OCT; ++u)
+      wv[u] = *reinterpret_cast<const uint4 *>(
+          a.w + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u)
+      cv[u] = *reinterpret_cast<const uint2 *>(
+          a.cache + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
       uint2 sm;
-      split4(wv.x, wv.y, ev[u].x, sm.x);
-      split4(wv.z, wv.w, ev[u].y, sm.y);
-      // padding values are 0 with a cached 0: never a change
-      changed = (ev[u].x != cv.x) || (ev[u].y != cv.y);
-      store_b8<VEC>(sm_out + elem, sm, valid);
+      split4(wv[u].x, wv[u].y, ev[u].x, sm.x);
+      split4(wv[u].z, wv[u].w, ev[u].y, sm.y);
+      *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
+      const uint64_t m = __ballot((ev[u].x != cv[u].x) || (ev[u].y != cv[u].y));
+      if (lane == 0) s_oct[wave * OCT + u] = m;
     }
-    const uint64_t m = __ballot(changed);
-    if (lane == 0) s_oct[wave * OCT + u] = m;
+  } else {
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
+      const uint64_t elem = base + uint64_t(o) * 8u;
+      const uint32_t valid = octet_valid(elem, n);
+      bool changed = false;
+      ev[u] = make_uint2(0u, 0u);
+      if (valid) {
+        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
+        const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
+        uint2 sm;
+        split4(wv.x, wv.y, ev[u].x, sm.x);
+        split4(wv.z, wv.w, ev[u].y, sm.y);
+        // padding values are 0 with a cached 0: never a change
+        changed = (ev[u].x != cv.x) || (ev[u].y != cv.y);
+        store_b8<VEC>(sm_out + elem, sm, valid);
+      }
+      const uint64_t m = __ballot(changed);
+      if (lane == 0) s_oct[wave * OCT + u] = m;
+    }
   }
   __syncthreads();
 
@@ -280,8 +329,17 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
   // ---- pass 3: scan across tiles (wave 0) while the other waves write the
   // tile's bitmap bytes ----
   if (wave == 0) {
-    const uint32_t excl = lookback(a.status, tile, count, epoch, a.ctl);
-    if (lane == 0) s_prefix = excl;
+    const uint32_t excl = tile_prefix(a.status, a.status + a.num_tiles, tile,
+                                      a.num_tiles, count, epoch, a.ctl);
+    if (lane == 0) {
+      s_prefix = excl;
+      // The last tile's prefix covers every other tile's published count, and
+      // a tile reads the epoch before it publishes: no tile of this call can
+      // still read the epoch, so it may advance for the next call.
+      if (tile == a.num_tiles - 1 && epoch != kEpochMask)
+        __hip_atomic_store(&a.ctl->epoch, epoch + 1u, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
   } else {
     const uint64_t byte0 = uint64_t(tile) * (nb >> 3);
     for (uint32_t i = uint32_t(tid) - 64u; i < (nb >> 3); i += kThreads - 64) {
@@ -356,30 +414,27 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
     for (uint64_t i = E + tid; i < pad16(E); i += kThreads) exc_out[i] = 0;
   }
 
-  // ---- the last tile to finish resets the ticket and advances the epoch ----
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t d = __hip_atomic_fetch_add(&a.ctl->done, 1u,
-                                              __ATOMIC_ACQ_REL,
-                                              __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (d == a.num_tiles - 1) ? 1u : 0u;
-  }
-  __syncthreads();
-  if (s_last) {
-    const uint32_t next = (epoch + 1u) & kEpochMask;
-    if (next == 0u) {
-      // epoch wrapped: no old status word may look current
+  // ---- epoch wrap: once every 2^30 calls all tiles count themselves out and
+  // the last one clears every scan word before the epoch restarts at 0 ----
+  if (epoch == kEpochMask) {
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t d = __hip_atomic_fetch_add(&a.ctl->done, 1u,
+                                                __ATOMIC_ACQ_REL,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      s_last = (d == a.num_tiles - 1) ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_last) {
       for (uint64_t i = tid; i < a.status_cap; i += kThreads)
         st_status(&a.status[i], 0ull);
       __syncthreads();
-    }
-    if (tid == 0) {
-      __hip_atomic_store(&a.ctl->ticket, 0u, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.ctl->done, 0u, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.ctl->epoch, next, __ATOMIC_RELEASE,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      if (tid == 0) {
+        __hip_atomic_store(&a.ctl->done, 0u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.ctl->epoch, 0u, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   }
 }
@@ -470,6 +525,10 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
 }
 
 // UPDATE_ONLY: the ExpCache patch alone (no sign+mantissa, no output).
+// A whole tile issues its loads in two batches (sign|mantissa bytes together
+// with the bitmap words, then one cache-or-exception load per octet, chosen
+// by address rather than by branch); the ragged last tile and unaligned
+// buffers go element by element.
 template <int OCT, bool VEC, bool UPDATE_ONLY>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   constexpr uint32_t T = kThreads * 8 * OCT;
@@ -486,12 +545,31 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   if (!sv.ok) return;
   const uint64_t n = a.n;
   if (base >= n) return;
+  const bool full = VEC && base + T <= n;
   uint8_t *const cache = a.cache + uint64_t(j) * n;
   uint16_t *const out = UPDATE_ONLY ? nullptr : a.out + uint64_t(j) * n;
 
   if (sv.mode == kModeRaw) {
     const uint16_t *body =
         reinterpret_cast<const uint16_t *>(sv.enc + kHeaderBytes);
+    if (full) {
+      uint4 wv[OCT];
+#pragma unroll
+      for (int u = 0; u < OCT; ++u)
+        wv[u] = *reinterpret_cast<const uint4 *>(
+            body + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+#pragma unroll
+      for (int u = 0; u < OCT; ++u) {
+        const uint64_t elem =
+            base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+        uint2 e, sm;
+        split4(wv[u].x, wv[u].y, e.x, sm.x);
+        split4(wv[u].z, wv[u].w, e.y, sm.y);
+        if (!UPDATE_ONLY) *reinterpret_cast<uint4 *>(out + elem) = wv[u];
+        *reinterpret_cast<uint2 *>(cache + elem) = e;
+      }
+      return;
+    }
 #pragma unroll
     for (int u = 0; u < OCT; ++u) {
       const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
@@ -519,12 +597,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   // sign|mantissa bytes first: they do not depend on the bitmap
   uint2 smv[OCT];
   if (!UPDATE_ONLY) {
+    if (full) {
 #pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
-      const uint64_t elem = base + uint64_t(o) * 8u;
-      const uint32_t valid = octet_valid(elem, n);
-      smv[u] = valid ? load_b8<true>(sm_in + elem, valid) : make_uint2(0u, 0u);
+      for (int u = 0; u < OCT; ++u)
+        smv[u] = *reinterpret_cast<const uint2 *>(
+            sm_in + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+    } else {
+#pragma unroll
+      for (int u = 0; u < OCT; ++u) {
+        const uint64_t elem =
+            base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+        const uint32_t valid = octet_valid(elem, n);
+        smv[u] =
+            valid ? load_b8<true>(sm_in + elem, valid) : make_uint2(0u, 0u);
+      }
     }
   }
 
@@ -563,35 +649,71 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   __syncthreads();
 
   bool bad = false;
+  if (full) {
+    bool ch[OCT];
+    const uint8_t *src[OCT];
 #pragma unroll
-  for (int u = 0; u < OCT; ++u) {
-    const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
-    const uint64_t elem = base + uint64_t(o) * 8u;
-    const uint32_t valid = octet_valid(elem, n);
-    if (!valid) continue;
-    const uint32_t rel = uint32_t((elem >> log2B) - (w0 << 5));
-    const uint32_t word = s_bits[rel >> 5];
-    uint2 ev;
-    if ((word >> (rel & 31u)) & 1u) {
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      const uint32_t rel = uint32_t((elem >> log2B) - (w0 << 5));
+      const uint32_t word = s_bits[rel >> 5];
+      ch[u] = (word >> (rel & 31u)) & 1u;
       const uint32_t rank =
           s_pre[rel >> 5] + __popc(word & ((1u << (rel & 31u)) - 1u));
       const uint64_t pos =
           (uint64_t(prefix + rank) << log2B) | (elem & uint64_t(B - 1u));
-      if (pos + valid > sv.E) {
+      if (ch[u] && pos + 8 > sv.E) {  // inconsistent shard: stay in bounds
         bad = true;
-        continue;
+        ch[u] = false;
       }
-      ev = load_b8<true>(exc + pos, valid);
-      store_b8<VEC>(cache + elem, ev, valid);
-    } else {
-      if (UPDATE_ONLY) continue;
-      ev = load_b8<VEC>(cache + elem, valid);
+      src[u] = ch[u] ? exc + pos : cache + elem;
     }
-    if (!UPDATE_ONLY) {
-      uint4 wv;
-      merge4(ev.x, smv[u].x, wv.x, wv.y);
-      merge4(ev.y, smv[u].y, wv.z, wv.w);
-      store_w8<VEC>(out + elem, wv, valid);
+    uint2 ev[OCT];
+#pragma unroll
+    for (int u = 0; u < OCT; ++u)
+      if (!UPDATE_ONLY || ch[u]) ev[u] = *reinterpret_cast<const uint2 *>(src[u]);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      if (ch[u]) *reinterpret_cast<uint2 *>(cache + elem) = ev[u];
+      if (!UPDATE_ONLY) {
+        uint4 wv;
+        merge4(ev[u].x, smv[u].x, wv.x, wv.y);
+        merge4(ev[u].y, smv[u].y, wv.z, wv.w);
+        *reinterpret_cast<uint4 *>(out + elem) = wv;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
+      const uint64_t elem = base + uint64_t(o) * 8u;
+      const uint32_t valid = octet_valid(elem, n);
+      if (!valid) continue;
+      const uint32_t rel = uint32_t((elem >> log2B) - (w0 << 5));
+      const uint32_t word = s_bits[rel >> 5];
+      uint2 ev;
+      if ((word >> (rel & 31u)) & 1u) {
+        const uint32_t rank =
+            s_pre[rel >> 5] + __popc(word & ((1u << (rel & 31u)) - 1u));
+        const uint64_t pos =
+            (uint64_t(prefix + rank) << log2B) | (elem & uint64_t(B - 1u));
+        if (pos + valid > sv.E) {
+          bad = true;
+          continue;
+        }
+        ev = load_b8<true>(exc + pos, valid);
+        store_b8<VEC>(cache + elem, ev, valid);
+      } else {
+        if (UPDATE_ONLY) continue;
+        ev = load_b8<VEC>(cache + elem, valid);
+      }
+      if (!UPDATE_ONLY) {
+        uint4 wv;
+        merge4(ev.x, smv[u].x, wv.x, wv.y);
+        merge4(ev.y, smv[u].y, wv.z, wv.w);
+        store_w8<VEC>(out + elem, wv, valid);
+      }
     }
   }
   if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
