@@ -42,21 +42,31 @@ constexpr uint64_t kWsCtlBytes = 256;
 // ---- tiling ----
 constexpr int kThreads = 256;  // 4 wave64 per workgroup
 // An "octet" is 8 consecutive values: 16 bytes of bf16, 8 bytes of exponent
-// or sign+mantissa. A lane handles `kOct` octets of a tile per pass.
-constexpr int kEncOct = 8;                           // encode: 16384 values
-constexpr int kEncTile = kThreads * 8 * kEncOct;
-constexpr int kEncOctWide = 16;                      // B = 4096: 32768 values
-constexpr int kEncTileWide = kThreads * 8 * kEncOctWide;
-constexpr int kDecOct = 8;                           // decode: 16384 values
-constexpr int kDecTile = kThreads * 8 * kDecOct;
+// or sign+mantissa. A lane handles OCT octets of a tile, so a tile holds
+// 2048 * OCT values. Small tiles keep many workgroups in flight, which lets
+// the load, store and scan phases of different tiles overlap.
+#ifndef CIERA_ENC_OCT
+#define CIERA_ENC_OCT 8
+#endif
+#ifndef CIERA_DEC_OCT
+#define CIERA_DEC_OCT 4
+#endif
+constexpr uint32_t kEncOctPref = CIERA_ENC_OCT;
+constexpr uint32_t kDecOct = CIERA_DEC_OCT;
+constexpr uint64_t kDecTile = uint64_t(kThreads) * 8 * kDecOct;
 
+// An encode tile writes whole bitmap bytes, so it must hold a multiple of 8
+// blocks: 2048 * OCT >= 8 * B.
+inline uint32_t enc_oct(uint32_t log2B) {
+  const uint32_t need = log2B > 8 ? (1u << (log2B - 8)) : 1u;
+  return need > kEncOctPref ? need : kEncOctPref;
+}
 inline uint64_t enc_tile_elems(uint32_t log2B) {
-  // a tile must hold whole bitmap bytes: a multiple of 8 blocks
-  return (log2B <= 11) ? uint64_t(kEncTile) : uint64_t(kEncTileWide);
+  return uint64_t(kThreads) * 8 * enc_oct(log2B);
 }
 inline uint64_t enc_tiles(uint64_t n, uint32_t log2B) {
-  uint64_t T = enc_tile_elems(log2B);
-  uint64_t t = (n + T - 1) / T;
+  const uint64_t T = enc_tile_elems(log2B);
+  const uint64_t t = (n + T - 1) / T;
   return t ? t : 1;
 }
 

@@ -728,20 +728,22 @@ __global__ void fill_zero_kernel(uint32_t *p, uint64_t words) {
 }  // namespace
 
 // ============================================================= launchers ==
-hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
+template <int OCT>
+static void launch_encode_oct(const EncArgs &a, bool vec, hipStream_t s) {
   const dim3 grid(a.num_tiles), block(kThreads);
-  if (a.log2B <= 11) {
-    if (vec)
-      hipLaunchKernelGGL((encode_kernel<kEncOct, true>), grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL((encode_kernel<kEncOct, false>), grid, block, 0, s, a);
-  } else {
-    if (vec)
-      hipLaunchKernelGGL((encode_kernel<kEncOctWide, true>), grid, block, 0, s,
-                         a);
-    else
-      hipLaunchKernelGGL((encode_kernel<kEncOctWide, false>), grid, block, 0,
-                         s, a);
+  if (vec)
+    hipLaunchKernelGGL((encode_kernel<OCT, true>), grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL((encode_kernel<OCT, false>), grid, block, 0, s, a);
+}
+
+hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
+  switch (enc_oct(a.log2B)) {
+    case 2: launch_encode_oct<2>(a, vec, s); break;
+    case 4: launch_encode_oct<4>(a, vec, s); break;
+    case 8: launch_encode_oct<8>(a, vec, s); break;
+    case 16: launch_encode_oct<16>(a, vec, s); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
@@ -768,18 +770,18 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
   const bool upd = a.out == nullptr;
   if (upd) {
     if (vec)
-      hipLaunchKernelGGL((decode_kernel<kDecOct, true, true>), grid, block, 0,
-                         s, a);
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, true>), grid,
+                         block, 0, s, a);
     else
-      hipLaunchKernelGGL((decode_kernel<kDecOct, false, true>), grid, block, 0,
-                         s, a);
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, true>), grid,
+                         block, 0, s, a);
   } else {
     if (vec)
-      hipLaunchKernelGGL((decode_kernel<kDecOct, true, false>), grid, block, 0,
-                         s, a);
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, false>), grid,
+                         block, 0, s, a);
     else
-      hipLaunchKernelGGL((decode_kernel<kDecOct, false, false>), grid, block,
-                         0, s, a);
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, false>), grid,
+                         block, 0, s, a);
   }
   return hipGetLastError();
 }
