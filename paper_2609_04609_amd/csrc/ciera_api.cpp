@@ -47,11 +47,28 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
                                uint32_t block_elems) {
   const int l = log2_block(block_elems);
   if (l < 0) return 0;
-  (void)nshards;  // decode needs only the control block at B >= 16
   const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  // one scan word per tile and one per group of 64 tiles
-  return kWsCtlBytes + 8 * (tiles + (tiles + 63) / 64 + 32);
+  // encode: one scan word per tile and one per group of 64 tiles
+  const uint64_t enc = kWsCtlBytes + 8 * (tiles + (tiles + 63) / 64 + 32);
+  // decode at B = 1: the first exception of every tile of every shard
+  const uint64_t dec =
+      l == 0 ? kWsCtlBytes + 4 * uint64_t(nshards ? nshards : 1) *
+                                 dec_tiles(n_elems) + 256
+             : kWsCtlBytes;
+  return enc > dec ? enc : dec;
 }
+
+namespace {
+bool dec_workspace_ok(uint64_t n, uint32_t nshards, int l, uint64_t bytes) {
+  if (bytes < kWsCtlBytes) return false;
+  if (l != 0) return true;
+  return (bytes - kWsCtlBytes) / 4 >= uint64_t(nshards) * dec_tiles(n);
+}
+uint32_t *tile_excl_of(void *workspace) {
+  return reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
+                                      kWsCtlBytes);
+}
+}  // namespace
 
 int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
                          hipStream_t stream) {
@@ -98,7 +115,6 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                ? CIERA_OK
                : CIERA_EHIP;
   }
-  if (l == 0) return CIERA_EUNSUPPORTED;  // element-level path: not yet built
   if (!workspace || !aligned(workspace, 8)) return CIERA_EINVAL;
   const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
   if (status_words(workspace_bytes) < tiles + (tiles + 63) / 64)
@@ -126,13 +142,13 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
                           uint64_t workspace_bytes, hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
-  if (l == 0) return CIERA_EUNSUPPORTED;
   if (!gathered || !shard_offsets || !out || !exp_cache || !workspace)
     return CIERA_EINVAL;
   if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
   if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(gathered, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
-  if (workspace_bytes < kWsCtlBytes) return CIERA_ENOSPC;
+  if (!dec_workspace_ok(shard_elems, nshards, l, workspace_bytes))
+    return CIERA_ENOSPC;
   DecArgs a;
   a.gathered = static_cast<const uint8_t *>(gathered);
   a.offsets = shard_offsets;
@@ -142,6 +158,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   a.out = out;
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
+  a.tile_excl = tile_excl_of(workspace);
   const bool vec =
       (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
@@ -152,11 +169,10 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
                        uint64_t workspace_bytes, hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
-  if (l == 0) return CIERA_EUNSUPPORTED;
   if (!encoded || (n_elems && !exp_cache) || !workspace) return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(encoded, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
-  if (workspace_bytes < kWsCtlBytes) return CIERA_ENOSPC;
+  if (!dec_workspace_ok(n_elems, 1, l, workspace_bytes)) return CIERA_ENOSPC;
   DecArgs a;
   a.gathered = static_cast<const uint8_t *>(encoded);
   a.offsets = nullptr;
@@ -166,6 +182,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   a.out = nullptr;
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
+  a.tile_excl = tile_excl_of(workspace);
   const bool vec = aligned(exp_cache, 8);
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }

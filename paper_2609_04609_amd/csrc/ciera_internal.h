@@ -92,7 +92,12 @@ struct DecArgs {
   uint16_t *out;            // nullptr for the cache-update-only pass
   uint8_t *cache;
   WsCtl *ctl;
+  uint32_t *tile_excl;      // B = 1: first exception of every decode tile
 };
+
+__host__ __device__ inline uint64_t dec_tiles(uint64_t n) {
+  return (n + kDecTile - 1) / kDecTile;
+}
 
 // Launchers (ciera_kernels.hip). Each returns the launch status.
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);

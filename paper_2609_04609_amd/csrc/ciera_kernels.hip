@@ -123,6 +123,37 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *s_red) {
   return v;
 }
 
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t t = __shfl_up(v, d, 64);
+    if (lane >= d) v += t;
+  }
+  return v;
+}
+
+// Bit i set iff byte i of a and b differ (i = 0..3).
+__device__ __forceinline__ uint32_t bytes_ne4(uint32_t a, uint32_t b) {
+  const uint32_t x = a ^ b;
+  const uint32_t m = (((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u;
+  // gather bits 7, 15, 23, 31 into bits 0..3
+  return (((m >> 7) * 0x00204081u) >> 21) & 0xFu;
+}
+
+// Byte i of an 8-byte octet held as two 32-bit words.
+__device__ __forceinline__ uint32_t octet_byte(uint2 v, uint32_t i) {
+  return ((i < 4 ? v.x : v.y) >> ((i & 3u) * 8u)) & 0xFFu;
+}
+__device__ __forceinline__ void set_octet_byte(uint2 &v, uint32_t i,
+                                               uint32_t b) {
+  const uint32_t sh = (i & 3u) * 8u;
+  if (i < 4)
+    v.x = (v.x & ~(0xFFu << sh)) | (b << sh);
+  else
+    v.y = (v.y & ~(0xFFu << sh)) | (b << sh);
+}
+
 __device__ __forceinline__ void set_error(WsCtl *ctl, uint32_t bits) {
   __hip_atomic_fetch_or(&ctl->err, bits, __ATOMIC_RELAXED,
                         __HIP_MEMORY_SCOPE_AGENT);
@@ -719,6 +750,341 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
 }
 
+// ============================================== element exceptions (B = 1) ==
+// At B = 1 the bitmap has one bit per value: octet o of the shard owns bitmap
+// byte o, and the exception list holds the changed exponent bytes in value
+// order. Within a tile the octets are ranked by a wave scan per 64-octet
+// segment and a scan of the segment totals; across tiles the two-level scan
+// (encode) or a per-shard scan of per-tile counts (decode) gives the start.
+
+// Exclusive rank of this lane's octet among the set bits of its tile, for
+// every u; returns the tile total. `cnt[u]` are the per-octet bit counts.
+template <int OCT>
+__device__ __forceinline__ uint32_t rank_octets(const uint32_t (&cnt)[OCT],
+                                                uint32_t (&excl)[OCT],
+                                                uint32_t *s_seg) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t incl[OCT];
+#pragma unroll
+  for (int u = 0; u < OCT; ++u) {
+    incl[u] = wave_incl_scan(cnt[u]);
+    if (lane == 63) s_seg[wave * OCT + u] = incl[u];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int i = 0; i < 4 * OCT; ++i) {
+      const uint32_t t = s_seg[i];
+      s_seg[i] = run;
+      run += t;
+    }
+    s_seg[4 * OCT] = run;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < OCT; ++u)
+    excl[u] = s_seg[wave * OCT + u] + incl[u] - cnt[u];
+  return s_seg[4 * OCT];
+}
+
+template <int OCT, bool VEC>
+__global__ __launch_bounds__(kThreads) void encode_elems_kernel(EncArgs a) {
+  constexpr uint32_t T = kThreads * 8 * OCT;
+  __shared__ uint32_t s_seg[4 * OCT + 1];
+  __shared__ uint32_t s_prefix, s_last;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t tile = blockIdx.x;
+  const uint32_t epoch = __hip_atomic_load(&a.ctl->epoch, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t n = a.n;
+  const uint64_t base = uint64_t(tile) * T;
+  const uint64_t n16 = pad16(n);
+  const uint64_t bm = (n + 7) / 8;
+  const uint64_t bm16 = pad16(bm);
+  uint8_t *const sm_out = a.out + kHeaderBytes;
+  uint8_t *const bmp_out = sm_out + n16;
+  uint8_t *const exc_out = bmp_out + bm16;
+
+  uint2 ev[OCT];
+  uint32_t mask[OCT], cnt[OCT];
+  if (VEC && base + T <= n) {
+    uint4 wv[OCT];
+    uint2 cv[OCT];
+#pragma unroll
+    for (int u = 0; u < OCT; ++u)
+      wv[u] = *reinterpret_cast<const uint4 *>(
+          a.w + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u)
+      cv[u] = *reinterpret_cast<const uint2 *>(
+          a.cache + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      uint2 sm;
+      split4(wv[u].x, wv[u].y, ev[u].x, sm.x);
+      split4(wv[u].z, wv[u].w, ev[u].y, sm.y);
+      *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
+      mask[u] = bytes_ne4(ev[u].x, cv[u].x) | (bytes_ne4(ev[u].y, cv[u].y) << 4);
+      bmp_out[elem >> 3] = uint8_t(mask[u]);
+      cnt[u] = __popc(mask[u]);
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      const uint32_t valid = octet_valid(elem, n);
+      ev[u] = make_uint2(0u, 0u);
+      mask[u] = 0;
+      if (valid) {
+        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
+        const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
+        uint2 sm;
+        split4(wv.x, wv.y, ev[u].x, sm.x);
+        split4(wv.z, wv.w, ev[u].y, sm.y);
+        store_b8<VEC>(sm_out + elem, sm, valid);
+        // padding values are 0 with a cached 0: never a change
+        mask[u] = bytes_ne4(ev[u].x, cv.x) | (bytes_ne4(ev[u].y, cv.y) << 4);
+        bmp_out[elem >> 3] = uint8_t(mask[u]);
+      }
+      cnt[u] = __popc(mask[u]);
+    }
+  }
+  uint32_t excl[OCT];
+  const uint32_t count = rank_octets<OCT>(cnt, excl, s_seg);
+
+  if (wave == 0) {
+    const uint32_t pre = tile_prefix(a.status, a.status + a.num_tiles, tile,
+                                     a.num_tiles, count, epoch, a.ctl);
+    if (lane == 0) {
+      s_prefix = pre;
+      if (tile == a.num_tiles - 1 && epoch != kEpochMask)
+        __hip_atomic_store(&a.ctl->epoch, epoch + 1u, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  __syncthreads();
+  const uint32_t prefix = s_prefix;
+
+  // the changed exponent bytes, in value order
+#pragma unroll
+  for (int u = 0; u < OCT; ++u) {
+    uint32_t m = mask[u];
+    uint64_t pos = uint64_t(prefix) + excl[u];
+    while (m) {
+      const uint32_t i = __builtin_ctz(m);
+      if (pos < n) exc_out[pos] = uint8_t(octet_byte(ev[u], i));
+      ++pos;
+      m &= m - 1u;
+    }
+  }
+
+  if (tile == a.num_tiles - 1) {
+    uint64_t E = uint64_t(prefix) + count;
+    if (E > n) {
+      if (tid == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+      E = n;
+    }
+    const uint64_t P = n + bm + E;
+    const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(E);
+    if (tid < 16) {
+      uint32_t v = 0;
+      switch (tid) {
+        case 0: v = kMagic; break;
+        case 1: v = kVersion | (kModeCompressed << 16); break;
+        case 2: v = 1u; break;
+        case 4: v = uint32_t(n); break;
+        case 5: v = uint32_t(n >> 32); break;
+        case 6: v = uint32_t(E); break;   // changed blocks = changed values
+        case 7: v = uint32_t(E >> 32); break;
+        case 8: v = uint32_t(E); break;
+        case 9: v = uint32_t(E >> 32); break;
+        case 10: v = uint32_t(P); break;
+        case 11: v = uint32_t(P >> 32); break;
+        case 12: v = uint32_t(total); break;
+        case 13: v = uint32_t(total >> 32); break;
+        default: v = 0; break;
+      }
+      reinterpret_cast<uint32_t *>(a.out)[tid] = v;
+    }
+    if (tid == 16 && a.out_bytes) *a.out_bytes = total;
+    for (uint64_t i = n + tid; i < n16; i += kThreads) sm_out[i] = 0;
+    for (uint64_t i = bm + tid; i < bm16; i += kThreads) bmp_out[i] = 0;
+    for (uint64_t i = E + tid; i < pad16(E); i += kThreads) exc_out[i] = 0;
+  }
+
+  if (epoch == kEpochMask) {
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t d = __hip_atomic_fetch_add(&a.ctl->done, 1u,
+                                                __ATOMIC_ACQ_REL,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      s_last = (d == a.num_tiles - 1) ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_last) {
+      for (uint64_t i = tid; i < a.status_cap; i += kThreads)
+        st_status(&a.status[i], 0ull);
+      __syncthreads();
+      if (tid == 0) {
+        __hip_atomic_store(&a.ctl->done, 0u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&a.ctl->epoch, 0u, __ATOMIC_RELEASE,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+}
+
+// Decode, B = 1, step 1: the number of set bitmap bits in every decode tile
+// of every shard (one wave per tile; raw or malformed shards count 0).
+__global__ __launch_bounds__(kThreads) void count_tile_bits_kernel(
+    DecArgs a, uint32_t tiles) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t j = blockIdx.y;
+  const uint32_t t = blockIdx.x * 4u + uint32_t(wave);
+  if (t >= tiles) return;
+  const ShardView sv = read_shard(a, j, false);
+  uint32_t c = 0;
+  if (sv.ok && sv.mode == kModeCompressed) {
+    const uint8_t *bmp = sv.enc + kHeaderBytes + pad16(a.n);
+    const uint64_t bm = (a.n + 7) / 8;
+    const uint64_t lo = uint64_t(t) * (kDecTile / 8);
+    const uint64_t hi = (lo + kDecTile / 8 < bm) ? lo + kDecTile / 8 : bm;
+    for (uint64_t i = lo + uint64_t(lane) * 16u; i < hi; i += 64u * 16u) {
+      if (i + 16 <= hi) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(bmp + i);
+        c += __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
+      } else {
+        for (uint64_t k = i; k < hi; ++k) c += __popc(uint32_t(bmp[k]));
+      }
+    }
+  }
+  c = wave_sum(c);
+  if (lane == 0) a.tile_excl[uint64_t(j) * tiles + t] = c;
+}
+
+// Decode, B = 1, step 2: exclusive scan of the tile counts of each shard, in
+// place (one workgroup per shard).
+__global__ __launch_bounds__(kThreads) void scan_tile_counts_kernel(
+    uint32_t *tile_excl, uint32_t tiles) {
+  __shared__ uint32_t s_wave[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint32_t *c = tile_excl + uint64_t(blockIdx.x) * tiles;
+  const uint32_t per = (tiles + kThreads - 1) / kThreads;
+  const uint32_t lo = tid * per;
+  const uint32_t hi = (lo + per < tiles) ? lo + per : tiles;
+  uint32_t sum = 0;
+  for (uint32_t i = lo; i < hi; ++i) sum += c[i];
+  const uint32_t incl = wave_incl_scan(sum);
+  if (lane == 63) s_wave[wave] = incl;
+  __syncthreads();
+  uint32_t run = incl - sum;
+  for (int w = 0; w < wave; ++w) run += s_wave[w];
+  for (uint32_t i = lo; i < hi; ++i) {
+    const uint32_t v = c[i];
+    c[i] = run;
+    run += v;
+  }
+}
+
+// Decode, B = 1, step 3: patch and merge (UPDATE_ONLY: patch only).
+template <int OCT, bool VEC, bool UPDATE_ONLY>
+__global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
+  constexpr uint32_t T = kThreads * 8 * OCT;
+  __shared__ uint32_t s_seg[4 * OCT + 1];
+
+  const uint32_t j = blockIdx.y;
+  const uint32_t t = blockIdx.x;
+  const uint64_t base = uint64_t(t) * T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const ShardView sv = read_shard(a, j, t == 0 && tid == 0);
+  if (!sv.ok) return;
+  const uint64_t n = a.n;
+  if (base >= n) return;
+  uint8_t *const cache = a.cache + uint64_t(j) * n;
+  uint16_t *const out = UPDATE_ONLY ? nullptr : a.out + uint64_t(j) * n;
+
+  if (sv.mode == kModeRaw) {
+    const uint16_t *body =
+        reinterpret_cast<const uint16_t *>(sv.enc + kHeaderBytes);
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      const uint32_t valid = octet_valid(elem, n);
+      if (!valid) continue;
+      const uint4 wv = load_w8<true>(body + elem, valid);
+      uint2 e, sm;
+      split4(wv.x, wv.y, e.x, sm.x);
+      split4(wv.z, wv.w, e.y, sm.y);
+      if (!UPDATE_ONLY) store_w8<VEC>(out + elem, wv, valid);
+      store_b8<VEC>(cache + elem, e, valid);
+    }
+    return;
+  }
+
+  const uint8_t *const sm_in = sv.enc + kHeaderBytes;
+  const uint8_t *const bmp = sm_in + pad16(n);
+  const uint8_t *const exc = bmp + pad16((n + 7) / 8);
+  const uint32_t tiles = uint32_t(dec_tiles(n));
+  const uint32_t tile_first = a.tile_excl[uint64_t(j) * tiles + t];
+  const bool full = VEC && base + T <= n;
+
+  uint32_t mask[OCT], cnt[OCT];
+  uint2 smv[OCT], ev[OCT];
+#pragma unroll
+  for (int u = 0; u < OCT; ++u) {
+    const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+    const uint32_t valid = full ? 8u : octet_valid(elem, n);
+    mask[u] = valid ? uint32_t(bmp[elem >> 3]) : 0u;
+    if (valid < 8) mask[u] &= (1u << valid) - 1u;
+    cnt[u] = __popc(mask[u]);
+    if (full) {
+      if (!UPDATE_ONLY) smv[u] = *reinterpret_cast<const uint2 *>(sm_in + elem);
+      ev[u] = *reinterpret_cast<const uint2 *>(cache + elem);
+    } else {
+      smv[u] = make_uint2(0u, 0u);
+      ev[u] = make_uint2(0u, 0u);
+      if (valid) {
+        if (!UPDATE_ONLY) smv[u] = load_b8<true>(sm_in + elem, valid);
+        ev[u] = load_b8<VEC>(cache + elem, valid);
+      }
+    }
+  }
+  uint32_t excl[OCT];
+  rank_octets<OCT>(cnt, excl, s_seg);
+
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < OCT; ++u) {
+    const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+    const uint32_t valid = full ? 8u : octet_valid(elem, n);
+    if (!valid) continue;
+    uint32_t m = mask[u];
+    if (m) {
+      uint64_t pos = uint64_t(tile_first) + excl[u];
+      if (pos + cnt[u] > sv.E) {
+        bad = true;
+        continue;
+      }
+      while (m) {
+        const uint32_t i = __builtin_ctz(m);
+        set_octet_byte(ev[u], i, exc[pos++]);
+        m &= m - 1u;
+      }
+      store_b8<VEC>(cache + elem, ev[u], valid);
+    }
+    if (!UPDATE_ONLY) {
+      uint4 wv;
+      merge4(ev[u].x, smv[u].x, wv.x, wv.y);
+      merge4(ev[u].y, smv[u].y, wv.z, wv.w);
+      store_w8<VEC>(out + elem, wv, valid);
+    }
+  }
+  if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+}
+
 __global__ void fill_zero_kernel(uint32_t *p, uint64_t words) {
   for (uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < words;
        i += uint64_t(gridDim.x) * blockDim.x)
@@ -738,6 +1104,16 @@ static void launch_encode_oct(const EncArgs &a, bool vec, hipStream_t s) {
 }
 
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
+  if (a.log2B == 0) {
+    const dim3 grid(a.num_tiles), block(kThreads);
+    if (vec)
+      hipLaunchKernelGGL((encode_elems_kernel<int(kEncOctPref), true>), grid,
+                         block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_elems_kernel<int(kEncOctPref), false>), grid,
+                         block, 0, s, a);
+    return hipGetLastError();
+  }
   switch (enc_oct(a.log2B)) {
     case 2: launch_encode_oct<2>(a, vec, s); break;
     case 4: launch_encode_oct<4>(a, vec, s); break;
@@ -764,10 +1140,34 @@ hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
 }
 
 hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
-  const uint64_t tiles = (a.n + kDecTile - 1) / kDecTile;
+  const uint64_t tiles = dec_tiles(a.n);
   if (tiles == 0 || a.nshards == 0) return hipSuccess;
   const dim3 grid(uint32_t(tiles), a.nshards), block(kThreads);
   const bool upd = a.out == nullptr;
+  if (a.log2B == 0) {
+    const dim3 cgrid(uint32_t((tiles + 3) / 4), a.nshards);
+    hipLaunchKernelGGL(count_tile_bits_kernel, cgrid, block, 0, s, a,
+                       uint32_t(tiles));
+    hipLaunchKernelGGL(scan_tile_counts_kernel, dim3(a.nshards), block, 0, s,
+                       a.tile_excl, uint32_t(tiles));
+    constexpr int O = int(kDecOct);
+    if (upd) {
+      if (vec)
+        hipLaunchKernelGGL((decode_elems_kernel<O, true, true>), grid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((decode_elems_kernel<O, false, true>), grid, block,
+                           0, s, a);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((decode_elems_kernel<O, true, false>), grid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((decode_elems_kernel<O, false, false>), grid,
+                           block, 0, s, a);
+    }
+    return hipGetLastError();
+  }
   if (upd) {
     if (vec)
       hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, true>), grid,

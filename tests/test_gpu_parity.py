@@ -12,7 +12,7 @@ pytestmark = pytest.mark.gpu
 # at B <= 2048, 32768 at B = 4096)
 SIZES = [1, 7, 8, 9, 100, 511, 4097, 16383, 16384, 16385, 40000,
          3 * 16384 + 17, 32768 * 3 + 8, 262147]
-BLOCKS = [16, 32, 64, 128, 512, 2048, 4096]
+BLOCKS = [1, 16, 32, 64, 128, 512, 2048, 4096]
 
 
 @pytest.fixture(scope="module")
@@ -80,10 +80,11 @@ def test_encode_edge_cases(gu, orc):
     assert ws.error() == 0
 
 
-def test_encode_unaligned_pointers(gu, orc):
+@pytest.mark.parametrize("B", [1, 64])
+def test_encode_unaligned_pointers(gu, orc, B):
     """Inputs that are not 16-byte aligned take the element-wise path."""
     from paper_2609_04609_amd import ciera
-    B, n = 64, 50001
+    n = 50001
     w_all, w2_all = gu.pair(n + 1, 31)
     w, w2 = w_all[1:], w2_all[1:]            # 2-byte offset
     cache_all = gu.dev_u8(np.concatenate(
@@ -95,11 +96,12 @@ def test_encode_unaligned_pointers(gu, orc):
     np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
 
 
-def test_encode_repeats_and_epoch_wrap(gu, orc):
+@pytest.mark.parametrize("B", [1, 512])
+def test_encode_repeats_and_epoch_wrap(gu, orc, B):
     """The workspace is reused call after call (epoch-tagged scan state); the
     bytes never change, also across the 30-bit epoch wrap."""
     from paper_2609_04609_amd import ciera
-    B, n = 512, 300000
+    n = 300000
     w, w2 = gu.pair(n, 41, c=0.001)
     cache_h, _ = orc.split(gu.host_u16(w))
     cache = gu.dev_u8(cache_h)
@@ -136,7 +138,7 @@ def _decode_case(gu, orc, R, n_s, B, raw_mask, seed):
     return gathered, offs, cache0, np.concatenate(values)
 
 
-@pytest.mark.parametrize("B", [16, 64, 512, 4096])
+@pytest.mark.parametrize("B", [1, 16, 64, 512, 4096])
 @pytest.mark.parametrize("R,n_s", [(1, 1), (3, 16385), (4, 40000),
                                    (5, 7777), (16, 16384), (2, 100003)])
 def test_decode_gathered_matches_oracle(gu, orc, B, R, n_s):
@@ -164,7 +166,7 @@ def test_decode_gathered_matches_oracle(gu, orc, B, R, n_s):
     assert ws.error() == 0
 
 
-@pytest.mark.parametrize("B", [16, 512, 4096])
+@pytest.mark.parametrize("B", [1, 16, 512, 4096])
 def test_update_cache_matches_oracle(gu, orc, B):
     from paper_2609_04609_amd import ciera
     for n, raw in [(1, False), (16385, False), (100003, False), (5000, True)]:
@@ -180,9 +182,10 @@ def test_update_cache_matches_oracle(gu, orc, B):
         assert ws.error() == 0
 
 
-def test_decode_unaligned_and_bad_shards(gu, orc):
+@pytest.mark.parametrize("B", [1, 64])
+def test_decode_unaligned_and_bad_shards(gu, orc, B):
     from paper_2609_04609_amd import ciera
-    B, R, n_s = 64, 3, 5003          # n_s % 8 != 0: element-wise stores
+    R, n_s = 3, 5003                 # n_s % 8 != 0: element-wise stores
     gathered, offs, cache0, values = _decode_case(gu, orc, R, n_s, B,
                                                   [False] * R, 555)
     cache_o = cache0.copy()
@@ -216,18 +219,20 @@ def test_decode_unaligned_and_bad_shards(gu, orc):
     torch.cuda.synchronize()
     assert ws.error() & ciera.DEVERR_ALIGN
     # a compressed shard decoded with the wrong block size
-    ciera.decode_gathered_t(g, o, n_s, 128, out2, cache2, ws)
+    ciera.decode_gathered_t(g, o, n_s, 128 if B != 128 else 64, out2, cache2,
+                            ws)
     torch.cuda.synchronize()
     assert ws.error() & ciera.DEVERR_FORMAT
 
 
-def test_round_trip_chain_on_gpu(gu, orc):
+@pytest.mark.parametrize("B", [1, 512])
+def test_round_trip_chain_on_gpu(gu, orc, B):
     """T iterations of encode -> gather -> decode entirely on the GPU: every
     shard decodes to its exact values, the sender caches (brought forward by
     ciera_update_cache) equal the receiver caches, and the oracle agrees on
     every encoded byte."""
     from paper_2609_04609_amd import ciera, synth
-    R, n, B, T = 4, 33333, 512, 4
+    R, n, T = 4, 33333, 4
     ws_e = ciera.Workspace(n, 1, B)
     ws_d = ciera.Workspace(n, R, B)
     ws = [synth.normal_bf16_bits(n, 0.02, 300 + j, "cuda") for j in range(R)]
