@@ -77,7 +77,6 @@ enum ciera_status {
 #define CIERA_DEVERR_FORMAT 0x1u   /* header magic/version/mode/n/B mismatch */
 #define CIERA_DEVERR_ALIGN 0x2u    /* a shard offset not 16-byte aligned */
 #define CIERA_DEVERR_BOUNDS 0x4u   /* bitmap flags more blocks than E holds */
-#define CIERA_DEVERR_TIMEOUT 0x8u  /* a scan step waited past its bound */
 
 /* ciera_encode flags */
 #define CIERA_ENC_RAW 0x1u /* emit the uncompressed form (first gather after

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libciera.so")
 
 OK, EINVAL, ENOSPC, EUNSUPPORTED, EFORMAT, EHIP = 0, -1, -2, -3, -4, -5
-DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS, DEVERR_TIMEOUT = 1, 2, 4, 8
+DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS = 1, 2, 4
 ENC_RAW = 0x1
 SELECT_STOP_AT_MISFIT = 0x1
 HEADER_BYTES = 64

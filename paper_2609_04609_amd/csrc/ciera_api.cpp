@@ -24,11 +24,6 @@ bool aligned(const void *p, uintptr_t a) {
   return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
 }
 
-uint64_t status_words(uint64_t workspace_bytes) {
-  return workspace_bytes > kWsCtlBytes ? (workspace_bytes - kWsCtlBytes) / 8
-                                       : 0;
-}
-
 }  // namespace
 
 extern "C" {
@@ -47,22 +42,23 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
                                uint32_t block_elems) {
   const int l = log2_block(block_elems);
   if (l < 0) return 0;
-  const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  // encode: one scan word per tile and one per group of 64 tiles
-  const uint64_t enc = kWsCtlBytes + 8 * (tiles + (tiles + 63) / 64 + 32);
-  // decode at B = 1: the first exception of every tile of every shard
+  // encode: one count per tile plus the total
+  const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n_elems, uint32_t(l)) + 1);
+  // decode at B = 1: the same per shard
   const uint64_t dec =
       l == 0 ? kWsCtlBytes + 4 * uint64_t(nshards ? nshards : 1) *
-                                 dec_tiles(n_elems) + 256
+                                 dec_count_stride(dec_tiles(n_elems))
              : kWsCtlBytes;
-  return enc > dec ? enc : dec;
+  const uint64_t need = enc > dec ? enc : dec;
+  return (need + 255) & ~uint64_t(255);
 }
 
 namespace {
 bool dec_workspace_ok(uint64_t n, uint32_t nshards, int l, uint64_t bytes) {
   if (bytes < kWsCtlBytes) return false;
   if (l != 0) return true;
-  return (bytes - kWsCtlBytes) / 4 >= uint64_t(nshards) * dec_tiles(n);
+  return (bytes - kWsCtlBytes) / 4 >=
+         uint64_t(nshards) * dec_count_stride(dec_tiles(n));
 }
 uint32_t *tile_excl_of(void *workspace) {
   return reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
@@ -72,7 +68,7 @@ uint32_t *tile_excl_of(void *workspace) {
 
 int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
                          hipStream_t stream) {
-  if (!workspace || workspace_bytes < kWsCtlBytes || !aligned(workspace, 8))
+  if (!workspace || workspace_bytes < kWsCtlBytes || !aligned(workspace, 16))
     return CIERA_EINVAL;
   return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream) ==
                  hipSuccess
@@ -115,22 +111,21 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                ? CIERA_OK
                : CIERA_EHIP;
   }
-  if (!workspace || !aligned(workspace, 8)) return CIERA_EINVAL;
+  if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
   const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  if (status_words(workspace_bytes) < tiles + (tiles + 63) / 64)
-    return CIERA_ENOSPC;
+  if (workspace_bytes < kWsCtlBytes + 4 * (tiles + 1)) return CIERA_ENOSPC;
   EncArgs a;
   a.w = w_new;
   a.cache = exp_cache;
   a.n = n_elems;
   a.log2B = uint32_t(l);
   a.num_tiles = uint32_t(tiles);
+  a.tile_elems = enc_tile_elems(uint32_t(l));
   a.out = o;
   a.out_bytes = out_bytes;
   a.ctl = static_cast<WsCtl *>(workspace);
-  a.status = reinterpret_cast<uint64_t *>(static_cast<uint8_t *>(workspace) +
+  a.counts = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
                                           kWsCtlBytes);
-  a.status_cap = status_words(workspace_bytes);
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
@@ -146,7 +141,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
     return CIERA_EINVAL;
   if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
   if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
-  if (!aligned(gathered, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
+  if (!aligned(gathered, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
   if (!dec_workspace_ok(shard_elems, nshards, l, workspace_bytes))
     return CIERA_ENOSPC;
   DecArgs a;
@@ -171,7 +166,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   if (l < 0) return CIERA_EUNSUPPORTED;
   if (!encoded || (n_elems && !exp_cache) || !workspace) return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
-  if (!aligned(encoded, 16) || !aligned(workspace, 8)) return CIERA_EINVAL;
+  if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
   if (!dec_workspace_ok(n_elems, 1, l, workspace_bytes)) return CIERA_ENOSPC;
   DecArgs a;
   a.gathered = static_cast<const uint8_t *>(encoded);

@@ -28,13 +28,11 @@ __host__ __device__ constexpr inline uint64_t bitmap_bytes(uint64_t n,
 }
 
 // ---- workspace ----
-// [0, 256): control words; [256, ...): one 64-bit scan status per encode
-// tile, or one 32-bit count per decode tile for B = 1.
+// [0, 256): control words; [256, ...): 32-bit per-tile counts (encode: one
+// per tile plus the total; decode at B = 1: the same per shard).
 struct WsCtl {
-  uint32_t err;    // sticky device error bits (CIERA_DEVERR_*)
-  uint32_t epoch;  // tags the scan words written by the current encode call
-  uint32_t done;   // tiles finished, counted only in the epoch-wrap call
-  uint32_t reserved[61];
+  uint32_t err;  // sticky device error bits (CIERA_DEVERR_*)
+  uint32_t reserved[63];
 };
 static_assert(sizeof(WsCtl) == 256, "control block is 256 bytes");
 constexpr uint64_t kWsCtlBytes = 256;
@@ -45,24 +43,18 @@ constexpr int kThreads = 256;  // 4 wave64 per workgroup
 // or sign+mantissa. A lane handles OCT octets of a tile, so a tile holds
 // 2048 * OCT values. Small tiles keep many workgroups in flight, which lets
 // the load, store and scan phases of different tiles overlap.
-#ifndef CIERA_ENC_OCT
-#define CIERA_ENC_OCT 8
-#endif
 #ifndef CIERA_DEC_OCT
 #define CIERA_DEC_OCT 4
 #endif
-constexpr uint32_t kEncOctPref = CIERA_ENC_OCT;
 constexpr uint32_t kDecOct = CIERA_DEC_OCT;
 constexpr uint64_t kDecTile = uint64_t(kThreads) * 8 * kDecOct;
 
-// An encode tile writes whole bitmap bytes, so it must hold a multiple of 8
-// blocks: 2048 * OCT >= 8 * B.
-inline uint32_t enc_oct(uint32_t log2B) {
-  const uint32_t need = log2B > 8 ? (1u << (log2B - 8)) : 1u;
-  return need > kEncOctPref ? need : kEncOctPref;
-}
+// Encode: one wave per tile. A tile is one 4096-value chunk (eight octets per
+// lane) when B <= 512, and 8 blocks (8B values, several chunks) when B > 512,
+// so that every tile owns whole bitmap bytes.
+constexpr uint64_t kEncChunk = 4096;
 inline uint64_t enc_tile_elems(uint32_t log2B) {
-  return uint64_t(kThreads) * 8 * enc_oct(log2B);
+  return log2B <= 9 ? kEncChunk : (uint64_t(8) << log2B);
 }
 inline uint64_t enc_tiles(uint64_t n, uint32_t log2B) {
   const uint64_t T = enc_tile_elems(log2B);
@@ -76,11 +68,11 @@ struct EncArgs {
   uint64_t n;
   uint32_t log2B;
   uint32_t num_tiles;
+  uint64_t tile_elems;
   uint8_t *out;
   uint64_t *out_bytes;
   WsCtl *ctl;
-  uint64_t *status;
-  uint64_t status_cap;  // status words available (for the epoch wrap clear)
+  uint32_t *counts;  // num_tiles + 1 words
 };
 
 struct DecArgs {
@@ -97,6 +89,10 @@ struct DecArgs {
 
 __host__ __device__ inline uint64_t dec_tiles(uint64_t n) {
   return (n + kDecTile - 1) / kDecTile;
+}
+// B = 1 decode: per-shard count segments (tiles + total), 16-byte aligned
+__host__ __device__ inline uint64_t dec_count_stride(uint64_t tiles) {
+  return (tiles + 1 + 3) & ~uint64_t(3);
 }
 
 // Launchers (ciera_kernels.hip). Each returns the launch status.

@@ -3,19 +3,28 @@
 // Everything here is integer byte manipulation on HBM-resident streams; the
 // roofline is HBM bandwidth, so the kernels are built around wide coalesced
 // accesses (16-byte bf16 loads, 8-byte exponent / sign+mantissa accesses per
-// lane), one pass over the data, and wave64 ballots for the per-block
+// lane), whole-tile load batches, and wave64 ballots for the per-block
 // reductions. No MFMA: nothing here is a contraction.
 //
-// Algorithm 1 (appendix of the paper) split into kernels:
-//   encode   SplitExpMant + change detection + bitmap + exception gather +
-//            payload layout, in one pass. The exception list is compacted in
-//            block order with a single-pass two-level scan over tiles (the
-//            wait is a constant number of memory round trips whatever the
-//            number of tiles).
+// Algorithm 1 (appendix of the paper) as kernels:
+//   encode   (1) encode_pass_kernel: SplitExpMant, change detection, the
+//                sign+mantissa plane, the bitmap and a changed-block count
+//                per tile, streaming at copy speed;
+//            (2) encode_exc_kernel: the exponents of the changed blocks, in
+//                block order, read back from W' for those blocks only; the
+//                header. A workgroup finds its first exception by counting
+//                the bitmap bits in front of it (the bitmap is 1/(8B) of the
+//                shard and stays in L2). At B = 1 a scan_counts_kernel over
+//                the per-tile counts stands in for that count.
+//            No workgroup ever waits on another: compacting the exception
+//            list costs one re-read of the changed blocks (2 bytes per
+//            changed value) instead of a cross-workgroup scan whose waits
+//            would hold every tile's slot behind its slowest predecessor.
 //   decode   for all R gathered shards at once: ExpCache patch + Merge. Each
 //            tile finds its first exception by counting the bitmap bits in
 //            front of it (the bitmap is 1/(8B) of the shard and stays in L2),
-//            so decode tiles never wait on each other.
+//            so decode tiles never wait on each other. At B = 1 a count and a
+//            scan kernel give every tile its first exception.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -25,13 +34,6 @@
 namespace ciera {
 
 namespace {
-
-// A scan word: bit 62 = published, bits 61..32 = epoch of the call that
-// wrote it, bits 31..0 = value (changed blocks).
-constexpr uint64_t kFlagAgg = 1ull << 62;
-constexpr uint64_t kFlagMask = 3ull << 62;
-constexpr uint32_t kEpochMask = 0x3FFFFFFFu;  // 30-bit epoch in bits 61..32
-constexpr uint32_t kSpinLimit = 1u << 22;     // scan waits before giving up
 
 // ------------------------------------------------------------ bit packing --
 // Four bf16 values held as two 32-bit words (a: values 0,1; b: values 2,3)
@@ -159,314 +161,454 @@ __device__ __forceinline__ void set_error(WsCtl *ctl, uint32_t bits) {
                         __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ void st_status(uint64_t *p, uint64_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint64_t ld_status(uint64_t *p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ bool status_ready(uint64_t s, uint32_t epoch) {
-  return (s & kFlagMask) != 0 &&
-         uint32_t((s >> 32) & kEpochMask) == (epoch & kEpochMask);
-}
-
-// Sum of the values in status words p[0, count), run by one whole wave. Each
-// word is polled until it carries the current epoch; up to 256 words are in
-// flight per round (4 per lane). A wait that exceeds the spin bound sets the
-// timeout bit and counts the missing words as 0, so the kernel always ends.
-__device__ uint32_t sum_published(uint64_t *p, uint32_t count, uint32_t epoch,
-                                  WsCtl *ctl) {
-  const uint32_t lane = threadIdx.x & 63;
-  uint32_t total = 0;
-  for (uint32_t base = 0; base < count; base += 256) {
-    uint64_t s[4];
-    bool ok[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t i = base + uint32_t(k) * 64u + lane;
-      ok[k] = i >= count;
-      s[k] = 0;
-    }
-    uint32_t spins = 0;
-    while (true) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const uint32_t i = base + uint32_t(k) * 64u + lane;
-        if (!ok[k]) {
-          s[k] = ld_status(&p[i]);
-          ok[k] = status_ready(s[k], epoch);
-        }
-      }
-      const bool mine = ok[0] && ok[1] && ok[2] && ok[3];
-      if (__ballot(!mine) == 0) break;
-      if (++spins > kSpinLimit) {
-        if (lane == 0) set_error(ctl, CIERA_DEVERR_TIMEOUT);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    uint32_t v = 0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t i = base + uint32_t(k) * 64u + lane;
-      if (i < count && ok[k]) v += uint32_t(s[k]);
-    }
-    total += wave_sum(v);
+__device__ __forceinline__ void put_header(uint8_t *out, uint32_t mode,
+                                           uint32_t B, uint64_t n,
+                                           uint64_t changed, uint64_t E,
+                                           uint64_t P, uint64_t total,
+                                           uint32_t i) {
+  if (i >= 16) return;
+  uint32_t v = 0;
+  switch (i) {
+    case 0: v = kMagic; break;
+    case 1: v = kVersion | (mode << 16); break;
+    case 2: v = B; break;
+    case 4: v = uint32_t(n); break;
+    case 5: v = uint32_t(n >> 32); break;
+    case 6: v = uint32_t(changed); break;
+    case 7: v = uint32_t(changed >> 32); break;
+    case 8: v = uint32_t(E); break;
+    case 9: v = uint32_t(E >> 32); break;
+    case 10: v = uint32_t(P); break;
+    case 11: v = uint32_t(P >> 32); break;
+    case 12: v = uint32_t(total); break;
+    case 13: v = uint32_t(total >> 32); break;
+    default: v = 0; break;
   }
-  return total;
+  reinterpret_cast<uint32_t *>(out)[i] = v;
 }
 
-// Exclusive prefix of per-tile counts across the grid, run by one whole wave
-// of every tile. Two levels, so that the wait does not grow with the number
-// of tiles: a tile publishes its count, adds up the counts of the earlier
-// tiles of its group of 64, and the last tile of a group publishes the group
-// total; a tile then adds up the totals of the earlier groups. A tile waits
-// only on tiles with lower ids, and publishes before it waits on another
-// group. Workgroups are dispatched in increasing id order on every XCD, so
-// the lowest unfinished tile is always resident and can finish: the waits end.
-// (The spin bound turns any breach of that into an error bit, never a hang.)
-__device__ uint32_t tile_prefix(uint64_t *status, uint64_t *gstatus,
-                                uint32_t tile, uint32_t num_tiles,
-                                uint32_t count, uint32_t epoch, WsCtl *ctl) {
-  const uint32_t lane = threadIdx.x & 63;
-  const uint64_t tag = uint64_t(epoch & kEpochMask) << 32;
-  const uint32_t g = tile >> 6, gbase = g << 6;
-  if (lane == 0) st_status(&status[tile], kFlagAgg | tag | count);
-  const uint32_t in_group =
-      sum_published(status + gbase, tile - gbase, epoch, ctl);
-  const bool group_last = (tile == gbase + 63u) || (tile == num_tiles - 1u);
-  if (group_last && lane == 0)
-    st_status(&gstatus[g], kFlagAgg | tag | (in_group + count));
-  return in_group + sum_published(gstatus, g, epoch, ctl);
+// Select x[i] for a lane-varying i < N (N small, x uniform). Written as mask
+// arithmetic so that the compiler keeps x in registers instead of turning
+// the choice into an indexed load from scratch memory.
+template <int N>
+__device__ __forceinline__ uint64_t pick(const uint64_t (&x)[N], uint32_t i) {
+  uint64_t r = 0;
+#pragma unroll
+  for (int k = 0; k < N; ++k)
+    r |= x[k] & (0ull - uint64_t(i == uint32_t(k)));
+  return r;
 }
 
 // ================================================================ encode ==
-// One tile = kThreads * 8 * OCT values; tile id = workgroup id. Lane l of
-// wave w handles octets (w*OCT + u)*64 + l, u = 0..OCT-1, so each wave
-// instruction covers 512 consecutive values (1 KiB of bf16, 512 B of
-// exponents). A whole tile issues every load before it touches any value;
-// only the ragged last tile (or unaligned input) goes element by element.
-template <int OCT, bool VEC>
-__global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
-  constexpr uint32_t T = kThreads * 8 * OCT;
-  constexpr uint32_t kOctWords = T / 512;   // octet change bits, 64 per word
-  constexpr uint32_t kBlkWords = T / 1024;  // block flags at B >= 16
-  __shared__ uint64_t s_oct[kOctWords];
-  __shared__ uint64_t s_blk[kBlkWords];
-  __shared__ uint32_t s_blk_pre[kBlkWords];
-  __shared__ uint32_t s_prefix, s_count, s_last;
+// A tile belongs to one wave (tile id = 4 * workgroup + wave) and holds
+// kEncTile = 4096 values, or 8 blocks when B > 512, so that a tile owns whole
+// bitmap bytes. Lane l handles octets u*64 + l (u = 0..7) of each 4096-value
+// chunk: wave instruction u covers values [512u, 512u + 512) of the chunk.
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint32_t tile = blockIdx.x;
-  // read before anything is published; consumed only after the data pass, so
-  // the load overlaps the tile's data loads
-  const uint32_t epoch = __hip_atomic_load(&a.ctl->epoch, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
+// Pass 1. Everything but the exception list.
+template <bool VEC, bool ELEMS>
+__global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t tile = blockIdx.x * 4u + (threadIdx.x >> 6);
+  if (tile >= a.num_tiles) return;
   const uint64_t n = a.n;
   const uint32_t log2B = a.log2B;
-  const uint32_t B = 1u << log2B;
-  const uint64_t base = uint64_t(tile) * T;
+  const uint64_t T = a.tile_elems;
+  const uint64_t tbase = uint64_t(tile) * T;
   const uint64_t n16 = pad16(n);
   const uint64_t bm = bitmap_bytes(n, log2B);
   const uint64_t bm16 = pad16(bm);
   uint8_t *const sm_out = a.out + kHeaderBytes;
   uint8_t *const bmp_out = sm_out + n16;
-  uint8_t *const exc_out = bmp_out + bm16;
 
-  // ---- pass 1: split, compare, pack sign|mantissa ----
-  uint2 ev[OCT];
-  if (VEC && base + T <= n) {
-    uint4 wv[OCT];
-    uint2 cv[OCT];
+  uint32_t count = 0;
+  uint64_t fw[4] = {0ull, 0ull, 0ull, 0ull};  // block flags, B <= 512
+  uint32_t fbyte = 0;                          // block flags, B > 512
+  for (uint64_t cbase = tbase; cbase < tbase + T; cbase += kEncChunk) {
+    uint32_t mask[8];  // change bits of the lane's octets
+    if (VEC && cbase + kEncChunk <= n) {
+      uint4 wv[8];
+      uint2 cv[8];
 #pragma unroll
-    for (int u = 0; u < OCT; ++u)
-      wv[u] = *reinterpret_cast<const uint4 *>(
-          a.w + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+      for (int u = 0; u < 8; ++u)
+        wv[u] = *reinterpret_cast<const uint4 *>(
+            a.w + cbase + (uint64_t(u) * 64 + lane) * 8);
 #pragma unroll
-    for (int u = 0; u < OCT; ++u)
-      cv[u] = *reinterpret_cast<const uint2 *>(
-          a.cache + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+      for (int u = 0; u < 8; ++u)
+        cv[u] = *reinterpret_cast<const uint2 *>(
+            a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
 #pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-      uint2 sm;
-      split4(wv[u].x, wv[u].y, ev[u].x, sm.x);
-      split4(wv[u].z, wv[u].w, ev[u].y, sm.y);
-      *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
-      const uint64_t m = __ballot((ev[u].x != cv[u].x) || (ev[u].y != cv[u].y));
-      if (lane == 0) s_oct[wave * OCT + u] = m;
-    }
-  } else {
-#pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
-      const uint64_t elem = base + uint64_t(o) * 8u;
-      const uint32_t valid = octet_valid(elem, n);
-      bool changed = false;
-      ev[u] = make_uint2(0u, 0u);
-      if (valid) {
-        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-        const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
-        uint2 sm;
-        split4(wv.x, wv.y, ev[u].x, sm.x);
-        split4(wv.z, wv.w, ev[u].y, sm.y);
-        // padding values are 0 with a cached 0: never a change
-        changed = (ev[u].x != cv.x) || (ev[u].y != cv.y);
-        store_b8<VEC>(sm_out + elem, sm, valid);
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
+        uint2 e, sm;
+        split4(wv[u].x, wv[u].y, e.x, sm.x);
+        split4(wv[u].z, wv[u].w, e.y, sm.y);
+        *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
+        mask[u] = ELEMS ? (bytes_ne4(e.x, cv[u].x) |
+                           (bytes_ne4(e.y, cv[u].y) << 4))
+                        : uint32_t((e.x != cv[u].x) || (e.y != cv[u].y));
       }
-      const uint64_t m = __ballot(changed);
-      if (lane == 0) s_oct[wave * OCT + u] = m;
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
+        const uint32_t valid = octet_valid(elem, n);
+        mask[u] = 0;
+        if (valid) {
+          const uint4 wv = load_w8<VEC>(a.w + elem, valid);
+          const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
+          uint2 e, sm;
+          split4(wv.x, wv.y, e.x, sm.x);
+          split4(wv.z, wv.w, e.y, sm.y);
+          store_b8<VEC>(sm_out + elem, sm, valid);
+          // padding values are 0 with a cached 0: never a change
+          mask[u] = ELEMS ? (bytes_ne4(e.x, cv.x) | (bytes_ne4(e.y, cv.y) << 4))
+                          : uint32_t((e.x != cv.x) || (e.y != cv.y));
+        }
+      }
     }
-  }
-  __syncthreads();
-
-  // ---- pass 2: block flags (B/8 octets per block) ----
-  const uint32_t opb_log2 = log2B - 3;
-  const uint32_t nb = T >> log2B;        // blocks per tile, multiple of 8
-  const uint32_t nbw = (nb + 63) >> 6;   // flag words in use
-  for (uint32_t b0 = 0; b0 < nb; b0 += kThreads) {
-    const uint32_t b = b0 + tid;
-    bool f = false;
-    if (b < nb) {
-      const uint32_t o0 = b << opb_log2;
-      if (opb_log2 >= 6) {
-        const uint32_t w0 = o0 >> 6, nw = 1u << (opb_log2 - 6);
-        uint64_t acc = 0;
-        for (uint32_t i = 0; i < nw; ++i) acc |= s_oct[w0 + i];
-        f = acc != 0;
+    if (ELEMS) {
+      // an octet's change byte is its bitmap byte
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
+        if (elem < n) bmp_out[elem >> 3] = uint8_t(mask[u]);
+        count += __popc(mask[u]);
+      }
+    } else {
+      uint64_t m[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) m[u] = __ballot(mask[u] != 0);
+      if (log2B <= 9) {
+        // 512/B blocks per 512-value unit, B/8 octets (bits of m[u]) each
+        const uint32_t opb_log2 = log2B - 3;
+        const uint32_t bpu_log2 = 6 - opb_log2;
+        const uint64_t gmask =
+            opb_log2 == 6 ? ~0ull : ((1ull << (1u << opb_log2)) - 1ull);
+        const uint32_t nb = kEncChunk >> log2B;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const uint32_t b = uint32_t(k) * 64u + lane;
+          bool f = false;
+          if (b < nb) {
+            const uint64_t word = pick<8>(m, b >> bpu_log2);
+            const uint32_t sh = (b & ((1u << bpu_log2) - 1u)) << opb_log2;
+            f = ((word >> sh) & gmask) != 0;
+          }
+          fw[k] = __ballot(f);
+        }
       } else {
-        const uint64_t word = s_oct[o0 >> 6];
-        const uint64_t mask = (1ull << (1u << opb_log2)) - 1ull;
-        f = ((word >> (o0 & 63u)) & mask) != 0;
+        // a block spans 2^(log2B-9) units; the tile holds 8 blocks
+        const uint32_t u0 = uint32_t((cbase - tbase) >> 9);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (m[u]) fbyte |= 1u << ((u0 + uint32_t(u)) >> (log2B - 9));
       }
     }
-    const uint64_t m = __ballot(f);
-    const uint32_t widx = (b0 >> 6) + uint32_t(wave);
-    if (lane == 0 && widx < nbw) s_blk[widx] = m;
   }
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t run = 0;
-    for (uint32_t i = 0; i < nbw; ++i) {
-      s_blk_pre[i] = run;
-      run += uint32_t(__popcll(s_blk[i]));
-    }
-    s_count = run;
-  }
-  __syncthreads();
-  const uint32_t count = s_count;
 
-  // ---- pass 3: scan across tiles (wave 0) while the other waves write the
-  // tile's bitmap bytes ----
-  if (wave == 0) {
-    const uint32_t excl = tile_prefix(a.status, a.status + a.num_tiles, tile,
-                                      a.num_tiles, count, epoch, a.ctl);
-    if (lane == 0) {
-      s_prefix = excl;
-      // The last tile's prefix covers every other tile's published count, and
-      // a tile reads the epoch before it publishes: no tile of this call can
-      // still read the epoch, so it may advance for the next call.
-      if (tile == a.num_tiles - 1 && epoch != kEpochMask)
-        __hip_atomic_store(&a.ctl->epoch, epoch + 1u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    }
-  } else {
-    const uint64_t byte0 = uint64_t(tile) * (nb >> 3);
-    for (uint32_t i = uint32_t(tid) - 64u; i < (nb >> 3); i += kThreads - 64) {
+  if (ELEMS) {
+    count = wave_sum(count);
+  } else if (log2B <= 9) {
+    const uint32_t nbytes = uint32_t(kEncChunk >> log2B) >> 3;
+    const uint64_t byte0 = uint64_t(tile) * nbytes;
+    for (uint32_t i = lane; i < nbytes; i += 64) {
       const uint64_t pos = byte0 + i;
-      if (pos < bm16) bmp_out[pos] = uint8_t(s_blk[i >> 3] >> ((i & 7u) * 8u));
+      if (pos < bm16)
+        bmp_out[pos] = uint8_t(pick<4>(fw, i >> 3) >> ((i & 7u) * 8u));
     }
-  }
-  __syncthreads();
-  const uint32_t prefix = s_prefix;
-
-  // ---- pass 4: the changed blocks' exponents, at (rank * B + offset) ----
 #pragma unroll
-  for (int u = 0; u < OCT; ++u) {
-    const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
-    const uint64_t elem = base + uint64_t(o) * 8u;
-    const uint32_t valid = octet_valid(elem, n);
-    if (!valid) continue;
-    const uint32_t bl = (o << 3) >> log2B;
-    const uint64_t word = s_blk[bl >> 6];
-    if ((word >> (bl & 63u)) & 1ull) {
-      const uint32_t rank =
-          s_blk_pre[bl >> 6] +
-          uint32_t(__popcll(word & ((1ull << (bl & 63u)) - 1ull)));
+    for (int k = 0; k < 4; ++k) count += uint32_t(__popcll(fw[k]));
+  } else {
+    if (lane == 0 && tile < bm16) bmp_out[tile] = uint8_t(fbyte);
+    count = __popc(fbyte);
+  }
+  if (ELEMS && lane == 0) a.counts[tile] = count;
+
+  // the last tile zeroes the padding of the first two sections, before the
+  // exception pass reads the bitmap back
+  if (tile == a.num_tiles - 1) {
+    for (uint64_t i = n + lane; i < n16; i += 64) sm_out[i] = 0;
+    uint64_t written = bm;
+    if (!ELEMS)
+      written = log2B <= 9 ? uint64_t(a.num_tiles) * ((kEncChunk >> log2B) >> 3)
+                           : uint64_t(a.num_tiles);
+    if (written > bm16) written = bm16;
+    for (uint64_t i = written + lane; i < bm16; i += 64) bmp_out[i] = 0;
+  }
+}
+
+// Exclusive scan of `count` 32-bit counts per segment, in place, one
+// 1024-thread workgroup per segment (segment j starts at c + j * stride, a
+// 16-byte aligned address); the segment's total goes to c[count]. Each pass
+// covers 16384 counts: 16 per thread, loaded as four 16-byte vectors.
+constexpr int kScanThreads = 1024;
+constexpr uint32_t kScanPer = 16;
+
+__global__ __launch_bounds__(kScanThreads) void scan_counts_kernel(
+    uint32_t *counts, uint32_t count, uint64_t stride) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  __shared__ uint32_t s_total;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  uint32_t *c = counts + uint64_t(blockIdx.x) * stride;
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < count; base += kScanThreads * kScanPer) {
+    const uint32_t lo = base + tid * kScanPer;
+    uint32_t v[kScanPer];
+    if (lo + kScanPer <= count) {
+#pragma unroll
+      for (uint32_t q = 0; q < kScanPer / 4; ++q) {
+        const uint4 x = *reinterpret_cast<const uint4 *>(c + lo + 4 * q);
+        v[4 * q] = x.x;
+        v[4 * q + 1] = x.y;
+        v[4 * q + 2] = x.z;
+        v[4 * q + 3] = x.w;
+      }
+    } else {
+#pragma unroll
+      for (uint32_t i = 0; i < kScanPer; ++i)
+        v[i] = lo + i < count ? c[lo + i] : 0u;
+    }
+    uint32_t sum = 0;
+#pragma unroll
+    for (uint32_t i = 0; i < kScanPer; ++i) {
+      const uint32_t t = v[i];
+      v[i] = sum;  // exclusive within the thread
+      sum += t;
+    }
+    const uint32_t incl = wave_incl_scan(sum);
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t run = 0;
+      for (int w = 0; w < kScanThreads / 64; ++w) {
+        const uint32_t t = s_wave[w];
+        s_wave[w] = run;
+        run += t;
+      }
+      s_total = run;
+    }
+    __syncthreads();
+    const uint32_t off = carry + s_wave[wave] + incl - sum;
+    if (lo + kScanPer <= count) {
+#pragma unroll
+      for (uint32_t q = 0; q < kScanPer / 4; ++q)
+        *reinterpret_cast<uint4 *>(c + lo + 4 * q) =
+            make_uint4(off + v[4 * q], off + v[4 * q + 1], off + v[4 * q + 2],
+                       off + v[4 * q + 3]);
+    } else {
+#pragma unroll
+      for (uint32_t i = 0; i < kScanPer; ++i)
+        if (lo + i < count) c[lo + i] = off + v[i];
+    }
+    carry += s_total;
+    __syncthreads();
+  }
+  if (tid == 0) c[count] = carry;
+}
+
+// Pass 2. The exceptions of the tile's changed blocks (B >= 16) or changed
+// values (B = 1), at the tile's offset in the list; the last tile writes the
+// header. W' is read again only where the bitmap says so.
+//
+// Offsets at B >= 16: the bitmap is 1/(8B) of the shard, so a workgroup
+// counts the flagged blocks in front of its first tile straight from it (an
+// L2 read) and each wave adds the flags of the sibling tiles before it. The
+// re-read of W' depends only on the tile's own flags, so it is issued before
+// that count and the two overlap. At B = 1 the offsets come from the scanned
+// per-tile counts.
+template <bool VEC, bool ELEMS>
+__global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
+  __shared__ uint32_t s_red[4];
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t tile = blockIdx.x * 4u + wave;
+  const bool live = tile < a.num_tiles;
+  const uint64_t n = a.n;
+  const uint32_t log2B = a.log2B;
+  const uint32_t B = 1u << log2B;
+  const uint64_t T = a.tile_elems;
+  const uint64_t tbase = uint64_t(tile) * T;
+  const uint64_t n16 = pad16(n);
+  const uint64_t bm = bitmap_bytes(n, log2B);
+  const uint64_t bm16 = pad16(bm);
+  const uint8_t *const bmp = a.out + kHeaderBytes + n16;
+  uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
+  // bitmap bytes per tile (B >= 16)
+  const uint64_t per_tile = log2B <= 9 ? (kEncChunk >> log2B) >> 3 : 1u;
+
+  // flagged blocks in bitmap bytes [lo, hi) (clipped to the bitmap), summed
+  // over the whole wave
+  auto wave_popc = [&](uint64_t lo, uint64_t hi) -> uint32_t {
+    if (hi > bm) hi = bm;
+    uint32_t c = 0;
+    for (uint64_t i = lo + lane; i < hi; i += 64) c += __popc(uint32_t(bmp[i]));
+    return wave_sum(c);
+  };
+  // flagged blocks in front of this workgroup's first tile (all threads)
+  auto group_prefix = [&](uint64_t before) -> uint32_t {
+    if (before > bm) before = bm;
+    uint32_t cnt = 0;
+    const uint64_t full16 = before >> 4;
+    const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
+    for (uint64_t i = threadIdx.x; i < full16; i += kThreads) {
+      const uint4 v = b4[i];
+      cnt += __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
+    }
+    for (uint64_t i = (full16 << 4) + threadIdx.x; i < before; i += kThreads)
+      cnt += __popc(uint32_t(bmp[i]));
+    return block_sum(cnt, s_red);
+  };
+
+  uint32_t prefix = 0;
+  if (ELEMS) {
+    if (!live) return;
+    prefix = a.counts[tile];
+    uint32_t mask[8], excl[8];
+    uint32_t run = 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
+      const uint32_t valid = octet_valid(elem, n);
+      mask[u] = valid ? uint32_t(bmp[elem >> 3]) & ((1u << valid) - 1u) : 0u;
+      const uint32_t c = __popc(mask[u]);
+      const uint32_t incl = wave_incl_scan(c);
+      excl[u] = run + incl - c;
+      run += __shfl(incl, 63, 64);
+    }
+    uint4 wv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
+      if (mask[u]) wv[u] = load_w8<VEC>(a.w + elem, octet_valid(elem, n));
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      uint32_t mm = mask[u];
+      if (!mm) continue;
+      uint2 e, sm;
+      split4(wv[u].x, wv[u].y, e.x, sm.x);
+      split4(wv[u].z, wv[u].w, e.y, sm.y);
+      uint64_t pos = uint64_t(prefix) + excl[u];
+      while (mm) {
+        const uint32_t i = __builtin_ctz(mm);
+        if (pos < n) exc_out[pos] = uint8_t(octet_byte(e, i));
+        ++pos;
+        mm &= mm - 1u;
+      }
+    }
+  } else if (log2B <= 9) {
+    // (1) the tile's own flags, as one to four 64-bit words, never reading
+    // past the zero-padded bitmap (the exception section behind it is being
+    // written by other tiles)
+    const uint32_t nbytes = uint32_t(per_tile);
+    const uint64_t byte0 = uint64_t(tile) * nbytes;
+    uint64_t fw[4] = {0ull, 0ull, 0ull, 0ull};
+    if (live) {
+      const uint64_t lim = bm16 > byte0 ? bm16 - byte0 : 0;
+      const uint32_t have = nbytes < lim ? nbytes : uint32_t(lim);
+      if (have == nbytes && nbytes >= 8) {
+        // byte0 is a multiple of nbytes, so 8-byte aligned
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          if (uint32_t(k) * 8u < nbytes)
+            fw[k] = *reinterpret_cast<const uint64_t *>(bmp + byte0 + 8u * k);
+      } else {
+        for (uint32_t i = 0; i < have; ++i)
+          fw[i >> 3] |= uint64_t(bmp[byte0 + i]) << (8u * (i & 7u));
+      }
+    }
+    // (2) W' of the changed octets
+    bool ch[8];
+    uint4 wv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t o = uint32_t(u) * 64u + lane;
+      const uint64_t elem = tbase + uint64_t(o) * 8;
+      const uint32_t bl = (o << 3) >> log2B;
+      ch[u] = live && elem < n && ((pick<4>(fw, bl >> 6) >> (bl & 63u)) & 1ull);
+      if (ch[u]) wv[u] = load_w8<VEC>(a.w + elem, octet_valid(elem, n));
+    }
+    // (3) the offset, overlapping the loads above
+    const uint32_t sib =
+        wave_popc(uint64_t(blockIdx.x) * 4u * per_tile, byte0);
+    prefix = group_prefix(uint64_t(blockIdx.x) * 4u * per_tile);
+    if (!live) return;
+    prefix += sib;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (!ch[u]) continue;
+      const uint32_t o = uint32_t(u) * 64u + lane;
+      const uint64_t elem = tbase + uint64_t(o) * 8;
+      const uint32_t valid = octet_valid(elem, n);
+      const uint32_t bl = (o << 3) >> log2B;
+      const uint64_t word = pick<4>(fw, bl >> 6);
+      uint32_t rank = uint32_t(__popcll(word & ((1ull << (bl & 63u)) - 1ull)));
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (uint32_t(k) < (bl >> 6)) rank += uint32_t(__popcll(fw[k]));
       const uint64_t pos =
           (uint64_t(prefix + rank) << log2B) | ((o << 3) & (B - 1u));
-      if (pos + valid <= n) store_b8<VEC>(exc_out + pos, ev[u], valid);
+      uint2 e, sm;
+      split4(wv[u].x, wv[u].y, e.x, sm.x);
+      split4(wv[u].z, wv[u].w, e.y, sm.y);
+      if (pos + valid <= n) store_b8<VEC>(exc_out + pos, e, valid);
+    }
+  } else {
+    // 8 blocks of B > 512 values; the wave copies each changed block's
+    // exponents 512 values at a time
+    const uint32_t sib = wave_popc(uint64_t(blockIdx.x) * 4u, tile);
+    prefix = group_prefix(uint64_t(blockIdx.x) * 4u);
+    if (!live) return;
+    prefix += sib;
+    const uint32_t fbyte = tile < bm ? bmp[tile] : 0u;
+    uint32_t rank = 0;
+    for (uint32_t k = 0; k < 8; ++k) {
+      if (!((fbyte >> k) & 1u)) continue;
+      const uint64_t bbase = tbase + (uint64_t(k) << log2B);
+      const uint64_t dst = uint64_t(prefix + rank) << log2B;
+      for (uint32_t c = 0; c < B; c += 512) {
+        const uint64_t elem = bbase + c + uint64_t(lane) * 8;
+        const uint32_t valid = octet_valid(elem, n);
+        if (!valid) continue;
+        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
+        uint2 e, sm;
+        split4(wv.x, wv.y, e.x, sm.x);
+        split4(wv.z, wv.w, e.y, sm.y);
+        const uint64_t pos = dst + c + uint64_t(lane) * 8;
+        if (pos + valid <= n) store_b8<VEC>(exc_out + pos, e, valid);
+      }
+      ++rank;
     }
   }
 
-  // ---- the last tile knows the totals: header, padding, size ----
-  if (tile == a.num_tiles - 1) {
-    const uint64_t nblk = blocks_of(n, log2B);
-    const uint64_t changed_blocks = uint64_t(prefix) + count;
-    uint64_t E = changed_blocks << log2B;
-    if (nblk) {
-      const uint32_t lb = uint32_t((nblk - 1) - uint64_t(tile) * nb);
-      const bool last_changed = (s_blk[lb >> 6] >> (lb & 63u)) & 1ull;
-      const uint64_t len_last = n - ((nblk - 1) << log2B);
-      if (last_changed) E -= (uint64_t(B) - len_last);
+  // ---- the last tile knows the totals: header, exception padding, size ----
+  const uint32_t last = a.num_tiles - 1;
+  if (tile == last) {
+    const uint64_t total_changed =
+        ELEMS ? uint64_t(a.counts[a.num_tiles])
+              : uint64_t(prefix) +
+                    wave_popc(uint64_t(last) * per_tile,
+                              uint64_t(last) * per_tile + per_tile);
+    uint64_t E = total_changed;
+    if (!ELEMS) {
+      E = total_changed << log2B;
+      const uint64_t nblk = blocks_of(n, log2B);
+      if (nblk) {
+        const uint64_t lb = nblk - 1;
+        const bool last_changed = (bmp[lb >> 3] >> (lb & 7u)) & 1u;
+        const uint64_t len_last = n - (lb << log2B);
+        if (last_changed) E -= (uint64_t(B) - len_last);
+      }
     }
-    if (E > n) {  // only with a corrupted scan state
-      if (tid == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+    if (E > n) {  // only with a count array that was written by someone else
+      if (lane == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
       E = n;
     }
     const uint64_t P = n + bm + E;
     const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(E);
-    if (tid < 16) {
-      uint32_t v = 0;
-      switch (tid) {
-        case 0: v = kMagic; break;
-        case 1: v = kVersion | (kModeCompressed << 16); break;
-        case 2: v = B; break;
-        case 4: v = uint32_t(n); break;
-        case 5: v = uint32_t(n >> 32); break;
-        case 6: v = uint32_t(changed_blocks); break;
-        case 7: v = uint32_t(changed_blocks >> 32); break;
-        case 8: v = uint32_t(E); break;
-        case 9: v = uint32_t(E >> 32); break;
-        case 10: v = uint32_t(P); break;
-        case 11: v = uint32_t(P >> 32); break;
-        case 12: v = uint32_t(total); break;
-        case 13: v = uint32_t(total >> 32); break;
-        default: v = 0; break;
-      }
-      reinterpret_cast<uint32_t *>(a.out)[tid] = v;
-    }
-    if (tid == 16 && a.out_bytes) *a.out_bytes = total;
-    // zero padding of the three sections
-    for (uint64_t i = n + tid; i < n16; i += kThreads) sm_out[i] = 0;
-    const uint64_t bm_written = uint64_t(tile + 1) * (nb >> 3);
-    for (uint64_t i = bm_written + tid; i < bm16; i += kThreads) bmp_out[i] = 0;
-    for (uint64_t i = E + tid; i < pad16(E); i += kThreads) exc_out[i] = 0;
-  }
-
-  // ---- epoch wrap: once every 2^30 calls all tiles count themselves out and
-  // the last one clears every scan word before the epoch restarts at 0 ----
-  if (epoch == kEpochMask) {
-    __syncthreads();
-    if (tid == 0) {
-      const uint32_t d = __hip_atomic_fetch_add(&a.ctl->done, 1u,
-                                                __ATOMIC_ACQ_REL,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (d == a.num_tiles - 1) ? 1u : 0u;
-    }
-    __syncthreads();
-    if (s_last) {
-      for (uint64_t i = tid; i < a.status_cap; i += kThreads)
-        st_status(&a.status[i], 0ull);
-      __syncthreads();
-      if (tid == 0) {
-        __hip_atomic_store(&a.ctl->done, 0u, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&a.ctl->epoch, 0u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
+    put_header(a.out, kModeCompressed, B, n, total_changed, E, P, total, lane);
+    if (lane == 16 && a.out_bytes) *a.out_bytes = total;
+    for (uint64_t i = E + lane; i < pad16(E); i += 64) exc_out[i] = 0;
   }
 }
 
@@ -485,23 +627,8 @@ __global__ __launch_bounds__(kThreads) void encode_raw_kernel(
     store_w8<VEC>(body + elem, load_w8<VEC>(w + elem, valid), valid);
   }
   if (blockIdx.x == 0) {
-    const int tid = threadIdx.x;
-    if (tid < 16) {
-      uint32_t v = 0;
-      switch (tid) {
-        case 0: v = kMagic; break;
-        case 1: v = kVersion | (kModeRaw << 16); break;
-        case 2: v = B; break;
-        case 4: v = uint32_t(n); break;
-        case 5: v = uint32_t(n >> 32); break;
-        case 10: v = uint32_t(2 * n); break;
-        case 11: v = uint32_t((2 * n) >> 32); break;
-        case 12: v = uint32_t(total); break;
-        case 13: v = uint32_t(total >> 32); break;
-        default: v = 0; break;
-      }
-      reinterpret_cast<uint32_t *>(out)[tid] = v;
-    }
+    const uint32_t tid = threadIdx.x;
+    put_header(out, kModeRaw, B, n, 0, 0, 2 * n, total, tid);
     if (tid == 16 && out_bytes) *out_bytes = total;
     uint8_t *bytes = out + kHeaderBytes;
     for (uint64_t i = 2 * n + tid; i < pad16(2 * n); i += kThreads) bytes[i] = 0;
@@ -753,9 +880,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
 // ============================================== element exceptions (B = 1) ==
 // At B = 1 the bitmap has one bit per value: octet o of the shard owns bitmap
 // byte o, and the exception list holds the changed exponent bytes in value
-// order. Within a tile the octets are ranked by a wave scan per 64-octet
-// segment and a scan of the segment totals; across tiles the two-level scan
-// (encode) or a per-shard scan of per-tile counts (decode) gives the start.
+// order (the encoder is encode_wave_kernel<..., true>). Within a decode tile
+// the octets are ranked by a wave scan per 64-octet segment and a scan of the
+// segment totals; a per-shard scan of per-tile counts gives the tile start.
 
 // Exclusive rank of this lane's octet among the set bits of its tile, for
 // every u; returns the tile total. `cnt[u]` are the per-octet bit counts.
@@ -787,156 +914,6 @@ __device__ __forceinline__ uint32_t rank_octets(const uint32_t (&cnt)[OCT],
   return s_seg[4 * OCT];
 }
 
-template <int OCT, bool VEC>
-__global__ __launch_bounds__(kThreads) void encode_elems_kernel(EncArgs a) {
-  constexpr uint32_t T = kThreads * 8 * OCT;
-  __shared__ uint32_t s_seg[4 * OCT + 1];
-  __shared__ uint32_t s_prefix, s_last;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint32_t tile = blockIdx.x;
-  const uint32_t epoch = __hip_atomic_load(&a.ctl->epoch, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t n = a.n;
-  const uint64_t base = uint64_t(tile) * T;
-  const uint64_t n16 = pad16(n);
-  const uint64_t bm = (n + 7) / 8;
-  const uint64_t bm16 = pad16(bm);
-  uint8_t *const sm_out = a.out + kHeaderBytes;
-  uint8_t *const bmp_out = sm_out + n16;
-  uint8_t *const exc_out = bmp_out + bm16;
-
-  uint2 ev[OCT];
-  uint32_t mask[OCT], cnt[OCT];
-  if (VEC && base + T <= n) {
-    uint4 wv[OCT];
-    uint2 cv[OCT];
-#pragma unroll
-    for (int u = 0; u < OCT; ++u)
-      wv[u] = *reinterpret_cast<const uint4 *>(
-          a.w + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
-#pragma unroll
-    for (int u = 0; u < OCT; ++u)
-      cv[u] = *reinterpret_cast<const uint2 *>(
-          a.cache + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
-#pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-      uint2 sm;
-      split4(wv[u].x, wv[u].y, ev[u].x, sm.x);
-      split4(wv[u].z, wv[u].w, ev[u].y, sm.y);
-      *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
-      mask[u] = bytes_ne4(ev[u].x, cv[u].x) | (bytes_ne4(ev[u].y, cv[u].y) << 4);
-      bmp_out[elem >> 3] = uint8_t(mask[u]);
-      cnt[u] = __popc(mask[u]);
-    }
-  } else {
-#pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-      const uint32_t valid = octet_valid(elem, n);
-      ev[u] = make_uint2(0u, 0u);
-      mask[u] = 0;
-      if (valid) {
-        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-        const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
-        uint2 sm;
-        split4(wv.x, wv.y, ev[u].x, sm.x);
-        split4(wv.z, wv.w, ev[u].y, sm.y);
-        store_b8<VEC>(sm_out + elem, sm, valid);
-        // padding values are 0 with a cached 0: never a change
-        mask[u] = bytes_ne4(ev[u].x, cv.x) | (bytes_ne4(ev[u].y, cv.y) << 4);
-        bmp_out[elem >> 3] = uint8_t(mask[u]);
-      }
-      cnt[u] = __popc(mask[u]);
-    }
-  }
-  uint32_t excl[OCT];
-  const uint32_t count = rank_octets<OCT>(cnt, excl, s_seg);
-
-  if (wave == 0) {
-    const uint32_t pre = tile_prefix(a.status, a.status + a.num_tiles, tile,
-                                     a.num_tiles, count, epoch, a.ctl);
-    if (lane == 0) {
-      s_prefix = pre;
-      if (tile == a.num_tiles - 1 && epoch != kEpochMask)
-        __hip_atomic_store(&a.ctl->epoch, epoch + 1u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
-  __syncthreads();
-  const uint32_t prefix = s_prefix;
-
-  // the changed exponent bytes, in value order
-#pragma unroll
-  for (int u = 0; u < OCT; ++u) {
-    uint32_t m = mask[u];
-    uint64_t pos = uint64_t(prefix) + excl[u];
-    while (m) {
-      const uint32_t i = __builtin_ctz(m);
-      if (pos < n) exc_out[pos] = uint8_t(octet_byte(ev[u], i));
-      ++pos;
-      m &= m - 1u;
-    }
-  }
-
-  if (tile == a.num_tiles - 1) {
-    uint64_t E = uint64_t(prefix) + count;
-    if (E > n) {
-      if (tid == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
-      E = n;
-    }
-    const uint64_t P = n + bm + E;
-    const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(E);
-    if (tid < 16) {
-      uint32_t v = 0;
-      switch (tid) {
-        case 0: v = kMagic; break;
-        case 1: v = kVersion | (kModeCompressed << 16); break;
-        case 2: v = 1u; break;
-        case 4: v = uint32_t(n); break;
-        case 5: v = uint32_t(n >> 32); break;
-        case 6: v = uint32_t(E); break;   // changed blocks = changed values
-        case 7: v = uint32_t(E >> 32); break;
-        case 8: v = uint32_t(E); break;
-        case 9: v = uint32_t(E >> 32); break;
-        case 10: v = uint32_t(P); break;
-        case 11: v = uint32_t(P >> 32); break;
-        case 12: v = uint32_t(total); break;
-        case 13: v = uint32_t(total >> 32); break;
-        default: v = 0; break;
-      }
-      reinterpret_cast<uint32_t *>(a.out)[tid] = v;
-    }
-    if (tid == 16 && a.out_bytes) *a.out_bytes = total;
-    for (uint64_t i = n + tid; i < n16; i += kThreads) sm_out[i] = 0;
-    for (uint64_t i = bm + tid; i < bm16; i += kThreads) bmp_out[i] = 0;
-    for (uint64_t i = E + tid; i < pad16(E); i += kThreads) exc_out[i] = 0;
-  }
-
-  if (epoch == kEpochMask) {
-    __syncthreads();
-    if (tid == 0) {
-      const uint32_t d = __hip_atomic_fetch_add(&a.ctl->done, 1u,
-                                                __ATOMIC_ACQ_REL,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (d == a.num_tiles - 1) ? 1u : 0u;
-    }
-    __syncthreads();
-    if (s_last) {
-      for (uint64_t i = tid; i < a.status_cap; i += kThreads)
-        st_status(&a.status[i], 0ull);
-      __syncthreads();
-      if (tid == 0) {
-        __hip_atomic_store(&a.ctl->done, 0u, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&a.ctl->epoch, 0u, __ATOMIC_RELEASE,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-  }
-}
-
 // Decode, B = 1, step 1: the number of set bitmap bits in every decode tile
 // of every shard (one wave per tile; raw or malformed shards count 0).
 __global__ __launch_bounds__(kThreads) void count_tile_bits_kernel(
@@ -962,31 +939,7 @@ __global__ __launch_bounds__(kThreads) void count_tile_bits_kernel(
     }
   }
   c = wave_sum(c);
-  if (lane == 0) a.tile_excl[uint64_t(j) * tiles + t] = c;
-}
-
-// Decode, B = 1, step 2: exclusive scan of the tile counts of each shard, in
-// place (one workgroup per shard).
-__global__ __launch_bounds__(kThreads) void scan_tile_counts_kernel(
-    uint32_t *tile_excl, uint32_t tiles) {
-  __shared__ uint32_t s_wave[4];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint32_t *c = tile_excl + uint64_t(blockIdx.x) * tiles;
-  const uint32_t per = (tiles + kThreads - 1) / kThreads;
-  const uint32_t lo = tid * per;
-  const uint32_t hi = (lo + per < tiles) ? lo + per : tiles;
-  uint32_t sum = 0;
-  for (uint32_t i = lo; i < hi; ++i) sum += c[i];
-  const uint32_t incl = wave_incl_scan(sum);
-  if (lane == 63) s_wave[wave] = incl;
-  __syncthreads();
-  uint32_t run = incl - sum;
-  for (int w = 0; w < wave; ++w) run += s_wave[w];
-  for (uint32_t i = lo; i < hi; ++i) {
-    const uint32_t v = c[i];
-    c[i] = run;
-    run += v;
-  }
+  if (lane == 0) a.tile_excl[uint64_t(j) * dec_count_stride(tiles) + t] = c;
 }
 
 // Decode, B = 1, step 3: patch and merge (UPDATE_ONLY: patch only).
@@ -1028,7 +981,8 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
   const uint8_t *const bmp = sm_in + pad16(n);
   const uint8_t *const exc = bmp + pad16((n + 7) / 8);
   const uint32_t tiles = uint32_t(dec_tiles(n));
-  const uint32_t tile_first = a.tile_excl[uint64_t(j) * tiles + t];
+  const uint32_t tile_first =
+      a.tile_excl[uint64_t(j) * dec_count_stride(tiles) + t];
   const bool full = VEC && base + T <= n;
 
   uint32_t mask[OCT], cnt[OCT];
@@ -1094,32 +1048,35 @@ __global__ void fill_zero_kernel(uint32_t *p, uint64_t words) {
 }  // namespace
 
 // ============================================================= launchers ==
-template <int OCT>
-static void launch_encode_oct(const EncArgs &a, bool vec, hipStream_t s) {
-  const dim3 grid(a.num_tiles), block(kThreads);
-  if (vec)
-    hipLaunchKernelGGL((encode_kernel<OCT, true>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((encode_kernel<OCT, false>), grid, block, 0, s, a);
-}
-
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
-  if (a.log2B == 0) {
-    const dim3 grid(a.num_tiles), block(kThreads);
+  const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
+  const bool elems = a.log2B == 0;
+  if (elems) {
     if (vec)
-      hipLaunchKernelGGL((encode_elems_kernel<int(kEncOctPref), true>), grid,
-                         block, 0, s, a);
+      hipLaunchKernelGGL((encode_pass_kernel<true, true>), grid, block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_elems_kernel<int(kEncOctPref), false>), grid,
-                         block, 0, s, a);
-    return hipGetLastError();
+      hipLaunchKernelGGL((encode_pass_kernel<false, true>), grid, block, 0, s, a);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((encode_pass_kernel<true, false>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_pass_kernel<false, false>), grid, block, 0, s, a);
   }
-  switch (enc_oct(a.log2B)) {
-    case 2: launch_encode_oct<2>(a, vec, s); break;
-    case 4: launch_encode_oct<4>(a, vec, s); break;
-    case 8: launch_encode_oct<8>(a, vec, s); break;
-    case 16: launch_encode_oct<16>(a, vec, s); break;
-    default: return hipErrorInvalidValue;
+  if (elems)
+    hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
+                       a.counts, a.num_tiles, uint64_t(0));
+  if (elems) {
+    if (vec)
+      hipLaunchKernelGGL((encode_exc_kernel<true, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_exc_kernel<false, true>), grid, block, 0, s, a);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((encode_exc_kernel<true, false>), grid, block, 0, s,
+                         a);
+    else
+      hipLaunchKernelGGL((encode_exc_kernel<false, false>), grid, block, 0, s,
+                         a);
   }
   return hipGetLastError();
 }
@@ -1148,8 +1105,9 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
     const dim3 cgrid(uint32_t((tiles + 3) / 4), a.nshards);
     hipLaunchKernelGGL(count_tile_bits_kernel, cgrid, block, 0, s, a,
                        uint32_t(tiles));
-    hipLaunchKernelGGL(scan_tile_counts_kernel, dim3(a.nshards), block, 0, s,
-                       a.tile_excl, uint32_t(tiles));
+    hipLaunchKernelGGL(scan_counts_kernel, dim3(a.nshards),
+                       dim3(kScanThreads), 0, s, a.tile_excl, uint32_t(tiles),
+                       dec_count_stride(tiles));
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
