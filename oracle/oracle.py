@@ -40,42 +40,33 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
-_lib = None
-
-
-def _load():
-    global _lib
-    if _lib is None:
-        if not os.path.exists(_LIB):
-            build(force=True)
-        lib = ctypes.CDLL(_LIB)
-        lib.oracle_encoded_bound.restype = ctypes.c_uint64
-        lib.oracle_encoded_bound.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
-        lib.oracle_split.restype = None
-        lib.oracle_split.argtypes = [_u16p, ctypes.c_uint64, _u8p, _u8p]
-        lib.oracle_encode.restype = ctypes.c_uint64
-        lib.oracle_encode.argtypes = [_u16p, _u8p, ctypes.c_uint64,
-                                      ctypes.c_uint64, ctypes.c_int, _u8p,
-                                      ctypes.c_uint64]
-        lib.oracle_decode.restype = ctypes.c_int
-        lib.oracle_decode.argtypes = [_u8p, ctypes.c_uint64, _u8p, _u16p]
-        lib.oracle_decode_gathered.restype = ctypes.c_int
-        lib.oracle_decode_gathered.argtypes = [_u8p, _u64p, ctypes.c_uint64,
-                                               ctypes.c_uint64, _u16p, _u8p]
-        lib.oracle_update_cache.restype = ctypes.c_int
-        lib.oracle_update_cache.argtypes = [_u8p, _u8p, ctypes.c_uint64]
-        lib.oracle_gain.restype = ctypes.c_double
-        lib.oracle_gain.argtypes = [ctypes.c_uint64, ctypes.c_uint64,
-                                    ctypes.c_double, ctypes.c_uint64,
-                                    ctypes.c_double, ctypes.c_double,
-                                    ctypes.c_double, ctypes.c_double,
-                                    ctypes.c_double, ctypes.c_int,
-                                    ctypes.c_double]
-        lib.oracle_select.restype = ctypes.c_uint64
-        lib.oracle_select.argtypes = [_f64p, _f64p, ctypes.c_uint64,
-                                      ctypes.c_double, ctypes.c_int, _u8p]
-        _lib = lib
-    return _lib
+def _bind(lib):
+    lib.oracle_encoded_bound.restype = ctypes.c_uint64
+    lib.oracle_encoded_bound.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+    lib.oracle_split.restype = None
+    lib.oracle_split.argtypes = [_u16p, ctypes.c_uint64, _u8p, _u8p]
+    lib.oracle_encode.restype = ctypes.c_uint64
+    lib.oracle_encode.argtypes = [_u16p, _u8p, ctypes.c_uint64,
+                                  ctypes.c_uint64, ctypes.c_int, _u8p,
+                                  ctypes.c_uint64]
+    lib.oracle_decode.restype = ctypes.c_int
+    lib.oracle_decode.argtypes = [_u8p, ctypes.c_uint64, _u8p, _u16p]
+    lib.oracle_decode_gathered.restype = ctypes.c_int
+    lib.oracle_decode_gathered.argtypes = [_u8p, _u64p, ctypes.c_uint64,
+                                           ctypes.c_uint64, _u16p, _u8p]
+    lib.oracle_update_cache.restype = ctypes.c_int
+    lib.oracle_update_cache.argtypes = [_u8p, _u8p, ctypes.c_uint64]
+    lib.oracle_gain.restype = ctypes.c_double
+    lib.oracle_gain.argtypes = [ctypes.c_uint64, ctypes.c_uint64,
+                                ctypes.c_double, ctypes.c_uint64,
+                                ctypes.c_double, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_double,
+                                ctypes.c_double, ctypes.c_int,
+                                ctypes.c_double]
+    lib.oracle_select.restype = ctypes.c_uint64
+    lib.oracle_select.argtypes = [_f64p, _f64p, ctypes.c_uint64,
+                                  ctypes.c_double, ctypes.c_int, _u8p]
+    return lib
 
 
 def _ptr(a: np.ndarray, typ):
@@ -83,94 +74,150 @@ def _ptr(a: np.ndarray, typ):
     return a.ctypes.data_as(typ)
 
 
-def encoded_bound(n: int, B: int) -> int:
-    return int(_load().oracle_encoded_bound(n, B))
+class Oracle:
+    """The oracle's functions bound to one compiled library (the default one,
+    or a copy built from another source, as the mutation tests do)."""
+
+    def __init__(self, lib_path: str):
+        self._lib = _bind(ctypes.CDLL(lib_path))
+
+    def encoded_bound(self, n: int, B: int) -> int:
+        return int(self._lib.oracle_encoded_bound(n, B))
+
+    def split(self, w: np.ndarray):
+        """Algorithm 1 SplitExpMant: (exponent bytes, sign+mantissa bytes)."""
+        w = np.ascontiguousarray(w, dtype=np.uint16)
+        e = np.empty(w.size, np.uint8)
+        sm = np.empty(w.size, np.uint8)
+        self._lib.oracle_split(_ptr(w, _u16p), w.size, _ptr(e, _u8p),
+                               _ptr(sm, _u8p))
+        return e, sm
+
+    def encode(self, w: np.ndarray, cache, B: int,
+               raw: bool = False) -> np.ndarray:
+        """Encode one shard; returns the encoded bytes (exactly ``total``
+        long). The output buffer starts filled with 0xA5, so a byte the
+        oracle forgets to write shows up."""
+        w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
+        n = w.size
+        cap = self.encoded_bound(n, B)
+        out = np.full(cap, 0xA5, np.uint8)
+        if cache is None:
+            cptr = ctypes.cast(None, _u8p)
+        else:
+            cache = np.ascontiguousarray(cache, dtype=np.uint8).ravel()
+            assert cache.size == n
+            cptr = _ptr(cache, _u8p)
+        total = self._lib.oracle_encode(_ptr(w, _u16p), cptr, n, B, int(raw),
+                                        _ptr(out, _u8p), cap)
+        if total == 0 or total > cap:
+            raise ValueError("oracle_encode rejected its arguments")
+        return out[:total].copy()
+
+    def decode(self, enc: np.ndarray, n: int, cache: np.ndarray):
+        """Decode one shard; ``cache`` is updated in place. Returns values."""
+        enc = np.ascontiguousarray(enc, dtype=np.uint8)
+        assert cache.dtype == np.uint8 and cache.flags["C_CONTIGUOUS"]
+        out = np.empty(n, np.uint16)
+        rc = self._lib.oracle_decode(_ptr(enc, _u8p), n, _ptr(cache, _u8p),
+                                     _ptr(out, _u16p))
+        if rc:
+            raise ValueError(f"oracle_decode: bad shard ({rc})")
+        return out
+
+    def decode_gathered(self, gathered: np.ndarray, offsets, n_s: int,
+                        cache: np.ndarray):
+        gathered = np.ascontiguousarray(gathered, dtype=np.uint8)
+        offs = np.ascontiguousarray(offsets, dtype=np.uint64)
+        R = offs.size
+        assert cache.size == R * n_s and cache.flags["C_CONTIGUOUS"]
+        out = np.empty(R * n_s, np.uint16)
+        rc = self._lib.oracle_decode_gathered(
+            _ptr(gathered, _u8p), _ptr(offs, _u64p), R, n_s,
+            _ptr(out, _u16p), _ptr(cache, _u8p))
+        if rc:
+            raise ValueError(f"oracle_decode_gathered: bad shard ({rc})")
+        return out
+
+    def update_cache(self, cache: np.ndarray, enc: np.ndarray, n: int):
+        enc = np.ascontiguousarray(enc, dtype=np.uint8)
+        assert cache.dtype == np.uint8 and cache.flags["C_CONTIGUOUS"]
+        rc = self._lib.oracle_update_cache(_ptr(cache, _u8p), _ptr(enc, _u8p),
+                                           n)
+        if rc:
+            raise ValueError(f"oracle_update_cache: bad shard ({rc})")
+
+    def gain(self, n: int, B: int, q: float, R: int, alpha_s: float,
+             bus_bw_Bps: float, t_hash_s: float = 0.0, t_cmp_s: float = 0.0,
+             t_decmp_s: float = 0.0, overlapped: bool = True,
+             header_bytes: float = HEADER_BYTES) -> float:
+        return float(self._lib.oracle_gain(n, B, q, R, alpha_s, bus_bw_Bps,
+                                           t_hash_s, t_cmp_s, t_decmp_s,
+                                           int(overlapped), header_bytes))
+
+    def should_compress(self, *args, **kw) -> bool:
+        """Section 3.2: keep a shard only when its gain is positive."""
+        return self.gain(*args, **kw) > 0.0
+
+    def select(self, gains, mems, budget: float,
+               stop_at_first_misfit: bool = False):
+        g = np.ascontiguousarray(gains, dtype=np.float64)
+        m = np.ascontiguousarray(mems, dtype=np.float64)
+        sel = np.zeros(g.size, np.uint8)
+        self._lib.oracle_select(_ptr(g, _f64p), _ptr(m, _f64p), g.size,
+                                budget, int(stop_at_first_misfit),
+                                _ptr(sel, _u8p))
+        return sel.astype(bool)
+
+    header = staticmethod(lambda enc: header(enc))
 
 
-def split(w: np.ndarray):
-    """Algorithm 1 SplitExpMant: (exponent bytes, sign+mantissa bytes)."""
-    w = np.ascontiguousarray(w, dtype=np.uint16)
-    e = np.empty(w.size, np.uint8)
-    sm = np.empty(w.size, np.uint8)
-    _load().oracle_split(_ptr(w, _u16p), w.size, _ptr(e, _u8p), _ptr(sm, _u8p))
-    return e, sm
+_default = None
 
 
-def encode(w: np.ndarray, cache: np.ndarray | None, B: int,
-           raw: bool = False) -> np.ndarray:
-    """Encode one shard; returns the encoded bytes (exactly ``total`` long)."""
-    w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
-    n = w.size
-    cap = encoded_bound(n, B)
-    out = np.empty(cap, np.uint8)
-    if cache is None:
-        cptr = ctypes.cast(None, _u8p)
-    else:
-        cache = np.ascontiguousarray(cache, dtype=np.uint8).ravel()
-        assert cache.size == n
-        cptr = _ptr(cache, _u8p)
-    total = _load().oracle_encode(_ptr(w, _u16p), cptr, n, B, int(raw),
-                                  _ptr(out, _u8p), cap)
-    if total == 0:
-        raise ValueError("oracle_encode rejected its arguments")
-    return out[:total].copy()
+def _oracle() -> Oracle:
+    global _default
+    if _default is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        _default = Oracle(_LIB)
+    return _default
 
 
-def decode(enc: np.ndarray, n: int, cache: np.ndarray):
-    """Decode one shard; ``cache`` is updated in place. Returns the values."""
-    enc = np.ascontiguousarray(enc, dtype=np.uint8)
-    assert cache.dtype == np.uint8 and cache.flags["C_CONTIGUOUS"]
-    out = np.empty(n, np.uint16)
-    rc = _load().oracle_decode(_ptr(enc, _u8p), n, _ptr(cache, _u8p),
-                               _ptr(out, _u16p))
-    if rc:
-        raise ValueError(f"oracle_decode: bad shard ({rc})")
-    return out
+def encoded_bound(n, B):
+    return _oracle().encoded_bound(n, B)
 
 
-def decode_gathered(gathered: np.ndarray, offsets, n_s: int,
-                    cache: np.ndarray):
-    gathered = np.ascontiguousarray(gathered, dtype=np.uint8)
-    offs = np.ascontiguousarray(offsets, dtype=np.uint64)
-    R = offs.size
-    assert cache.size == R * n_s and cache.flags["C_CONTIGUOUS"]
-    out = np.empty(R * n_s, np.uint16)
-    rc = _load().oracle_decode_gathered(_ptr(gathered, _u8p), _ptr(offs, _u64p),
-                                        R, n_s, _ptr(out, _u16p),
-                                        _ptr(cache, _u8p))
-    if rc:
-        raise ValueError(f"oracle_decode_gathered: bad shard ({rc})")
-    return out
+def split(w):
+    return _oracle().split(w)
 
 
-def update_cache(cache: np.ndarray, enc: np.ndarray, n: int) -> None:
-    enc = np.ascontiguousarray(enc, dtype=np.uint8)
-    assert cache.dtype == np.uint8 and cache.flags["C_CONTIGUOUS"]
-    rc = _load().oracle_update_cache(_ptr(cache, _u8p), _ptr(enc, _u8p), n)
-    if rc:
-        raise ValueError(f"oracle_update_cache: bad shard ({rc})")
+def encode(w, cache, B, raw=False):
+    return _oracle().encode(w, cache, B, raw)
 
 
-def gain(n: int, B: int, q: float, R: int, alpha_s: float, bus_bw_Bps: float,
-         t_hash_s: float = 0.0, t_cmp_s: float = 0.0, t_decmp_s: float = 0.0,
-         overlapped: bool = True, header_bytes: float = HEADER_BYTES) -> float:
-    return float(_load().oracle_gain(n, B, q, R, alpha_s, bus_bw_Bps, t_hash_s,
-                                     t_cmp_s, t_decmp_s, int(overlapped),
-                                     header_bytes))
+def decode(enc, n, cache):
+    return _oracle().decode(enc, n, cache)
 
 
-def should_compress(*args, **kw) -> bool:
-    """Section 3.2: keep a shard only when its gain is positive."""
-    return gain(*args, **kw) > 0.0
+def decode_gathered(gathered, offsets, n_s, cache):
+    return _oracle().decode_gathered(gathered, offsets, n_s, cache)
 
 
-def select(gains, mems, budget: float, stop_at_first_misfit: bool = False):
-    g = np.ascontiguousarray(gains, dtype=np.float64)
-    m = np.ascontiguousarray(mems, dtype=np.float64)
-    sel = np.zeros(g.size, np.uint8)
-    _load().oracle_select(_ptr(g, _f64p), _ptr(m, _f64p), g.size, budget,
-                          int(stop_at_first_misfit), _ptr(sel, _u8p))
-    return sel.astype(bool)
+def update_cache(cache, enc, n):
+    return _oracle().update_cache(cache, enc, n)
+
+
+def gain(*args, **kw):
+    return _oracle().gain(*args, **kw)
+
+
+def should_compress(*args, **kw):
+    return _oracle().should_compress(*args, **kw)
+
+
+def select(gains, mems, budget, stop_at_first_misfit=False):
+    return _oracle().select(gains, mems, budget, stop_at_first_misfit)
 
 
 # ---- header fields, read straight from the bytes (no oracle arithmetic) ----

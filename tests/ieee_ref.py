@@ -14,10 +14,16 @@ def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
     return b.view(np.float32)
 
 
+def _to_f64(bits):
+    # signalling-NaN patterns raise a harmless "invalid" flag in the cast
+    with np.errstate(invalid="ignore"):
+        return bf16_to_f32(bits).astype(np.float64)
+
+
 def exponent_field(bits: np.ndarray) -> np.ndarray:
     """Biased 8-bit exponent: 0 for zero and subnormals, 255 for Inf/NaN,
     otherwise floor(log2|x|) + 127 (frexp returns |m| in [0.5, 1))."""
-    x = bf16_to_f32(bits).astype(np.float64)
+    x = _to_f64(bits)
     out = np.zeros(x.shape, np.int64)
     special = ~np.isfinite(x)
     out[special] = 255
@@ -36,7 +42,7 @@ def mantissa7(bits: np.ndarray) -> np.ndarray:
     """The 7 stored fraction bits of finite values, from the magnitude:
     normal |x| = (1 + m/128) 2^(e-127), subnormal |x| = (m/128) 2^-126.
     Non-finite values return -1 (their payload is not a magnitude)."""
-    x = bf16_to_f32(bits).astype(np.float64)
+    x = _to_f64(bits)
     out = np.full(x.shape, -1, np.int64)
     fin = np.isfinite(x)
     ax = np.abs(np.where(fin, x, 0.0))

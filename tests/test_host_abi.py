@@ -166,6 +166,10 @@ def test_select_ranking_hand_case(cl, orc):
     assert cl.ciera_select(g2, m2, 2e6, cl.SELECT_STOP_AT_MISFIT) == [
         True, False, False]
     assert list(orc.select(g2, m2, 2e6, True)) == [True, False, False]
+    # a zero gain is no gain, even where the budget has room for it
+    g3, m3 = [2e-3, 0.0, -0.0], [1e6, 1e6, 1e6]
+    assert cl.ciera_select(g3, m3, 5e6) == [True, False, False]
+    assert list(orc.select(g3, m3, 5e6)) == [True, False, False]
     rng = np.random.default_rng(9)
     for _ in range(50):
         k = int(rng.integers(1, 30))

@@ -1,0 +1,231 @@
+"""Do the pins catch plausible mistakes in the oracle?
+
+Each case plants one mistake in a copy of oracle/ciera_oracle.c (on the CPU
+only), builds it with gcc, and runs a condensed set of the pins against it:
+IEEE-semantics field extraction, brute force over old exponents, the
+hand-worked wire fixtures, closed-form sizes and zero padding, the raw form,
+a hand-computed gain and a hand-ranked selection. Every mutant must fail at
+least one of them; the real oracle must pass all of them.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from tests import ieee_ref
+from tests.test_oracle_pins import _read_golden
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "ciera_oracle.c")
+
+# (name, text in the source, planted replacement)
+MUTANTS = [
+    ("exponent shift", "uint8_t expo = (uint8_t)((x >> 7) & 0xFFu);",
+     "uint8_t expo = (uint8_t)((x >> 8) & 0xFFu);"),
+    ("sign bit position", "sm[k] = (uint8_t)((sign << 7) | mant);",
+     "sm[k] = (uint8_t)((sign << 6) | mant);"),
+    ("mantissa mask", "uint8_t mant = (uint8_t)(x & 0x7Fu);",
+     "uint8_t mant = (uint8_t)(x & 0x3Fu);"),
+    ("merge drops the sign", "return (uint16_t)((sign << 15) | ((uint16_t)expo << 7) | mant);",
+     "return (uint16_t)(((uint16_t)expo << 7) | mant);"),
+    ("change test ignores decreases", "if (expo[k] != cache[k]) {",
+     "if (expo[k] > cache[k]) {"),
+    ("bitmap bit order", "bitmap[b / 8u] = (uint8_t)(bitmap[b / 8u] | (1u << (b % 8u)));",
+     "bitmap[b / 8u] = (uint8_t)(bitmap[b / 8u] | (0x80u >> (b % 8u)));"),
+    ("last partial block dropped", "  uint64_t nblk = num_blocks(n, B);\n  uint8_t *changed",
+     "  uint64_t nblk = n / B;\n  uint8_t *changed"),
+    ("exceptions of the first element only", "for (uint64_t k = lo; k < hi; k++) exc[E++] = expo[k];",
+     "for (uint64_t k = lo; k < lo + 1; k++) exc[E++] = expo[k];"),
+    ("bitmap size floors", "return ceil_div(num_blocks(n, B), 8u);",
+     "return num_blocks(n, B) / 8u;"),
+    ("padding rounds wrong", "static uint64_t round16(uint64_t x) { return (x + 15u) / 16u * 16u; }",
+     "static uint64_t round16(uint64_t x) { return (x + 16u) / 16u * 16u; }"),
+    ("payload omits the bitmap", "uint64_t P = n + bm + E;", "uint64_t P = n + E;"),
+    ("header swaps E and count", "put_u64(out + 32, E);", "put_u64(out + 32, changed);"),
+    ("padding left unwritten", "  memset(out, 0, total);\n  write_header(out, OR_MODE_COMPRESSED",
+     "  write_header(out, OR_MODE_COMPRESSED"),
+    ("decode patches only the first value of a block",
+     "for (uint64_t k = lo; k < hi; k++) cache[k] = exc[j++];",
+     "cache[lo] = exc[j]; j += hi - lo;"),
+    ("raw cache from the wrong field", "cache[k] = (uint8_t)((x >> 7) & 0xFFu);\n    }\n    return 0;\n  }\n  patch_cache",
+     "cache[k] = (uint8_t)((x >> 6) & 0xFFu);\n    }\n    return 0;\n  }\n  patch_cache"),
+    ("raw decode seeds the wrong field",
+     "      out[k] = x;\n      cache[k] = (uint8_t)((x >> 7) & 0xFFu);",
+     "      out[k] = x;\n      cache[k] = (uint8_t)((x >> 8) & 0xFFu);"),
+    ("decode skips the patch", "  if (E > 0) patch_cache(enc, n, B, cache);",
+     "  if (E > n) patch_cache(enc, n, B, cache);"),
+    ("gain counts R hops", "double comm_raw = alpha_s + (double)(R - 1) * S / bw_Bps;",
+     "double comm_raw = alpha_s + (double)R * S / bw_Bps;"),
+    ("gain ignores overlap flag", "double sender = overlapped ? 0.0 : (t_hash_s + t_cmp_s);",
+     "double sender = 0.0;"),
+    ("gain drops the decode time", "return comm_raw - (comm_cmp + sender + t_decmp_s);",
+     "return comm_raw - (comm_cmp + sender);"),
+    ("select sorts ascending", "if (ry >= rx) break;", "if (ry <= rx) break;"),
+    ("select keeps non-positive gains", "if (gain[i] > 0.0) order[m++] = i;",
+     "if (gain[i] >= 0.0) order[m++] = i;"),
+]
+
+
+def _build(src_text, out_dir, tag):
+    c = os.path.join(out_dir, f"m_{tag}.c")
+    so = os.path.join(out_dir, f"libm_{tag}.so")
+    with open(c, "w") as f:
+        f.write(src_text)
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-w", "-fPIC", "-shared",
+                           "-I" + os.path.join(ROOT, "oracle"), "-o", so, c])
+    return so
+
+
+def _pins(o):
+    """Returns the list of pins the oracle object fails (empty = all pass)."""
+    failed = []
+
+    def check(name, fn):
+        try:
+            if not fn():
+                failed.append(name)
+        except Exception:  # an exception is a detection too
+            failed.append(name)
+
+    allw = ieee_ref.all_bf16_patterns()
+    e_ref = ieee_ref.exponent_field(allw)
+
+    def split_ieee():
+        e, sm = o.split(allw)
+        mant = ieee_ref.mantissa7(allw)
+        fin = mant >= 0
+        return (np.array_equal(e, e_ref)
+                and np.array_equal(sm >> 7, ieee_ref.sign_bit(allw))
+                and np.array_equal((sm & 0x7F)[fin], mant[fin]))
+    check("split", split_ieee)
+
+    def brute_force():
+        n = allw.size
+        a16 = lambda x: -(-x // 16) * 16
+        for old in (0, 1, 126, 127, 128, 200, 255):
+            cache = np.full(n, old, np.uint8)
+            enc = o.encode(allw, cache, 1)
+            h = o.header(enc)
+            changed = e_ref != old
+            if h["E"] != int(changed.sum()):
+                return False
+            exc0 = 64 + a16(n) + a16(n // 8)
+            if not np.array_equal(enc[exc0:exc0 + h["E"]], e_ref[changed]):
+                return False
+            c2 = cache.copy()
+            if not np.array_equal(o.decode(enc, n, c2), allw):
+                return False
+            if not np.array_equal(c2, e_ref):
+                return False
+            c3 = cache.copy()
+            if not np.array_equal(o.decode(o.encode(allw, cache, 512), n, c3),
+                                  allw):
+                return False
+        return True
+    check("brute force", brute_force)
+
+    def golden():
+        for name in ("worked_example_b2.txt", "worked_example_raw.txt"):
+            f, expect = _read_golden(name)
+            w = np.array([int(t, 16) for t in f["values_bits"].split()],
+                         np.uint16)
+            cache = np.array([int(t, 16) for t in f["cache"].split()],
+                             np.uint8)
+            raw = f.get("raw", "0") == "1"
+            enc = o.encode(w, None if raw else cache, int(f["B"]), raw=raw)
+            if not np.array_equal(enc, expect):
+                return False
+        return True
+    check("golden", golden)
+
+    def sizes():
+        rng = np.random.default_rng(3)
+        a16 = lambda x: -(-x // 16) * 16
+        for n in (1, 17, 511, 513, 4097, 10007):
+            for B in (1, 16, 512, 4096):
+                w = rng.integers(0, 65536, n, dtype=np.uint32).astype(np.uint16)
+                e_new = ieee_ref.exponent_field(w)
+                cache = e_new.copy()
+                flip = rng.random(n) < 0.05
+                cache[flip] = rng.integers(0, 256, int(flip.sum()),
+                                           dtype=np.uint8)
+                enc = o.encode(w, cache, B)
+                h = o.header(enc)
+                nb = -(-n // B)
+                diff = np.zeros(nb * B, bool)
+                diff[:n] = e_new != cache
+                ch = diff.reshape(nb, B).any(axis=1)
+                lens = np.full(nb, B)
+                lens[-1] = n - (nb - 1) * B
+                E = int(lens[ch].sum())
+                bm = -(-nb // 8)
+                if h["E"] != E or h["P"] != n + bm + E:
+                    return False
+                if h["changed_blocks"] != int(ch.sum()):
+                    return False
+                if h["total"] != 64 + a16(n) + a16(bm) + a16(E) != enc.size:
+                    return False
+                if enc[64 + n:64 + a16(n)].any() or enc[64 + a16(n) + bm:
+                                                         64 + a16(n) + a16(bm)].any():
+                    return False
+                if enc[64 + a16(n) + a16(bm) + E:].any():
+                    return False
+                c2 = cache.copy()
+                if not np.array_equal(o.decode(enc, n, c2), w):
+                    return False
+                c3 = cache.copy()
+                o.update_cache(c3, enc, n)
+                if not np.array_equal(c3, e_new):
+                    return False
+        return True
+    check("sizes", sizes)
+
+    def raw_mode():
+        w = np.random.default_rng(5).integers(0, 65536, 999, dtype=np.uint32
+                                              ).astype(np.uint16)
+        enc = o.encode(w, None, 512, raw=True)
+        cache = np.zeros(999, np.uint8)
+        c2 = cache.copy()
+        ok = np.array_equal(o.decode(enc, 999, cache), w)
+        o.update_cache(c2, enc, 999)
+        e = ieee_ref.exponent_field(w)
+        return ok and np.array_equal(cache, e) and np.array_equal(c2, e)
+    check("raw", raw_mode)
+
+    def gain_hand():
+        g = o.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_decmp_s=1e-3)
+        g2 = o.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_hash_s=2e-4,
+                    t_cmp_s=4e-4, t_decmp_s=1e-3, overlapped=False)
+        return (abs(g - 0.000499420625) < 1e-12
+                and abs(g2 - (0.000499420625 - 6e-4)) < 1e-12)
+    check("gain", gain_hand)
+
+    def select_hand():
+        # budget 6.5 MB: 3, 4, 0 fill 6 MB; the zero-gain shard 5 would fit
+        g = [3e-3, 1e-3, -1e-3, 4e-3, 2e-3, 0.0]
+        m = [3e6, 2e6, 1e6, 2e6, 1e6, 0.5e6]
+        return list(o.select(g, m, 6.5e6)) == [True, False, False, True, True,
+                                               False]
+    check("select", select_hand)
+    return failed
+
+
+@pytest.fixture(scope="module")
+def src_text():
+    with open(SRC) as f:
+        return f.read()
+
+
+def test_real_oracle_passes_condensed_pins(orc):
+    from oracle import oracle
+    assert _pins(oracle.Oracle(oracle._LIB)) == []
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, src_text, name, old, new):
+    from oracle import oracle
+    assert src_text.count(old) == 1, f"mutation site not found: {name}"
+    so = _build(src_text.replace(old, new), str(tmp_path), "m")
+    failed = _pins(oracle.Oracle(so))
+    assert failed, f"no pin catches the planted mistake: {name}"

@@ -192,8 +192,12 @@ def test_raw_mode(orc):
         assert h["total"] == 64 + _a16(2 * n) == enc.size
         np.testing.assert_array_equal(enc[64:64 + 2 * n].view(np.uint16), w)
         cache = rng.integers(0, 256, n, dtype=np.uint8)
+        c2 = cache.copy()
         np.testing.assert_array_equal(orc.decode(enc, n, cache), w)
         np.testing.assert_array_equal(cache, ieee_ref.exponent_field(w))
+        # the cache update alone seeds the same exponents
+        orc.update_cache(c2, enc, n)
+        np.testing.assert_array_equal(c2, ieee_ref.exponent_field(w))
 
 
 def test_special_values_round_trip(orc):
