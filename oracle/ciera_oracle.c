@@ -103,6 +103,53 @@ static void write_header(uint8_t *out, uint32_t mode, uint64_t B, uint64_t n,
   put_u64(out + 48, total);
 }
 
+/* Steps 3 to 6 of the encoder for given changed-block flags: the bitmap, the
+ * exception list, the payload size and the wire layout. Returns total. */
+static uint64_t emit_compressed(const uint8_t *expo, const uint8_t *sm,
+                                const uint8_t *changed, uint64_t n, uint64_t B,
+                                uint8_t *out) {
+  uint64_t nblocks = num_blocks(n, B);
+
+  /* Step 3: pack the flags, block b in bit (b mod 8) of byte b/8. */
+  uint64_t bm = bitmap_bytes(n, B);
+  uint8_t *bitmap = (uint8_t *)calloc(bm ? bm : 1, 1);
+  uint64_t nchanged = 0;
+  for (uint64_t b = 0; b < nblocks; b++) {
+    if (changed[b]) {
+      bitmap[b / 8u] = (uint8_t)(bitmap[b / 8u] | (1u << (b % 8u)));
+      nchanged++;
+    }
+  }
+
+  /* Step 4: the changed blocks' exponents, block order, element order. */
+  uint8_t *exc = (uint8_t *)malloc(n ? n : 1);
+  uint64_t E = 0;
+  for (uint64_t b = 0; b < nblocks; b++) {
+    if (!changed[b]) continue;
+    uint64_t lo = b * B;
+    uint64_t hi = lo + B < n ? lo + B : n;
+    for (uint64_t k = lo; k < hi; k++) exc[E++] = expo[k];
+  }
+
+  /* Step 5: payload = S_{s+m} + S_bm + (changed exponent bytes). */
+  uint64_t P = n + bm + E;
+
+  /* Step 6: lay the sections out. */
+  uint64_t off_sm = OR_HEADER;
+  uint64_t off_bm = off_sm + round16(n);
+  uint64_t off_exc = off_bm + round16(bm);
+  uint64_t total = off_exc + round16(E);
+  memset(out, 0, total);
+  write_header(out, OR_MODE_COMPRESSED, B, n, nchanged, E, P, total);
+  memcpy(out + off_sm, sm, n);
+  memcpy(out + off_bm, bitmap, bm);
+  memcpy(out + off_exc, exc, E);
+
+  free(bitmap);
+  free(exc);
+  return total;
+}
+
 uint64_t oracle_encode(const uint16_t *w, const uint8_t *cache, uint64_t n,
                        uint64_t B, int raw, uint8_t *out, uint64_t out_cap) {
   if (B == 0 || B > 0xFFFFFFFFu) return 0;
@@ -139,46 +186,97 @@ uint64_t oracle_encode(const uint16_t *w, const uint8_t *cache, uint64_t n,
     }
   }
 
-  /* Step 3: pack the flags, block b in bit (b mod 8) of byte b/8. */
-  uint64_t bm = bitmap_bytes(n, B);
-  uint8_t *bitmap = (uint8_t *)calloc(bm ? bm : 1, 1);
-  uint64_t nchanged = 0;
-  for (uint64_t b = 0; b < nblk; b++) {
-    if (changed[b]) {
-      bitmap[b / 8u] = (uint8_t)(bitmap[b / 8u] | (1u << (b % 8u)));
-      nchanged++;
-    }
-  }
-
-  /* Step 4: the changed blocks' exponents, block order, element order. */
-  uint8_t *exc = (uint8_t *)malloc(n ? n : 1);
-  uint64_t E = 0;
-  for (uint64_t b = 0; b < nblk; b++) {
-    if (!changed[b]) continue;
-    uint64_t lo = b * B;
-    uint64_t hi = lo + B < n ? lo + B : n;
-    for (uint64_t k = lo; k < hi; k++) exc[E++] = expo[k];
-  }
-
-  /* Step 5: payload = S_{s+m} + S_bm + (changed exponent bytes). */
-  uint64_t P = n + bm + E;
-
-  /* Step 6: lay the sections out. */
-  uint64_t off_sm = OR_HEADER;
-  uint64_t off_bm = off_sm + round16(n);
-  uint64_t off_exc = off_bm + round16(bm);
-  uint64_t total = off_exc + round16(E);
-  memset(out, 0, total);
-  write_header(out, OR_MODE_COMPRESSED, B, n, nchanged, E, P, total);
-  memcpy(out + off_sm, sm, n);
-  memcpy(out + off_bm, bitmap, bm);
-  memcpy(out + off_exc, exc, E);
-
+  uint64_t total = emit_compressed(expo, sm, changed, n, B, out);
   free(expo);
   free(sm);
   free(changed);
-  free(bitmap);
-  free(exc);
+  return total;
+}
+
+/* ---- sender-side change detection by block hash (Section 3.1) ----
+ * SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+ * generators", OOPSLA 2014): the generator adds GAMMA, the odd integer
+ * nearest to 2^64 divided by the golden ratio, to a 64-bit state and returns
+ * the new state passed through the finaliser below. */
+#define OR_SM64_GAMMA 0x9E3779B97F4A7C15ull
+
+uint64_t oracle_sm64_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* Hash128 of Algorithm 1 for one block. The paper builds the 128-bit hash
+ * from two independent 64-bit SplitMix64 hashes and leaves open how a block's
+ * exponents enter them; the reading taken here: the block's exponent bytes
+ * are read as little-endian 64-bit words u_0, u_1, ... (the last word
+ * zero-filled past the block's end), and hash t (t = 0, 1) with seed s_t is
+ *   H_t = sum over j of mix(u_j XOR (s_t + (j + 1) GAMMA))   (mod 2^64),
+ * word j meeting the j-th state of a SplitMix64 generator seeded with s_t.
+ * The seeds are the first two 64-bit words of the binary fraction of pi.
+ * A change confined to one word changes one term and, the finaliser being a
+ * bijection, always changes H_t. */
+static const uint64_t OR_HASH_SEED[2] = {0x243F6A8885A308D3ull,
+                                         0x13198A2E03707344ull};
+
+void oracle_block_hash(const uint8_t *e, uint64_t len, uint64_t h[2]) {
+  uint64_t words = ceil_div(len, 8u);
+  for (int t = 0; t < 2; t++) {
+    uint64_t acc = 0;
+    for (uint64_t j = 0; j < words; j++) {
+      uint64_t u = 0;
+      for (uint64_t i = 0; i < 8u; i++) {
+        uint64_t k = 8u * j + i;
+        if (k < len) u |= (uint64_t)e[k] << (8u * i);
+      }
+      uint64_t state = OR_HASH_SEED[t] + (j + 1u) * OR_SM64_GAMMA;
+      acc += oracle_sm64_mix(u ^ state);
+    }
+    h[t] = acc;
+  }
+}
+
+int oracle_hash_blocks(const uint16_t *w, uint64_t n, uint64_t B,
+                       uint64_t *hash) {
+  if (B == 0) return -1;
+  uint8_t *expo = (uint8_t *)malloc(n ? n : 1);
+  uint8_t *sm = (uint8_t *)malloc(n ? n : 1);
+  oracle_split(w, n, expo, sm);
+  for (uint64_t b = 0; b < num_blocks(n, B); b++) {
+    uint64_t lo = b * B;
+    uint64_t hi = lo + B < n ? lo + B : n;
+    oracle_block_hash(expo + lo, hi - lo, hash + 2u * b);
+  }
+  free(expo);
+  free(sm);
+  return 0;
+}
+
+uint64_t oracle_encode_hashed(const uint16_t *w, const uint64_t *hash_in,
+                              uint64_t *hash_out, uint64_t n, uint64_t B,
+                              uint8_t *out, uint64_t out_cap) {
+  if (B == 0 || B > 0xFFFFFFFFu) return 0;
+  if (out_cap < oracle_encoded_bound(n, B)) return 0;
+  uint8_t *expo = (uint8_t *)malloc(n ? n : 1);
+  uint8_t *sm = (uint8_t *)malloc(n ? n : 1);
+  oracle_split(w, n, expo, sm);
+  /* Step 2 with HashCache: a block counts as changed iff its hash differs
+   * from the stored one; the stored hash becomes the new one. */
+  uint64_t count = num_blocks(n, B);
+  uint8_t *flags = (uint8_t *)calloc(count ? count : 1, 1);
+  for (uint64_t b = 0; b < count; b++) {
+    uint64_t lo = b * B;
+    uint64_t hi = lo + B < n ? lo + B : n;
+    uint64_t h[2];
+    oracle_block_hash(expo + lo, hi - lo, h);
+    flags[b] = (uint8_t)(h[0] != hash_in[2u * b] || h[1] != hash_in[2u * b + 1u]);
+    hash_out[2u * b] = h[0];
+    hash_out[2u * b + 1u] = h[1];
+  }
+  uint64_t total = emit_compressed(expo, sm, flags, n, B, out);
+  free(expo);
+  free(sm);
+  free(flags);
   return total;
 }
 

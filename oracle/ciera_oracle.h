@@ -15,9 +15,10 @@
  *   - Section 3.2: the size definitions S, S_e, S_{s+m}, S_b, S_bm, the
  *     expected payload S_{s+m} + S_bm + q S_e, the gain g_i and the
  *     benefit-to-memory ranking.
- * Readings where the paper is silent (exact compare instead of a block hash,
- * no entropy coder on the exceptions, the wire header and alignment) are
- * stated next to the code that takes them.
+ * Readings where the paper is silent (exact compare as the default change
+ * detector, how the block hash consumes a block's exponents, no entropy coder
+ * on the exceptions, the wire header and alignment) are stated next to the
+ * code that takes them.
  *
  * Parity pins: every function here is pinned by tests that do not re-use
  * this code (IEEE-semantics exponent extraction, brute force over all bf16
@@ -44,6 +45,26 @@ void oracle_split(const uint16_t *w, uint64_t n, uint8_t *e, uint8_t *sm);
  * too small). out must hold oracle_encoded_bound(n, B) bytes. */
 uint64_t oracle_encode(const uint16_t *w, const uint8_t *cache, uint64_t n,
                        uint64_t B, int raw, uint8_t *out, uint64_t out_cap);
+
+/* The SplitMix64 finaliser (Steele, Lea and Flood 2014). */
+uint64_t oracle_sm64_mix(uint64_t z);
+
+/* Hash128 of one block of len exponent bytes (Section 3.1): h[0], h[1]. */
+void oracle_block_hash(const uint8_t *e, uint64_t len, uint64_t h[2]);
+
+/* HashCache of a shard: hash[2b], hash[2b+1] for every block b of B values.
+ * Returns 0, or -1 for B = 0. */
+int oracle_hash_blocks(const uint16_t *w, uint64_t n, uint64_t B,
+                       uint64_t *hash);
+
+/* Encode with the sender's HashCache in place of an exponent cache
+ * (Algorithm 1, Hash128 and the HashCache update): block b counts as changed
+ * iff its hash differs from hash_in[2b..2b+1]; hash_out receives every
+ * block's new hash (it may be hash_in). The wire is that of oracle_encode.
+ * Returns the total size, or 0 on error. */
+uint64_t oracle_encode_hashed(const uint16_t *w, const uint64_t *hash_in,
+                              uint64_t *hash_out, uint64_t n, uint64_t B,
+                              uint8_t *out, uint64_t out_cap);
 
 /* Decode one encoded shard of n elements against cache (updated in place to
  * the exponents of the decoded values). Returns 0, or a negative code when

@@ -66,6 +66,17 @@ def _bind(lib):
     lib.oracle_select.restype = ctypes.c_uint64
     lib.oracle_select.argtypes = [_f64p, _f64p, ctypes.c_uint64,
                                   ctypes.c_double, ctypes.c_int, _u8p]
+    lib.oracle_sm64_mix.restype = ctypes.c_uint64
+    lib.oracle_sm64_mix.argtypes = [ctypes.c_uint64]
+    lib.oracle_block_hash.restype = None
+    lib.oracle_block_hash.argtypes = [_u8p, ctypes.c_uint64, _u64p]
+    lib.oracle_hash_blocks.restype = ctypes.c_int
+    lib.oracle_hash_blocks.argtypes = [_u16p, ctypes.c_uint64,
+                                       ctypes.c_uint64, _u64p]
+    lib.oracle_encode_hashed.restype = ctypes.c_uint64
+    lib.oracle_encode_hashed.argtypes = [_u16p, _u64p, _u64p, ctypes.c_uint64,
+                                         ctypes.c_uint64, _u8p,
+                                         ctypes.c_uint64]
     return lib
 
 
@@ -169,6 +180,45 @@ class Oracle:
                                 _ptr(sel, _u8p))
         return sel.astype(bool)
 
+    # ---- sender-side block hash (Section 3.1, Hash128 / HashCache) ----
+
+    def sm64_mix(self, z: int) -> int:
+        return int(self._lib.oracle_sm64_mix(z))
+
+    def block_hash(self, e: np.ndarray):
+        e = np.ascontiguousarray(e, dtype=np.uint8).ravel()
+        h = np.zeros(2, np.uint64)
+        self._lib.oracle_block_hash(_ptr(e, _u8p), e.size, _ptr(h, _u64p))
+        return int(h[0]), int(h[1])
+
+    def hash_blocks(self, w: np.ndarray, B: int) -> np.ndarray:
+        """HashCache of a shard: uint64[2 * ceil(n/B)], (H_0, H_1) per block."""
+        w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
+        nb = -(-w.size // B)
+        h = np.zeros(max(2 * nb, 1), np.uint64)
+        if self._lib.oracle_hash_blocks(_ptr(w, _u16p), w.size, B,
+                                        _ptr(h, _u64p)):
+            raise ValueError("oracle_hash_blocks rejected its arguments")
+        return h[:2 * nb].copy()
+
+    def encode_hashed(self, w: np.ndarray, hash_in: np.ndarray, B: int):
+        """Encode against a HashCache; returns (encoded bytes, new HashCache)."""
+        w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
+        n = w.size
+        nb = -(-n // B)
+        hin = np.ascontiguousarray(hash_in, dtype=np.uint64).ravel()
+        assert hin.size == 2 * nb
+        hin = np.concatenate([hin, np.zeros(1, np.uint64)])
+        hout = np.full(2 * nb + 1, 0xA5A5A5A5A5A5A5A5, np.uint64)
+        cap = self.encoded_bound(n, B)
+        out = np.full(cap, 0xA5, np.uint8)
+        total = self._lib.oracle_encode_hashed(
+            _ptr(w, _u16p), _ptr(hin, _u64p), _ptr(hout, _u64p), n, B,
+            _ptr(out, _u8p), cap)
+        if total == 0 or total > cap:
+            raise ValueError("oracle_encode_hashed rejected its arguments")
+        return out[:total].copy(), hout[:2 * nb].copy()
+
     header = staticmethod(lambda enc: header(enc))
 
 
@@ -218,6 +268,22 @@ def should_compress(*args, **kw):
 
 def select(gains, mems, budget, stop_at_first_misfit=False):
     return _oracle().select(gains, mems, budget, stop_at_first_misfit)
+
+
+def sm64_mix(z):
+    return _oracle().sm64_mix(z)
+
+
+def block_hash(e):
+    return _oracle().block_hash(e)
+
+
+def hash_blocks(w, B):
+    return _oracle().hash_blocks(w, B)
+
+
+def encode_hashed(w, hash_in, B):
+    return _oracle().encode_hashed(w, hash_in, B)
 
 
 # ---- header fields, read straight from the bytes (no oracle arithmetic) ----

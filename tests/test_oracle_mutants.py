@@ -4,7 +4,7 @@ Each case plants one mistake in a copy of oracle/ciera_oracle.c (on the CPU
 only), builds it with gcc, and runs a condensed set of the pins against it:
 IEEE-semantics field extraction, brute force over old exponents, the
 hand-worked wire fixtures, closed-form sizes and zero padding, the raw form,
-a hand-computed gain and a hand-ranked selection. Every mutant must fail at
+a hand-computed gain and a hand-ranked selection, and the block-hash pins. Every mutant must fail at
 least one of them; the real oracle must pass all of them.
 """
 import os
@@ -61,6 +61,17 @@ MUTANTS = [
      "double sender = 0.0;"),
     ("gain drops the decode time", "return comm_raw - (comm_cmp + sender + t_decmp_s);",
      "return comm_raw - (comm_cmp + sender);"),
+    ("hash word index off by one", "(j + 1u) * OR_SM64_GAMMA",
+     "j * OR_SM64_GAMMA"),
+    ("hash decision reads one half",
+     "h[0] != hash_in[2u * b] || h[1] != hash_in[2u * b + 1u]",
+     "h[0] != hash_in[2u * b]"),
+    ("hash adds the word to the state", "oracle_sm64_mix(u ^ state)",
+     "oracle_sm64_mix(u + state)"),
+    ("hash drops the last partial word", "uint64_t words = ceil_div(len, 8u);",
+     "uint64_t words = len / 8u;"),
+    ("finaliser shift", "z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;",
+     "z = (z ^ (z >> 28)) * 0x94D049BB133111EBull;"),
     ("select sorts ascending", "if (ry >= rx) break;", "if (ry <= rx) break;"),
     ("select keeps non-positive gains", "if (gain[i] > 0.0) order[m++] = i;",
      "if (gain[i] >= 0.0) order[m++] = i;"),
@@ -200,6 +211,38 @@ def _pins(o):
         return (abs(g - 0.000499420625) < 1e-12
                 and abs(g2 - (0.000499420625 - 6e-4)) < 1e-12)
     check("gain", gain_hand)
+
+    def hash_pins():
+        from tests.test_oracle_hash_pins import GAMMA, SEEDS, _pandas_mix
+        M = (1 << 64) - 1
+        if o.sm64_mix(GAMMA) != 0xE220A8397B1DCDAF:
+            return False
+        e = np.array([3, 0, 250, 17, 9], np.uint8)
+        u = int.from_bytes(bytes(e) + bytes(3), "little")
+        for t in range(2):
+            if o.block_hash(e)[t] != _pandas_mix([u ^ ((SEEDS[t] + GAMMA) & M)])[0]:
+                return False
+            if o.block_hash(np.zeros(16, np.uint8))[t] != sum(_pandas_mix(
+                    [(SEEDS[t] + GAMMA) & M, (SEEDS[t] + 2 * GAMMA) & M])) & M:
+                return False
+        rng = np.random.default_rng(15)
+        for n, B in ((20011, 512), (13, 8)):
+            w_old = rng.integers(0, 65536, n, dtype=np.uint32).astype(np.uint16)
+            w_new = w_old.copy()
+            w_new[-1] ^= np.uint16(0x0080)
+            w_new[n // 3] ^= np.uint16(0x0080)
+            h = o.hash_blocks(w_old, B)
+            enc, _ = o.encode_hashed(w_new, h, B)
+            if not np.array_equal(enc, o.encode(
+                    w_new, ieee_ref.exponent_field(w_old), B)):
+                return False
+            h2 = o.hash_blocks(w_new, B)
+            h2[1] ^= np.uint64(1)
+            enc, _ = o.encode_hashed(w_new, h2, B)
+            if o.header(enc)["changed_blocks"] != 1:
+                return False
+        return True
+    check("hash", hash_pins)
 
     def select_hand():
         # budget 6.5 MB: 3, 4, 0 fill 6 MB; the zero-gain shard 5 would fit
