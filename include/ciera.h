@@ -142,6 +142,40 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
                        void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream);
 
+/* -------------------------- sender-side block hash (Section 3.1, Alg. 1) ----
+ * The paper's sender detects changed blocks with a 128-bit hash per block kept
+ * in a HashCache: 16 bytes per block instead of one cached exponent byte per
+ * value, which removes the n-byte cache read from the sender's pass. The
+ * 128 bits are two 64-bit SplitMix64-based hashes (Steele, Lea and Flood
+ * 2014) of the block's exponent bytes taken as little-endian 64-bit words
+ * u_0, u_1, ... (the last one zero-filled past the block's end):
+ *   H_t = sum over j of mix(u_j XOR (s_t + (j + 1) GAMMA))  (mod 2^64),
+ * GAMMA = 0x9E3779B97F4A7C15, s_0 = 0x243F6A8885A308D3,
+ * s_1 = 0x13198A2E03707344 (pi), mix = the SplitMix64 finaliser. A block is
+ * reused only when both halves match. HashCache layout: u64[2 * ceil(n/B)],
+ * (H_0, H_1) of block b at [2b], [2b + 1], 8-byte aligned. B >= 16 (a hash per
+ * value would outweigh the exponent it stands for); B = 1 returns
+ * CIERA_EUNSUPPORTED. The hashes never travel: the wire is unchanged. */
+
+/* HashCache of a shard of n values (seeding it, e.g. from the weights of the
+ * raw first gather). No workspace. */
+int ciera_hash_blocks(const uint16_t *w, uint64_t n_elems,
+                      uint32_t block_elems, uint64_t *hash_cache,
+                      hipStream_t stream);
+
+/* ciera_encode with the HashCache detector: block b counts as changed iff its
+ * hash differs from hash_in[2b..2b+1]; hash_out receives every block's new
+ * hash and may be hash_in (the in-place HashCache update of Algorithm 1). The
+ * encoded bytes equal those of ciera_encode(w_new, C) for any exponent cache C
+ * whose blocks hash to hash_in, barring a 128-bit collision. Arguments,
+ * workspace and errors as for ciera_encode. */
+int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
+                        uint64_t *hash_out, uint64_t n_elems,
+                        uint32_t block_elems, void *out,
+                        uint64_t out_capacity, uint64_t *out_bytes,
+                        void *workspace, uint64_t workspace_bytes,
+                        hipStream_t stream);
+
 /* ---------------------------------------------- selection (Section 3.2) ----
  * Per-shard gain with an alpha-beta Allgather model
  *   Comm(x) = alpha + (R - 1) x / bw

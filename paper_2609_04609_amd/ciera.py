@@ -55,6 +55,9 @@ _SIGS = {
     "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _vp, _vp, _vp,
                                      _u64, _vp]),
     "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _vp, _u64, _vp]),
+    "ciera_hash_blocks": (_i32, [_vp, _u64, _u32, _vp, _vp]),
+    "ciera_encode_hashed": (_i32, [_vp, _vp, _vp, _u64, _u32, _vp, _u64, _vp,
+                                   _vp, _u64, _vp]),
     "ciera_should_compress": (_i32, [ctypes.POINTER(ShardStats),
                                      ctypes.POINTER(CostModel),
                                      ctypes.POINTER(ctypes.c_double)]),
@@ -133,6 +136,18 @@ def ciera_update_cache(exp_cache, encoded, n_elems, block_elems, workspace,
                                     workspace, workspace_bytes, stream)
 
 
+def ciera_hash_blocks(w, n_elems, block_elems, hash_cache, stream):
+    return lib().ciera_hash_blocks(w, n_elems, block_elems, hash_cache, stream)
+
+
+def ciera_encode_hashed(w_new, hash_in, hash_out, n_elems, block_elems, out,
+                        out_capacity, out_bytes, workspace, workspace_bytes,
+                        stream):
+    return lib().ciera_encode_hashed(w_new, hash_in, hash_out, n_elems,
+                                     block_elems, out, out_capacity, out_bytes,
+                                     workspace, workspace_bytes, stream)
+
+
 def ciera_should_compress(n_elems, block_elems, q, world_size, alpha_s,
                           bus_bw_Bps, t_hash_s=0.0, t_cmp_s=0.0, t_decmp_s=0.0,
                           header_bytes=float(HEADER_BYTES), overlapped=True):
@@ -194,6 +209,22 @@ def encode_t(w_bits, cache, block_elems, ws, out, raw=False, out_bytes=None):
                       ENC_RAW if raw else 0, _ptr(out), out.numel(),
                       _ptr(out_bytes), ws.ptr, ws.nbytes, _stream())
     return _check("ciera_encode", rc)
+
+
+def hash_blocks_t(w_bits, block_elems, hash_cache):
+    """HashCache (int64 tensor of 2 * ceil(n/B) words) of a 1-D bit tensor."""
+    rc = ciera_hash_blocks(_ptr(w_bits), w_bits.numel(), block_elems,
+                           _ptr(hash_cache), _stream())
+    return _check("ciera_hash_blocks", rc)
+
+
+def encode_hashed_t(w_bits, hash_in, hash_out, block_elems, ws, out,
+                    out_bytes=None):
+    rc = ciera_encode_hashed(_ptr(w_bits), _ptr(hash_in), _ptr(hash_out),
+                             w_bits.numel(), block_elems, _ptr(out),
+                             out.numel(), _ptr(out_bytes), ws.ptr, ws.nbytes,
+                             _stream())
+    return _check("ciera_encode_hashed", rc)
 
 
 def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,

@@ -88,6 +88,40 @@ int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
   return hipStreamSynchronize(stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
 
+namespace {
+
+// Shared by both compressed encoders: `hashed` selects the HashCache detector
+// (hash_in, hash_out) over exact compare with exp_cache.
+int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
+                      const uint64_t *hash_in, uint64_t *hash_out,
+                      uint64_t n_elems, uint32_t l, void *out,
+                      uint64_t *out_bytes, void *workspace,
+                      uint64_t workspace_bytes, hipStream_t stream,
+                      bool hashed) {
+  if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
+  const uint64_t tiles = enc_tiles(n_elems, l);
+  if (workspace_bytes < kWsCtlBytes + 4 * (tiles + 1)) return CIERA_ENOSPC;
+  EncArgs a{};
+  a.w = w_new;
+  a.cache = exp_cache;
+  a.n = n_elems;
+  a.log2B = l;
+  a.num_tiles = uint32_t(tiles);
+  a.tile_elems = enc_tile_elems(l);
+  a.out = static_cast<uint8_t *>(out);
+  a.out_bytes = out_bytes;
+  a.ctl = static_cast<WsCtl *>(workspace);
+  a.counts = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
+                                          kWsCtlBytes);
+  a.hash_in = hash_in;
+  a.hash_out = hash_out;
+  a.hashed = hashed;
+  const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
+  return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+}  // namespace
+
 int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                  uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                  void *out, uint64_t out_capacity, uint64_t *out_bytes,
@@ -103,31 +137,57 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
   if (!aligned(out, 16)) return CIERA_EINVAL;
   if (out_capacity < ciera_encoded_bound(n_elems, block_elems))
     return CIERA_ENOSPC;
-  uint8_t *o = static_cast<uint8_t *>(out);
   if (raw) {
     const bool vec = aligned(w_new, 16);
-    return launch_encode_raw(w_new, n_elems, block_elems, o, out_bytes, vec,
+    return launch_encode_raw(w_new, n_elems, block_elems,
+                             static_cast<uint8_t *>(out), out_bytes, vec,
                              stream) == hipSuccess
                ? CIERA_OK
                : CIERA_EHIP;
   }
-  if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
-  const uint64_t tiles = enc_tiles(n_elems, uint32_t(l));
-  if (workspace_bytes < kWsCtlBytes + 4 * (tiles + 1)) return CIERA_ENOSPC;
-  EncArgs a;
-  a.w = w_new;
-  a.cache = exp_cache;
+  return encode_compressed(w_new, exp_cache, nullptr, nullptr, n_elems,
+                           uint32_t(l), out, out_bytes, workspace,
+                           workspace_bytes, stream, false);
+}
+
+int ciera_hash_blocks(const uint16_t *w, uint64_t n_elems,
+                      uint32_t block_elems, uint64_t *hash_cache,
+                      hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0 || l < kHashMinLog2B) return CIERA_EUNSUPPORTED;
+  if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (n_elems == 0) return CIERA_OK;
+  if (!w || !hash_cache || !aligned(hash_cache, 8)) return CIERA_EINVAL;
+  EncArgs a{};
+  a.w = w;
   a.n = n_elems;
   a.log2B = uint32_t(l);
-  a.num_tiles = uint32_t(tiles);
+  a.num_tiles = uint32_t(enc_tiles(n_elems, uint32_t(l)));
   a.tile_elems = enc_tile_elems(uint32_t(l));
-  a.out = o;
-  a.out_bytes = out_bytes;
-  a.ctl = static_cast<WsCtl *>(workspace);
-  a.counts = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
-                                          kWsCtlBytes);
-  const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
-  return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+  a.hash_out = hash_cache;
+  return launch_hash_blocks(a, aligned(w, 16), stream) == hipSuccess
+             ? CIERA_OK
+             : CIERA_EHIP;
+}
+
+int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
+                        uint64_t *hash_out, uint64_t n_elems,
+                        uint32_t block_elems, void *out,
+                        uint64_t out_capacity, uint64_t *out_bytes,
+                        void *workspace, uint64_t workspace_bytes,
+                        hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0 || l < kHashMinLog2B) return CIERA_EUNSUPPORTED;
+  if (!out || (n_elems && (!w_new || !hash_in || !hash_out)))
+    return CIERA_EINVAL;
+  if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(out, 16) || !aligned(hash_in, 8) || !aligned(hash_out, 8))
+    return CIERA_EINVAL;
+  if (out_capacity < ciera_encoded_bound(n_elems, block_elems))
+    return CIERA_ENOSPC;
+  return encode_compressed(w_new, nullptr, hash_in, hash_out, n_elems,
+                           uint32_t(l), out, out_bytes, workspace,
+                           workspace_bytes, stream, true);
 }
 
 int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,

@@ -73,7 +73,12 @@ struct EncArgs {
   uint64_t *out_bytes;
   WsCtl *ctl;
   uint32_t *counts;  // num_tiles + 1 words
+  // block-hash detector (B >= 16) in place of exact compare with `cache`
+  bool hashed;
+  const uint64_t *hash_in;
+  uint64_t *hash_out;
 };
+constexpr int kHashMinLog2B = 4;  // the block hash needs B >= 16
 
 struct DecArgs {
   const uint8_t *gathered;
@@ -97,6 +102,8 @@ __host__ __device__ inline uint64_t dec_count_stride(uint64_t tiles) {
 
 // Launchers (ciera_kernels.hip). Each returns the launch status.
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
+// pass 1 with the hash detector only: a.hash_out receives every block's hash
+hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s);
 hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
                              uint8_t *out, uint64_t *out_bytes, bool vec,
                              hipStream_t s);

@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "ciera.h"
 #include "ciera_internal.h"
 
@@ -199,15 +201,41 @@ __device__ __forceinline__ uint64_t pick(const uint64_t (&x)[N], uint32_t i) {
   return r;
 }
 
+// ------------------------------------------------- block hash (Hash128) --
+// Two 64-bit hashes per block from SplitMix64 (Steele, Lea and Flood 2014):
+// the block's exponent bytes as little-endian 64-bit words u_j, and
+//   H_t = sum over j of mix(u_j XOR (s_t + (j + 1) GAMMA))   (mod 2^64)
+// with GAMMA the odd integer nearest 2^64 / golden ratio, mix the SplitMix64
+// finaliser and the seeds s_0, s_1 the first two 64-bit words of the binary
+// fraction of pi. Word j is one octet of the block, so each lane hashes its
+// own octets and a wave sum finishes the block.
+constexpr uint64_t kSm64Gamma = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kHashSeed0 = 0x243F6A8885A308D3ull;
+constexpr uint64_t kHashSeed1 = 0x13198A2E03707344ull;
+
+__device__ __forceinline__ uint64_t sm64_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
 // ================================================================ encode ==
 // A tile belongs to one wave (tile id = 4 * workgroup + wave) and holds
 // kEncTile = 4096 values, or 8 blocks when B > 512, so that a tile owns whole
 // bitmap bytes. Lane l handles octets u*64 + l (u = 0..7) of each 4096-value
 // chunk: wave instruction u covers values [512u, 512u + 512) of the chunk.
 
+// Change detectors of pass 1: exact compare with the exponent cache, or the
+// sender's block hash (HashCache) of Algorithm 1; kDetHashOnly computes the
+// hashes and writes nothing else (seeding HashCache).
+enum : int { kDetExact = 0, kDetHash = 1, kDetHashOnly = 2 };
+
 // Pass 1. Everything but the exception list.
-template <bool VEC, bool ELEMS>
+template <bool VEC, bool ELEMS, int DET>
 __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
+  constexpr bool HASH = DET != kDetExact;
+  constexpr bool OUT = DET != kDetHashOnly;
+  static_assert(!(HASH && ELEMS), "the block hash needs B >= 16");
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t tile = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (tile >= a.num_tiles) return;
@@ -218,14 +246,150 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   const uint64_t n16 = pad16(n);
   const uint64_t bm = bitmap_bytes(n, log2B);
   const uint64_t bm16 = pad16(bm);
-  uint8_t *const sm_out = a.out + kHeaderBytes;
-  uint8_t *const bmp_out = sm_out + n16;
+  uint8_t *const sm_out = OUT ? a.out + kHeaderBytes : nullptr;
+  uint8_t *const bmp_out = OUT ? sm_out + n16 : nullptr;
 
   uint32_t count = 0;
   uint64_t fw[4] = {0ull, 0ull, 0ull, 0ull};  // block flags, B <= 512
   uint32_t fbyte = 0;                          // block flags, B > 512
+
+  // Block hash. The lane's octet in unit u is word j of its block: j = lane
+  // mod (B/8) when B <= 512, 64 * (u mod (B/512)) + lane above.
+  uint64_t st0 = 0, st1 = 0;
+  // Sums over a block: v = log2 of the values each lane holds per chunk (one
+  // per unit when B <= 512, one per block above), g = log2 of the lanes
+  // sharing a block, t = exchange steps (see hash_chunk).
+  uint32_t hv = 0, hg = 0, ht = 0;
+  if (HASH) {
+    const uint64_t j =
+        log2B <= 9 ? uint64_t(lane & ((1u << (log2B - 3)) - 1u)) : lane;
+    st0 = kHashSeed0 + (j + 1) * kSm64Gamma;
+    st1 = kHashSeed1 + (j + 1) * kSm64Gamma;
+    hv = log2B <= 9 ? 3u : 12u - log2B;
+    hg = log2B <= 9 ? log2B - 3u : 6u;
+    ht = hv < hg ? hv : hg;
+  }
+  // The terms of unit u: mix(word XOR state) for both hashes, 0 past n.
+  auto hash_terms = [&](uint32_t u, uint64_t cbase, uint64_t word,
+                        uint64_t &ta, uint64_t &tb) {
+    const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
+    uint64_t s0 = st0, s1 = st1;
+    if (log2B > 9) {
+      const uint64_t shift =
+          uint64_t(u & ((1u << (log2B - 9)) - 1u)) * 64 * kSm64Gamma;
+      s0 += shift;
+      s1 += shift;
+    }
+    ta = elem < n ? sm64_mix(word ^ s0) : 0ull;
+    tb = elem < n ? sm64_mix(word ^ s1) : 0ull;
+  };
+  // Finish the chunk's block hashes from the per-unit terms: fold units into
+  // blocks (B > 512), then sum over the lanes of each block. Each exchange
+  // step hands half of the lane's values to the partner lane across one lane
+  // bit and keeps the other half, so 8 values take 4 + 2 + 1 exchanges
+  // instead of 8 full reductions; plain xor steps finish the remaining lane
+  // bits. Value i then belongs to local index k = (sel << (v - t)) + i (sel:
+  // the lane's bits g-1 .. g-t) and is complete in the lanes whose low g - t
+  // bits are 0. Those lanes compare and store the hashes; the change flags go
+  // to fw (B <= 512) or fbyte.
+  auto hash_chunk = [&](uint64_t cbase, uint64_t (&x)[8], uint64_t (&y)[8]) {
+    if (log2B > 9) {
+      const uint32_t ul = log2B - 9;
+      if (ul >= 1) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          x[i] = x[2 * i] + x[2 * i + 1];
+          y[i] = y[2 * i] + y[2 * i + 1];
+        }
+      }
+      if (ul >= 2) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          x[i] = x[2 * i] + x[2 * i + 1];
+          y[i] = y[2 * i] + y[2 * i + 1];
+        }
+      }
+      if (ul >= 3) {
+        x[0] += x[1];
+        y[0] += y[1];
+      }
+    }
+    // exchange with half size 2^p, p = v-1 .. v-t, across lane bit g-(v-p)
+    auto exchange = [&](auto hc, uint32_t lbit) {
+      constexpr int H = decltype(hc)::value;
+      const bool hi = (lane >> lbit) & 1u;
+      const int off = int(1u << lbit);
+#pragma unroll
+      for (int i = 0; i < H; ++i) {
+        const uint64_t sa = hi ? x[i] : x[i + H], ka = hi ? x[i + H] : x[i];
+        const uint64_t sb = hi ? y[i] : y[i + H], kb = hi ? y[i + H] : y[i];
+        x[i] = ka + __shfl_xor(sa, off, 64);
+        y[i] = kb + __shfl_xor(sb, off, 64);
+      }
+    };
+    if (hv >= 3 && hv - ht <= 2)
+      exchange(std::integral_constant<int, 4>{}, hg - 1u);
+    if (hv >= 2 && hv - ht <= 1)
+      exchange(std::integral_constant<int, 2>{}, hg - (hv - 1u));
+    if (hv >= 1 && hv == ht)
+      exchange(std::integral_constant<int, 1>{}, hg - hv);
+    const uint32_t cnt = 1u << (hv - ht);  // values left per lane
+    for (uint32_t off = (1u << (hg - ht)) >> 1; off > 0; off >>= 1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (uint32_t(i) < cnt) {
+          x[i] += __shfl_xor(x[i], int(off), 64);
+          y[i] += __shfl_xor(y[i], int(off), 64);
+        }
+      }
+    }
+    const bool leader = (lane & ((1u << (hg - ht)) - 1u)) == 0;
+    const uint32_t sel =
+        (lane >> (hg - ht)) & ((1u << ht) - 1u);
+    uint32_t flags = 0;  // bit i: value i's block changed
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (uint32_t(i) >= cnt) continue;
+      const uint32_t k = (sel << (hv - ht)) + uint32_t(i);
+      const uint64_t b_idx = log2B <= 9
+                                 ? ((cbase + uint64_t(k) * 512) >> log2B) +
+                                       (lane >> hg)
+                                 : (cbase >> log2B) + k;
+      if (leader && (b_idx << log2B) < n) {
+        bool ch = false;
+        if (DET == kDetHash)
+          ch = x[i] != a.hash_in[2 * b_idx] || y[i] != a.hash_in[2 * b_idx + 1];
+        a.hash_out[2 * b_idx] = x[i];
+        a.hash_out[2 * b_idx + 1] = y[i];
+        flags |= uint32_t(ch) << i;
+      }
+    }
+    if (!OUT) return;
+    if (log2B <= 9) {
+      // chunk block c = (k << (6 - g)) + grp; its value sits in lane
+      // (grp << g) + (sel << (g - t)) as value i = k mod cnt
+      const uint32_t nb = kEncChunk >> log2B;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t c = uint32_t(q) * 64u + lane;
+        const uint32_t k = c >> (6u - hg);
+        const uint32_t grp = c & ((1u << (6u - hg)) - 1u);
+        const uint32_t src =
+            ((grp << hg) + ((k >> (hv - ht)) << (hg - ht))) & 63u;
+        const uint32_t fl = __shfl(flags, int(src), 64);
+        fw[q] = __ballot(c < nb && ((fl >> (k & (cnt - 1u))) & 1u));
+      }
+    } else {
+      const uint64_t m = __ballot(leader && (flags & 1u));
+      const uint32_t cb0 = uint32_t((cbase - tbase) >> log2B);
+      for (uint32_t k = 0; k < (1u << hv); ++k)
+        if ((m >> (k << (6u - ht))) & 1ull) fbyte |= 1u << (cb0 + k);
+    }
+  };
+
   for (uint64_t cbase = tbase; cbase < tbase + T; cbase += kEncChunk) {
     uint32_t mask[8];  // change bits of the lane's octets
+    uint64_t ta[8], tb[8];  // block-hash terms of the lane's octets
     if (VEC && cbase + kEncChunk <= n) {
       uint4 wv[8];
       uint2 cv[8];
@@ -233,20 +397,28 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
       for (int u = 0; u < 8; ++u)
         wv[u] = *reinterpret_cast<const uint4 *>(
             a.w + cbase + (uint64_t(u) * 64 + lane) * 8);
+      if (!HASH) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        cv[u] = *reinterpret_cast<const uint2 *>(
-            a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
+        for (int u = 0; u < 8; ++u)
+          cv[u] = *reinterpret_cast<const uint2 *>(
+              a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
+      }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
         uint2 e, sm;
         split4(wv[u].x, wv[u].y, e.x, sm.x);
         split4(wv[u].z, wv[u].w, e.y, sm.y);
-        *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
-        mask[u] = ELEMS ? (bytes_ne4(e.x, cv[u].x) |
-                           (bytes_ne4(e.y, cv[u].y) << 4))
-                        : uint32_t((e.x != cv[u].x) || (e.y != cv[u].y));
+        if (OUT) *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
+        if (HASH) {
+          hash_terms(uint32_t(u), cbase,
+                     uint64_t(e.x) | (uint64_t(e.y) << 32), ta[u], tb[u]);
+          mask[u] = 0;
+        } else {
+          mask[u] = ELEMS ? (bytes_ne4(e.x, cv[u].x) |
+                             (bytes_ne4(e.y, cv[u].y) << 4))
+                          : uint32_t((e.x != cv[u].x) || (e.y != cv[u].y));
+        }
       }
     } else {
 #pragma unroll
@@ -254,19 +426,29 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
         const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
         const uint32_t valid = octet_valid(elem, n);
         mask[u] = 0;
+        uint64_t word = 0;
         if (valid) {
           const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-          const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
           uint2 e, sm;
           split4(wv.x, wv.y, e.x, sm.x);
           split4(wv.z, wv.w, e.y, sm.y);
-          store_b8<VEC>(sm_out + elem, sm, valid);
-          // padding values are 0 with a cached 0: never a change
-          mask[u] = ELEMS ? (bytes_ne4(e.x, cv.x) | (bytes_ne4(e.y, cv.y) << 4))
-                          : uint32_t((e.x != cv.x) || (e.y != cv.y));
+          if (OUT) store_b8<VEC>(sm_out + elem, sm, valid);
+          if (HASH) {
+            // load_w8 zero-fills past n: those bytes are 0 in the word
+            word = uint64_t(e.x) | (uint64_t(e.y) << 32);
+          } else {
+            const uint2 cv = load_b8<VEC>(a.cache + elem, valid);
+            // padding values are 0 with a cached 0: never a change
+            mask[u] = ELEMS ? (bytes_ne4(e.x, cv.x) |
+                               (bytes_ne4(e.y, cv.y) << 4))
+                            : uint32_t((e.x != cv.x) || (e.y != cv.y));
+          }
         }
+        if (HASH) hash_terms(uint32_t(u), cbase, word, ta[u], tb[u]);
       }
     }
+    if (HASH) hash_chunk(cbase, ta, tb);
+    if (!OUT) continue;
     if (ELEMS) {
       // an octet's change byte is its bitmap byte
 #pragma unroll
@@ -278,8 +460,10 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
     } else {
       uint64_t m[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) m[u] = __ballot(mask[u] != 0);
-      if (log2B <= 9) {
+      for (int u = 0; u < 8; ++u) m[u] = HASH ? 0ull : __ballot(mask[u] != 0);
+      if (HASH) {
+        // hash_chunk has set the flags
+      } else if (log2B <= 9) {
         // 512/B blocks per 512-value unit, B/8 octets (bits of m[u]) each
         const uint32_t opb_log2 = log2B - 3;
         const uint32_t bpu_log2 = 6 - opb_log2;
@@ -306,6 +490,7 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
       }
     }
   }
+  if (!OUT) return;
 
   if (ELEMS) {
     count = wave_sum(count);
@@ -1053,14 +1238,25 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
   const bool elems = a.log2B == 0;
   if (elems) {
     if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, true>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((encode_pass_kernel<true, true, kDetExact>), grid,
+                         block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_pass_kernel<false, true>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((encode_pass_kernel<false, true, kDetExact>), grid,
+                         block, 0, s, a);
+  } else if (a.hashed) {
+    if (vec)
+      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHash>), grid,
+                         block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHash>), grid,
+                         block, 0, s, a);
   } else {
     if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, false>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetExact>), grid,
+                         block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_pass_kernel<false, false>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetExact>), grid,
+                         block, 0, s, a);
   }
   if (elems)
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
@@ -1078,6 +1274,17 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
       hipLaunchKernelGGL((encode_exc_kernel<false, false>), grid, block, 0, s,
                          a);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s) {
+  const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
+  if (vec)
+    hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHashOnly>), grid,
+                       block, 0, s, a);
+  else
+    hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHashOnly>), grid,
+                       block, 0, s, a);
   return hipGetLastError();
 }
 

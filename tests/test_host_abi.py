@@ -92,6 +92,22 @@ def test_host_argument_checks(cl):
     assert cl.ciera_update_cache(0, fake, 1000, 512, fake, ws_bytes,
                                  0) == cl.EINVAL
     assert cl.ciera_workspace_init(0, 1024, 0) == cl.EINVAL
+    # block hash: B = 1 and unsupported B, null / misaligned hash arrays
+    assert cl.ciera_hash_blocks(fake, 1000, 1, fake, 0) == cl.EUNSUPPORTED
+    assert cl.ciera_hash_blocks(fake, 1000, 100, fake, 0) == cl.EUNSUPPORTED
+    assert cl.ciera_hash_blocks(fake, 1000, 512, 0, 0) == cl.EINVAL
+    assert cl.ciera_hash_blocks(fake, 1000, 512, fake + 4, 0) == cl.EINVAL
+    assert cl.ciera_hash_blocks(0, 0, 512, 0, 0) == cl.OK  # nothing to do
+    assert cl.ciera_encode_hashed(fake, fake, fake, 1000, 1, fake, bound, 0,
+                                  fake, ws_bytes, 0) == cl.EUNSUPPORTED
+    assert cl.ciera_encode_hashed(fake, 0, fake, 1000, 512, fake, bound, 0,
+                                  fake, ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_encode_hashed(fake, fake, fake + 4, 1000, 512, fake,
+                                  bound, 0, fake, ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_encode_hashed(fake, fake, fake, 1000, 512, fake,
+                                  bound - 1, 0, fake, ws_bytes, 0) == cl.ENOSPC
+    assert cl.ciera_encode_hashed(fake, fake, fake, 1000, 512, fake, bound, 0,
+                                  fake, 256, 0) == cl.ENOSPC
     assert L is not None
 
 
