@@ -17,12 +17,17 @@
  *  40 payload bytes P u64   48 total bytes u64   56 reserved u64 = 0
  * Compressed body: sign+mantissa plane (n bytes), bitmap (ceil(ceil(n/B)/8)
  * bytes), exceptions (E bytes); each section starts on a 16-byte boundary and
- * every padding byte is zero. Raw body: the n 16-bit values (2n bytes). */
+ * every padding byte is zero. Raw body: the n 16-bit values (2n bytes).
+ * Mode 2 is the compressed body with the exception section entropy-coded
+ * (see the rANS part below); E stays the number of exception bytes and P
+ * counts the coded section's bytes. */
 #define OR_MAGIC 0x52454943u
 #define OR_VERSION 1u
 #define OR_MODE_COMPRESSED 0u
 #define OR_MODE_RAW 1u
+#define OR_MODE_ANS 2u /* compressed, exception section rANS-coded */
 #define OR_HEADER 64u
+#define OR_ANS_FIXED 520u /* coded section: K, chunk size, 256 frequencies */
 
 static uint64_t round16(uint64_t x) { return (x + 15u) / 16u * 16u; }
 
@@ -280,19 +285,220 @@ uint64_t oracle_encode_hashed(const uint16_t *w, const uint64_t *hash_in,
   return total;
 }
 
+/* ---- entropy coding of the exception section (Section 3.1) ----
+ * The paper codes the changed blocks' exponents with ANS (nvCOMP, whose
+ * format is not published). The reading taken here is range ANS (Duda 2013)
+ * with 16-bit renormalisation, interleaved over 64 states in the manner of
+ * Giesen ("Interleaved entropy coders", 2014):
+ *   - frequencies f_s are quantised to a total M = 2^12 (cumulative c_s);
+ *   - a state x lives in [L, 2^16 L) with L = 2^16; coding symbol s first
+ *     emits the low 16 bits while x >= 2^20 f_s, then sets
+ *     x = floor(x / f_s) * M + (x mod f_s) + c_s;
+ *   - decoding reads slot = x mod M, finds s with c_s <= slot < c_s + f_s,
+ *     sets x = f_s * floor(x / M) + slot - c_s and, while x < L, shifts in
+ *     the next 16-bit word.
+ * The exception list is cut into chunks of 4096 symbols. In a chunk, symbol
+ * i belongs to state i mod 64; the encoder runs the chunk backwards (last
+ * step first, lanes from 63 down to 0), starting every state at L. A chunk's
+ * stream is its 64 final states (u32) followed by the emitted words in the
+ * order the decoder reads them (steps forward, lanes from 0 up), zero-padded
+ * to a multiple of 4 bytes. Decoding must consume the stream exactly and
+ * bring every state back to L.
+ * Section layout (little-endian): u32 chunk count K, u32 symbols per chunk
+ * (4096), u16 f_s for s = 0..255 (sum M), u32 end offset of every chunk's
+ * stream (relative to the first stream), then the streams. The section
+ * replaces the raw exceptions only when it is smaller than E bytes. */
+#define OR_ANS_M 4096u
+#define OR_ANS_SCALE 12u
+#define OR_ANS_L 65536u
+#define OR_ANS_LANES 64u
+#define OR_ANS_CHUNK 4096u
+
+void oracle_ans_normalize(const uint64_t *hist, uint32_t *freq) {
+  uint64_t E = 0, sum = 0;
+  for (int s = 0; s < 256; s++) E += hist[s];
+  for (int s = 0; s < 256; s++) {
+    freq[s] = 0;
+    if (hist[s] == 0) continue;
+    uint64_t f = hist[s] * OR_ANS_M / E;
+    freq[s] = (uint32_t)(f == 0 ? 1 : f);
+    sum += freq[s];
+  }
+  if (E == 0) return;
+  if (sum < OR_ANS_M) {
+    /* the rounding deficit goes to the most frequent symbol (lowest value
+     * on ties) */
+    int best = 0;
+    for (int s = 1; s < 256; s++)
+      if (hist[s] > hist[best]) best = s;
+    freq[best] += (uint32_t)(OR_ANS_M - sum);
+    sum = OR_ANS_M;
+  }
+  while (sum > OR_ANS_M) {
+    /* an excess (from symbols raised to 1) comes off the largest frequency
+     * (lowest value on ties), never below 1 */
+    int best = 0;
+    for (int s = 1; s < 256; s++)
+      if (freq[s] > freq[best]) best = s;
+    uint64_t take = sum - OR_ANS_M;
+    if (take > freq[best] - 1u) take = freq[best] - 1u;
+    freq[best] -= (uint32_t)take;
+    sum -= take;
+  }
+}
+
+static void ans_cumulative(const uint32_t *freq, uint32_t *cum) {
+  uint32_t run = 0;
+  for (int s = 0; s < 256; s++) {
+    cum[s] = run;
+    run += freq[s];
+  }
+}
+
+uint64_t oracle_ans_encode_chunk(const uint8_t *sym, uint64_t len,
+                                 const uint32_t *freq, uint8_t *stream) {
+  uint32_t cum[256];
+  ans_cumulative(freq, cum);
+  uint32_t x[OR_ANS_LANES];
+  for (uint32_t l = 0; l < OR_ANS_LANES; l++) x[l] = OR_ANS_L;
+  uint16_t *emitted = (uint16_t *)malloc((len ? len : 1) * sizeof(uint16_t));
+  uint64_t nw = 0;
+  uint64_t steps = ceil_div(len, OR_ANS_LANES);
+  for (uint64_t t = steps; t-- > 0;) {
+    for (uint32_t l = OR_ANS_LANES; l-- > 0;) {
+      uint64_t i = t * OR_ANS_LANES + l;
+      if (i >= len) continue;
+      uint32_t s = sym[i], f = freq[s];
+      uint64_t x_max = (uint64_t)((OR_ANS_L >> OR_ANS_SCALE) << 16) * f;
+      if (x[l] >= x_max) {
+        emitted[nw++] = (uint16_t)(x[l] & 0xFFFFu);
+        x[l] >>= 16;
+      }
+      x[l] = ((x[l] / f) << OR_ANS_SCALE) + (x[l] % f) + cum[s];
+    }
+  }
+  for (uint32_t l = 0; l < OR_ANS_LANES; l++) put_u32(stream + 4u * l, x[l]);
+  /* the decoder reads the words in the reverse of the order they came out */
+  for (uint64_t k = 0; k < nw; k++)
+    put_u16(stream + 4u * OR_ANS_LANES + 2u * k, emitted[nw - 1u - k]);
+  free(emitted);
+  return 4u * OR_ANS_LANES + 2u * nw;
+}
+
+int oracle_ans_decode_chunk(const uint8_t *stream, uint64_t avail,
+                            uint64_t len, const uint32_t *freq, uint8_t *sym,
+                            uint64_t *consumed) {
+  uint32_t cum[256];
+  ans_cumulative(freq, cum);
+  if (avail < 4u * OR_ANS_LANES) return -4;
+  uint32_t x[OR_ANS_LANES];
+  for (uint32_t l = 0; l < OR_ANS_LANES; l++) {
+    x[l] = get_u32(stream + 4u * l);
+    if (x[l] < OR_ANS_L) return -4;
+  }
+  uint64_t rd = 4u * OR_ANS_LANES;
+  uint64_t steps = ceil_div(len, OR_ANS_LANES);
+  for (uint64_t t = 0; t < steps; t++) {
+    for (uint32_t l = 0; l < OR_ANS_LANES; l++) {
+      uint64_t i = t * OR_ANS_LANES + l;
+      if (i >= len) continue;
+      uint32_t slot = x[l] & (OR_ANS_M - 1u);
+      uint32_t s = 0;
+      while (!(cum[s] <= slot && slot < cum[s] + freq[s])) s++;
+      sym[i] = (uint8_t)s;
+      x[l] = freq[s] * (x[l] >> OR_ANS_SCALE) + slot - cum[s];
+      if (x[l] < OR_ANS_L) {
+        if (rd + 2u > avail) return -4;
+        x[l] = (x[l] << 16) | get_u16(stream + rd);
+        rd += 2u;
+      }
+    }
+  }
+  for (uint32_t l = 0; l < OR_ANS_LANES; l++)
+    if (x[l] != OR_ANS_L) return -4;
+  *consumed = rd;
+  return 0;
+}
+
+uint64_t oracle_ans_section_bound(uint64_t E) {
+  uint64_t K = ceil_div(E, OR_ANS_CHUNK);
+  return OR_ANS_FIXED + 4u * K + K * (4u * OR_ANS_LANES + 4u) + 2u * E;
+}
+
+uint64_t oracle_ans_code_section(const uint8_t *exc, uint64_t E,
+                                 uint8_t *section) {
+  uint64_t hist[256] = {0};
+  for (uint64_t i = 0; i < E; i++) hist[exc[i]]++;
+  uint32_t freq[256];
+  oracle_ans_normalize(hist, freq);
+  uint64_t K = ceil_div(E, OR_ANS_CHUNK);
+  put_u32(section + 0, (uint32_t)K);
+  put_u32(section + 4, OR_ANS_CHUNK);
+  for (int s = 0; s < 256; s++) put_u16(section + 8 + 2 * s, (uint16_t)freq[s]);
+  uint8_t *streams = section + OR_ANS_FIXED + 4u * K;
+  uint64_t off = 0;
+  for (uint64_t c = 0; c < K; c++) {
+    uint64_t lo = c * OR_ANS_CHUNK;
+    uint64_t len = E - lo < OR_ANS_CHUNK ? E - lo : OR_ANS_CHUNK;
+    uint64_t bytes = oracle_ans_encode_chunk(exc + lo, len, freq, streams + off);
+    while (bytes % 4u) streams[off + bytes++] = 0;
+    off += bytes;
+    put_u32(section + OR_ANS_FIXED + 4u * c, (uint32_t)off);
+  }
+  return OR_ANS_FIXED + 4u * K + off;
+}
+
+int oracle_ans_decode_section(const uint8_t *section, uint64_t C, uint64_t E,
+                              uint8_t *exc) {
+  if (C < OR_ANS_FIXED) return -4;
+  uint64_t K = get_u32(section + 0);
+  if (K != ceil_div(E, OR_ANS_CHUNK)) return -4;
+  if (get_u32(section + 4) != OR_ANS_CHUNK) return -4;
+  if (C < OR_ANS_FIXED + 4u * K) return -4;
+  uint32_t freq[256];
+  uint64_t total = 0;
+  for (int s = 0; s < 256; s++) {
+    freq[s] = get_u16(section + 8 + 2 * s);
+    total += freq[s];
+  }
+  if (total != OR_ANS_M) return -4;
+  const uint8_t *streams = section + OR_ANS_FIXED + 4u * K;
+  uint64_t avail_all = C - OR_ANS_FIXED - 4u * K;
+  uint64_t start = 0;
+  for (uint64_t c = 0; c < K; c++) {
+    uint64_t end = get_u32(section + OR_ANS_FIXED + 4u * c);
+    if (end < start || end > avail_all || end % 4u) return -4;
+    uint64_t lo = c * OR_ANS_CHUNK;
+    uint64_t len = E - lo < OR_ANS_CHUNK ? E - lo : OR_ANS_CHUNK;
+    uint64_t used = 0;
+    if (oracle_ans_decode_chunk(streams + start, end - start, len, freq,
+                                exc + lo, &used))
+      return -4;
+    /* only zero padding may follow the words */
+    if (end - start - used >= 4u) return -4;
+    for (uint64_t k = start + used; k < end; k++)
+      if (streams[k]) return -4;
+    start = end;
+  }
+  return start == avail_all ? 0 : -4;
+}
+
+
 /* Header check shared by the two receiver-side routines. */
 static int read_header(const uint8_t *enc, uint64_t n, uint32_t *mode,
                        uint64_t *B, uint64_t *E) {
   if (get_u32(enc + 0) != OR_MAGIC) return -4;
   if (get_u16(enc + 4) != OR_VERSION) return -4;
   *mode = get_u16(enc + 6);
-  if (*mode != OR_MODE_COMPRESSED && *mode != OR_MODE_RAW) return -4;
+  if (*mode != OR_MODE_COMPRESSED && *mode != OR_MODE_RAW &&
+      *mode != OR_MODE_ANS)
+    return -4;
   *B = get_u32(enc + 8);
   if (*B == 0) return -4;
   if (get_u64(enc + 16) != n) return -4;
   *E = get_u64(enc + 32);
   if (*E > n) return -4;
-  if (*mode == OR_MODE_COMPRESSED) {
+  if (*mode == OR_MODE_COMPRESSED || *mode == OR_MODE_ANS) {
     /* the exception list must hold exactly the flagged blocks' exponents */
     uint64_t bm = bitmap_bytes(n, *B);
     const uint8_t *bitmap = enc + OR_HEADER + round16(n);
@@ -305,7 +511,14 @@ static int read_header(const uint8_t *enc, uint64_t n, uint32_t *mode,
       }
     }
     if (want != *E) return -4;
-    if (get_u64(enc + 48) != OR_HEADER + round16(n) + round16(bm) + round16(*E))
+    uint64_t section = *E; /* bytes of the exception section */
+    if (*mode == OR_MODE_ANS) {
+      uint64_t P = get_u64(enc + 40);
+      if (P < n + bm + OR_ANS_FIXED) return -4;
+      section = P - n - bm;
+    }
+    if (get_u64(enc + 48) !=
+        OR_HEADER + round16(n) + round16(bm) + round16(section))
       return -4;
   } else if (get_u64(enc + 48) != OR_HEADER + round16(2u * n)) {
     return -4;
@@ -315,12 +528,24 @@ static int read_header(const uint8_t *enc, uint64_t n, uint32_t *mode,
 
 /* Algorithm 1 receiver: patch ExpCache for every block flagged in the bitmap
  * with the next B exponents of the exception list (j advances one block at a
- * time). */
-static void patch_cache(const uint8_t *enc, uint64_t n, uint64_t B,
-                        uint8_t *cache) {
+ * time). An entropy-coded list is decoded first (ANS-decode, then replace
+ * the changed blocks). Returns 0 or -4 for a malformed coded section. */
+static int patch_cache(const uint8_t *enc, uint64_t n, uint64_t B,
+                       uint8_t *cache) {
   uint64_t bm = bitmap_bytes(n, B);
   const uint8_t *bitmap = enc + OR_HEADER + round16(n);
   const uint8_t *exc = bitmap + round16(bm);
+  uint8_t *decoded = NULL;
+  if (get_u16(enc + 6) == OR_MODE_ANS) {
+    uint64_t E = get_u64(enc + 32);
+    uint64_t section = get_u64(enc + 40) - n - bm;
+    decoded = (uint8_t *)malloc(E ? E : 1);
+    if (oracle_ans_decode_section(exc, section, E, decoded)) {
+      free(decoded);
+      return -4;
+    }
+    exc = decoded;
+  }
   uint64_t nblk = num_blocks(n, B);
   uint64_t j = 0; /* index of the next unread exception byte */
   for (uint64_t b = 0; b < nblk; b++) {
@@ -330,6 +555,8 @@ static void patch_cache(const uint8_t *enc, uint64_t n, uint64_t B,
     uint64_t hi = lo + B < n ? lo + B : n;
     for (uint64_t k = lo; k < hi; k++) cache[k] = exc[j++];
   }
+  free(decoded);
+  return 0;
 }
 
 int oracle_update_cache(uint8_t *cache, const uint8_t *enc, uint64_t n) {
@@ -344,8 +571,7 @@ int oracle_update_cache(uint8_t *cache, const uint8_t *enc, uint64_t n) {
     }
     return 0;
   }
-  patch_cache(enc, n, B, cache);
-  return 0;
+  return patch_cache(enc, n, B, cache);
 }
 
 int oracle_decode(const uint8_t *enc, uint64_t n, uint8_t *cache,
@@ -363,7 +589,7 @@ int oracle_decode(const uint8_t *enc, uint64_t n, uint8_t *cache,
     return 0;
   }
   /* Algorithm 1: if the payload holds exceptions, patch the cache first ... */
-  if (E > 0) patch_cache(enc, n, B, cache);
+  if (E > 0 && patch_cache(enc, n, B, cache)) return -4;
   /* ... then Merge(ExpCache, mant) rebuilds the whole shard. */
   const uint8_t *sm = enc + OR_HEADER;
   for (uint64_t k = 0; k < n; k++) out[k] = merge_one(cache[k], sm[k]);
@@ -380,6 +606,31 @@ int oracle_decode_gathered(const uint8_t *gathered, const uint64_t *offsets,
     if (rc && !first) first = rc;
   }
   return first;
+}
+
+/* Entropy-code the exception section of an encoded shard in place when
+ * that makes it smaller (mode 2); returns the shard's total size. */
+uint64_t oracle_ans_code_shard(uint8_t *enc, uint64_t n) {
+  uint32_t mode;
+  uint64_t B, E;
+  if (read_header(enc, n, &mode, &B, &E)) return 0;
+  uint64_t total = get_u64(enc + 48);
+  if (mode != OR_MODE_COMPRESSED) return total;
+  uint64_t bm = bitmap_bytes(n, B);
+  uint8_t *exc = enc + OR_HEADER + round16(n) + round16(bm);
+  uint8_t *section = (uint8_t *)malloc(oracle_ans_section_bound(E));
+  uint64_t C = oracle_ans_code_section(exc, E, section);
+  if (C < E) {
+    /* smaller: the coded section replaces the raw exceptions */
+    memcpy(exc, section, C);
+    memset(exc + C, 0, round16(C) - C);
+    total = OR_HEADER + round16(n) + round16(bm) + round16(C);
+    put_u16(enc + 6, (uint16_t)OR_MODE_ANS);
+    put_u64(enc + 40, n + bm + C);
+    put_u64(enc + 48, total);
+  }
+  free(section);
+  return total;
 }
 
 /* Section 3.2 gain:

@@ -66,6 +66,38 @@ uint64_t oracle_encode_hashed(const uint16_t *w, const uint64_t *hash_in,
                               uint64_t *hash_out, uint64_t n, uint64_t B,
                               uint8_t *out, uint64_t out_cap);
 
+/* ---- rANS on the exception section (Section 3.1; format in the .c file) */
+
+/* Frequencies (sum 2^12) of a 256-symbol histogram. */
+void oracle_ans_normalize(const uint64_t *hist, uint32_t *freq);
+
+/* One chunk (len <= 4096 symbols, 64 interleaved states) into stream, which
+ * must hold 256 + 2 len bytes. Returns the stream bytes (unpadded). */
+uint64_t oracle_ans_encode_chunk(const uint8_t *sym, uint64_t len,
+                                 const uint32_t *freq, uint8_t *stream);
+
+/* Decode one chunk of len symbols from at most avail stream bytes; *consumed
+ * receives the bytes read. Returns 0 or -4 (malformed stream). */
+int oracle_ans_decode_chunk(const uint8_t *stream, uint64_t avail,
+                            uint64_t len, const uint32_t *freq, uint8_t *sym,
+                            uint64_t *consumed);
+
+/* Upper bound of a coded section for E exception bytes. */
+uint64_t oracle_ans_section_bound(uint64_t E);
+
+/* Code E exception bytes into a section; returns its size C. */
+uint64_t oracle_ans_code_section(const uint8_t *exc, uint64_t E,
+                                 uint8_t *section);
+
+/* Decode a C-byte section holding E exception bytes. Returns 0 or -4. */
+int oracle_ans_decode_section(const uint8_t *section, uint64_t C, uint64_t E,
+                              uint8_t *exc);
+
+/* Recode a compressed shard in place with an rANS-coded exception section
+ * when that is smaller than E bytes (mode 2). Returns the total size after,
+ * or 0 when the header does not describe an n-value shard. */
+uint64_t oracle_ans_code_shard(uint8_t *enc, uint64_t n);
+
 /* Decode one encoded shard of n elements against cache (updated in place to
  * the exponents of the decoded values). Returns 0, or a negative code when
  * the header does not describe an n-element shard. */

@@ -22,6 +22,7 @@ _LIB = os.path.join(_HERE, "libciera_oracle.so")
 
 _u8p = ctypes.POINTER(ctypes.c_uint8)
 _u16p = ctypes.POINTER(ctypes.c_uint16)
+_u32p = ctypes.POINTER(ctypes.c_uint32)
 _u64p = ctypes.POINTER(ctypes.c_uint64)
 _f64p = ctypes.POINTER(ctypes.c_double)
 
@@ -73,6 +74,23 @@ def _bind(lib):
     lib.oracle_hash_blocks.restype = ctypes.c_int
     lib.oracle_hash_blocks.argtypes = [_u16p, ctypes.c_uint64,
                                        ctypes.c_uint64, _u64p]
+    lib.oracle_ans_normalize.restype = None
+    lib.oracle_ans_normalize.argtypes = [_u64p, _u32p]
+    lib.oracle_ans_encode_chunk.restype = ctypes.c_uint64
+    lib.oracle_ans_encode_chunk.argtypes = [_u8p, ctypes.c_uint64, _u32p, _u8p]
+    lib.oracle_ans_decode_chunk.restype = ctypes.c_int
+    lib.oracle_ans_decode_chunk.argtypes = [_u8p, ctypes.c_uint64,
+                                            ctypes.c_uint64, _u32p, _u8p,
+                                            _u64p]
+    lib.oracle_ans_section_bound.restype = ctypes.c_uint64
+    lib.oracle_ans_section_bound.argtypes = [ctypes.c_uint64]
+    lib.oracle_ans_code_section.restype = ctypes.c_uint64
+    lib.oracle_ans_code_section.argtypes = [_u8p, ctypes.c_uint64, _u8p]
+    lib.oracle_ans_decode_section.restype = ctypes.c_int
+    lib.oracle_ans_decode_section.argtypes = [_u8p, ctypes.c_uint64,
+                                              ctypes.c_uint64, _u8p]
+    lib.oracle_ans_code_shard.restype = ctypes.c_uint64
+    lib.oracle_ans_code_shard.argtypes = [_u8p, ctypes.c_uint64]
     lib.oracle_encode_hashed.restype = ctypes.c_uint64
     lib.oracle_encode_hashed.argtypes = [_u16p, _u64p, _u64p, ctypes.c_uint64,
                                          ctypes.c_uint64, _u8p,
@@ -219,6 +237,61 @@ class Oracle:
             raise ValueError("oracle_encode_hashed rejected its arguments")
         return out[:total].copy(), hout[:2 * nb].copy()
 
+    # ---- rANS on the exception section (Section 3.1) ----
+
+    def ans_normalize(self, hist) -> np.ndarray:
+        h = np.ascontiguousarray(hist, dtype=np.uint64)
+        assert h.size == 256
+        f = np.zeros(256, np.uint32)
+        self._lib.oracle_ans_normalize(_ptr(h, _u64p), _ptr(f, _u32p))
+        return f
+
+    def ans_encode_chunk(self, sym, freq) -> np.ndarray:
+        sym = np.ascontiguousarray(sym, dtype=np.uint8).ravel()
+        f = np.ascontiguousarray(freq, dtype=np.uint32)
+        buf = np.full(256 + 2 * sym.size, 0xA5, np.uint8)
+        nb = self._lib.oracle_ans_encode_chunk(_ptr(sym, _u8p), sym.size,
+                                               _ptr(f, _u32p), _ptr(buf, _u8p))
+        return buf[:nb].copy()
+
+    def ans_decode_chunk(self, stream, length, freq):
+        """Returns (symbols, bytes consumed); raises on a malformed stream."""
+        st = np.ascontiguousarray(stream, dtype=np.uint8)
+        f = np.ascontiguousarray(freq, dtype=np.uint32)
+        out = np.zeros(max(length, 1), np.uint8)
+        used = np.zeros(1, np.uint64)
+        rc = self._lib.oracle_ans_decode_chunk(
+            _ptr(st, _u8p), st.size, length, _ptr(f, _u32p), _ptr(out, _u8p),
+            _ptr(used, _u64p))
+        if rc:
+            raise ValueError("oracle_ans_decode_chunk: malformed stream")
+        return out[:length].copy(), int(used[0])
+
+    def ans_code_section(self, exc) -> np.ndarray:
+        exc = np.ascontiguousarray(exc, dtype=np.uint8).ravel()
+        cap = int(self._lib.oracle_ans_section_bound(exc.size))
+        sec = np.full(cap, 0xA5, np.uint8)
+        C = self._lib.oracle_ans_code_section(_ptr(exc, _u8p), exc.size,
+                                              _ptr(sec, _u8p))
+        return sec[:C].copy()
+
+    def ans_decode_section(self, section, E) -> np.ndarray:
+        sec = np.ascontiguousarray(section, dtype=np.uint8)
+        out = np.zeros(max(E, 1), np.uint8)
+        if self._lib.oracle_ans_decode_section(_ptr(sec, _u8p), sec.size, E,
+                                               _ptr(out, _u8p)):
+            raise ValueError("oracle_ans_decode_section: malformed section")
+        return out[:E].copy()
+
+    def ans_code(self, enc: np.ndarray, n: int) -> np.ndarray:
+        """An encoded shard with its exception section rANS-coded when that
+        is smaller (mode 2); otherwise the same bytes."""
+        buf = np.array(enc, dtype=np.uint8, copy=True)
+        total = self._lib.oracle_ans_code_shard(_ptr(buf, _u8p), n)
+        if total == 0:
+            raise ValueError("oracle_ans_code_shard: bad shard")
+        return buf[:total].copy()
+
     header = staticmethod(lambda enc: header(enc))
 
 
@@ -284,6 +357,30 @@ def hash_blocks(w, B):
 
 def encode_hashed(w, hash_in, B):
     return _oracle().encode_hashed(w, hash_in, B)
+
+
+def ans_normalize(hist):
+    return _oracle().ans_normalize(hist)
+
+
+def ans_encode_chunk(sym, freq):
+    return _oracle().ans_encode_chunk(sym, freq)
+
+
+def ans_decode_chunk(stream, length, freq):
+    return _oracle().ans_decode_chunk(stream, length, freq)
+
+
+def ans_code_section(exc):
+    return _oracle().ans_code_section(exc)
+
+
+def ans_decode_section(section, E):
+    return _oracle().ans_decode_section(section, E)
+
+
+def ans_code(enc, n):
+    return _oracle().ans_code(enc, n)
 
 
 # ---- header fields, read straight from the bytes (no oracle arithmetic) ----

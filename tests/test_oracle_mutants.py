@@ -4,11 +4,13 @@ Each case plants one mistake in a copy of oracle/ciera_oracle.c (on the CPU
 only), builds it with gcc, and runs a condensed set of the pins against it:
 IEEE-semantics field extraction, brute force over old exponents, the
 hand-worked wire fixtures, closed-form sizes and zero padding, the raw form,
-a hand-computed gain and a hand-ranked selection, and the block-hash pins. Every mutant must fail at
+a hand-computed gain and a hand-ranked selection, the block-hash pins and
+the rANS pins. Every mutant must fail at
 least one of them; the real oracle must pass all of them.
 """
 import os
 import subprocess
+import sys
 
 import numpy as np
 import pytest
@@ -48,13 +50,23 @@ MUTANTS = [
     ("decode patches only the first value of a block",
      "for (uint64_t k = lo; k < hi; k++) cache[k] = exc[j++];",
      "cache[lo] = exc[j]; j += hi - lo;"),
-    ("raw cache from the wrong field", "cache[k] = (uint8_t)((x >> 7) & 0xFFu);\n    }\n    return 0;\n  }\n  patch_cache",
-     "cache[k] = (uint8_t)((x >> 6) & 0xFFu);\n    }\n    return 0;\n  }\n  patch_cache"),
+    ("raw cache from the wrong field", "cache[k] = (uint8_t)((x >> 7) & 0xFFu);\n    }\n    return 0;\n  }\n  return patch_cache",
+     "cache[k] = (uint8_t)((x >> 6) & 0xFFu);\n    }\n    return 0;\n  }\n  return patch_cache"),
     ("raw decode seeds the wrong field",
      "      out[k] = x;\n      cache[k] = (uint8_t)((x >> 7) & 0xFFu);",
      "      out[k] = x;\n      cache[k] = (uint8_t)((x >> 8) & 0xFFu);"),
-    ("decode skips the patch", "  if (E > 0) patch_cache(enc, n, B, cache);",
-     "  if (E > n) patch_cache(enc, n, B, cache);"),
+    ("decode skips the patch", "  if (E > 0 && patch_cache(enc, n, B, cache)) return -4;",
+     "  if (E > n && patch_cache(enc, n, B, cache)) return -4;"),
+    ("ans emission bound", "(uint64_t)((OR_ANS_L >> OR_ANS_SCALE) << 16) * f;",
+     "(uint64_t)((OR_ANS_L >> OR_ANS_SCALE) << 15) * f;"),
+    ("ans decoder drops the cumulative",
+     "x[l] = freq[s] * (x[l] >> OR_ANS_SCALE) + slot - cum[s];",
+     "x[l] = freq[s] * (x[l] >> OR_ANS_SCALE) + slot;"),
+    ("ans words in emission order", "emitted[nw - 1u - k]", "emitted[k]"),
+    ("ans deficit tie to the last symbol", "if (hist[s] > hist[best]) best = s;",
+     "if (hist[s] >= hist[best]) best = s;"),
+    ("ans chunk size", "#define OR_ANS_CHUNK 4096u", "#define OR_ANS_CHUNK 2048u"),
+    ("ans codes when not smaller", "  if (C < E) {", "  if (C < E + 100000u) {"),
     ("gain counts R hops", "double comm_raw = alpha_s + (double)(R - 1) * S / bw_Bps;",
      "double comm_raw = alpha_s + (double)R * S / bw_Bps;"),
     ("gain ignores overlap flag", "double sender = overlapped ? 0.0 : (t_hash_s + t_cmp_s);",
@@ -244,6 +256,50 @@ def _pins(o):
         return True
     check("hash", hash_pins)
 
+    def ans_pins():
+        from tests.test_oracle_ans_pins import _read_chunk_fixture
+        f = o.ans_normalize(np.bincount([3, 7, 8], minlength=256))
+        if (f[3], f[7], f[8]) != (1366, 1365, 1365):
+            return False
+        f = o.ans_normalize(np.bincount([5, 5, 9], minlength=256))
+        if (f[5], f[9]) != (2731, 1365):
+            return False
+        for name in ("ans_chunk_three_symbols.txt", "ans_chunk_one_word.txt"):
+            sym, freq, stream = _read_chunk_fixture(name)
+            if not np.array_equal(o.ans_encode_chunk(sym, freq), stream):
+                return False
+        rng = np.random.default_rng(26)
+        sym = rng.choice([118, 119, 120, 121, 7], 3000,
+                         p=[.4, .3, .2, .09, .01]).astype(np.uint8)
+        f = o.ans_normalize(np.bincount(sym, minlength=256))
+        dec, _ = o.ans_decode_chunk(o.ans_encode_chunk(sym, f), sym.size, f)
+        if not np.array_equal(dec, sym):
+            return False
+        sec = o.ans_code_section(np.tile(sym, 3))
+        if int(sec[4:8].view(np.uint32)[0]) != 4096 or \
+                int(sec[0:4].view(np.uint32)[0]) != 3:
+            return False
+        n = 30011
+        w = (rng.normal(0, 0.02, n).astype(np.float32).view(np.uint32)
+             >> 16).astype(np.uint16)
+        for rate in (0.01, 0.0):
+            w2 = w.copy()
+            w2[rng.random(n) < rate] ^= np.uint16(0x0080)
+            cache = ieee_ref.exponent_field(w)
+            enc = o.encode(w2, cache, 64)
+            coded = o.ans_code(enc, n)
+            E = o.header(enc)["E"]
+            a16 = lambda x: -(-x // 16) * 16
+            exc = enc[64 + a16(n) + a16(-(-(-(-n // 64)) // 8)):][:E]
+            if (o.header(coded)["mode"] == 2) != \
+                    (o.ans_code_section(exc).size < E):
+                return False
+            c2 = cache.copy()
+            if not np.array_equal(o.decode(coded, n, c2), w2):
+                return False
+        return True
+    check("ans", ans_pins)
+
     def select_hand():
         # budget 6.5 MB: 3, 4, 0 fill 6 MB; the zero-gain shard 5 would fit
         g = [3e-3, 1e-3, -1e-3, 4e-3, 2e-3, 0.0]
@@ -267,8 +323,16 @@ def test_real_oracle_passes_condensed_pins(orc):
 
 @pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
 def test_mutant_is_caught(tmp_path, src_text, name, old, new):
-    from oracle import oracle
+    """The pins run in a child process: a planted mistake that crashes the
+    oracle (an overrun, say) is a detection too."""
     assert src_text.count(old) == 1, f"mutation site not found: {name}"
     so = _build(src_text.replace(old, new), str(tmp_path), "m")
-    failed = _pins(oracle.Oracle(so))
-    assert failed, f"no pin catches the planted mistake: {name}"
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from oracle import oracle\n"
+            "from tests.test_oracle_mutants import _pins\n"
+            "failed = _pins(oracle.Oracle(%r))\n"
+            "print('FAILED:', failed)\n"
+            "sys.exit(3 if failed else 0)\n") % (ROOT, so)
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode != 0, f"no pin catches the planted mistake: {name}"
