@@ -13,18 +13,21 @@
  * sign+mantissa back into the exact bf16 values. Section 3.2 decides per
  * tensor whether compression pays off at all.
  *
- * Differences from the paper's own implementation, all lossless:
- *   - change detection compares each exponent with the cached byte exactly
- *     instead of comparing a 128-bit hash per block (same result without the
- *     2^-128 collision chance);
- *   - the changed blocks' exponents travel raw (no entropy coder);
+ * Choices beside the paper's own implementation, all lossless:
+ *   - change detection by exact compare with the cached exponents
+ *     (ciera_encode) or by the paper's 128-bit block hash (ciera_encode_hashed);
+ *     both give the same bytes, barring a 2^-128 hash collision;
+ *   - the changed blocks' exponents travel raw, or rANS-coded in place of the
+ *     paper's nvCOMP ANS (ciera_ans_code, used when it makes the shard
+ *     smaller);
  *   - B is a parameter: 1 (one exception per changed value) or a power of two
  *     from 16 to 4096 (the paper's default is 512).
  *
  * ---------------------------------------------------------------- wire ----
  * An encoded shard starts with a 64-byte little-endian header:
  *    0 magic u32 0x52454943 ("CIER")  4 version u16 = 1  6 mode u16
- *      (0 compressed, 1 raw)          8 B u32           12 reserved u32 = 0
+ *      (0 compressed, 1 raw, 2 compressed with rANS-coded exceptions)
+ *    8 B u32   12 reserved u32 = 0
  *   16 n u64 (values)   24 changed blocks u64   32 exception bytes E u64
  *   40 payload bytes P u64   48 total bytes u64   56 reserved u64 = 0
  * compressed body: sign+mantissa plane (n bytes: sign in bit 7, mantissa in
@@ -33,6 +36,19 @@
  *   order); each section starts on a 16-byte boundary, padding bytes are 0;
  *   P = n + bitmap bytes + E, the paper's S_{s+m} + S_bm + q S_e.
  * raw body: the n values as little-endian 16-bit words (P = 2n).
+ * mode 2 body: as compressed, with the exception section replaced by its
+ *   rANS coding (E still counts exception bytes; P = n + bitmap bytes + C for
+ *   a C-byte coded section). Coded section, little-endian: u32 K = ceil(E /
+ *   4096) chunks, u32 4096, u16 f[256] (frequencies summing to 4096), u32
+ *   end[K] (byte offset past chunk k's stream, from the first stream), then
+ *   the streams. Chunk k holds exception bytes [4096k, 4096k + 4096); its
+ *   byte i belongs to rANS state i mod 64. A stream is the 64 final states
+ *   (u32) and then 16-bit words, zero-padded to a multiple of 4 bytes. With
+ *   c_s the prefix sums of f, M = 4096 and L = 65536, decoding a state x gives
+ *   symbol s with c_s <= x mod M < c_s + f_s, then x = f_s (x div M) +
+ *   (x mod M) - c_s and, if x < L, x = 65536 x + the next word; words are
+ *   read in step order (step t decodes bytes 64t .. 64t + 63), lanes in
+ *   ascending order within a step. Every state ends at L. Only B >= 16.
  * total = 64 + the padded sections, always a multiple of 16, so shards
  * placed back to back keep every shard 16-byte aligned.
  *
@@ -77,6 +93,8 @@ enum ciera_status {
 #define CIERA_DEVERR_FORMAT 0x1u   /* header magic/version/mode/n/B mismatch */
 #define CIERA_DEVERR_ALIGN 0x2u    /* a shard offset not 16-byte aligned */
 #define CIERA_DEVERR_BOUNDS 0x4u   /* bitmap flags more blocks than E holds */
+#define CIERA_DEVERR_NOSPACE 0x8u  /* an rANS-coded shard met a workspace
+                                      sized without CIERA_WS_ANS */
 
 /* ciera_encode flags */
 #define CIERA_ENC_RAW 0x1u /* emit the uncompressed form (first gather after
@@ -87,9 +105,13 @@ enum ciera_status {
 uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems);
 
 /* Workspace bytes for encoding an n-value shard and for decoding (or cache
- * updating) `nshards` such shards at block size B (host). */
+ * updating) `nshards` such shards at block size B (host). With
+ * CIERA_WS_ANS (B >= 16) it also covers ciera_ans_code on such a shard and
+ * decoding rANS-coded shards: about 2.1 n bytes for coding, n per shard for
+ * decoding. Returns 0 for an unsupported B or flag. */
+#define CIERA_WS_ANS 0x1u
 uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
-                               uint32_t block_elems);
+                               uint32_t block_elems, uint32_t flags);
 
 /* Zero the workspace (a fill kernel on `stream`, capturable). Required once
  * before the first call that uses the workspace. */
@@ -125,13 +147,28 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
  * For every shard j it patches exp_cache[j*shard_elems ...] with the changed
  * blocks' exponents and writes the exact values to out[j*shard_elems ...]
  * (the Merge step); raw shards are copied and seed the cache. Compressed
- * shards must have been encoded with block_elems. Decoding is idempotent: a
+ * shards must have been encoded with block_elems. rANS-coded shards (mode 2)
+ * are decoded first into the workspace, which must then be sized with
+ * CIERA_WS_ANS (else CIERA_DEVERR_NOSPACE). Decoding is idempotent: a
  * second call with the same gathered buffer gives the same out and cache. */
 int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
                           uint32_t block_elems, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream);
+
+/* Entropy coding of the exception section (Section 3.1: the changed
+ * exponents travel ANS-coded), in place on an encoded shard of n values at
+ * block size B >= 16: when the rANS-coded section (format above) is smaller
+ * than the E raw exception bytes, the shard becomes mode 2 and its total
+ * shrinks; otherwise, and for raw or already coded shards, it is left as it
+ * is. *out_bytes (device, may be NULL) receives the total afterwards. Bytes
+ * of the buffer past the new total are unspecified. The workspace must hold
+ * ciera_workspace_bytes(n, 1, B, CIERA_WS_ANS). Deterministic: the same shard
+ * always gives the same bytes. */
+int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
+                   uint64_t *out_bytes, void *workspace,
+                   uint64_t workspace_bytes, hipStream_t stream);
 
 /* The ExpCache patch of Algorithm 1 alone for one encoded shard: afterwards
  * exp_cache holds the exponents of the values that were encoded (changed

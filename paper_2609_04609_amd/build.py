@@ -12,7 +12,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libciera.so")
-SOURCES = ["ciera_kernels.hip", "ciera_api.cpp", "ciera_select.cpp"]
+SOURCES = ["ciera_kernels.hip", "ciera_ans.hip", "ciera_api.cpp",
+           "ciera_select.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed-fp32 instructions are disabled for every device compile: the codec

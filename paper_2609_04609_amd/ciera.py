@@ -17,8 +17,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libciera.so")
 
 OK, EINVAL, ENOSPC, EUNSUPPORTED, EFORMAT, EHIP = 0, -1, -2, -3, -4, -5
-DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS = 1, 2, 4
+DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS, DEVERR_NOSPACE = 1, 2, 4, 8
 ENC_RAW = 0x1
+WS_ANS = 0x1
 SELECT_STOP_AT_MISFIT = 0x1
 HEADER_BYTES = 64
 STATUS_NAMES = {OK: "OK", EINVAL: "EINVAL", ENOSPC: "ENOSPC",
@@ -47,7 +48,7 @@ class CostModel(ctypes.Structure):
 _vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
 _SIGS = {
     "ciera_encoded_bound": (_u64, [_u64, _u32]),
-    "ciera_workspace_bytes": (_u64, [_u64, _u32, _u32]),
+    "ciera_workspace_bytes": (_u64, [_u64, _u32, _u32, _u32]),
     "ciera_workspace_init": (_i32, [_vp, _u64, _vp]),
     "ciera_workspace_error": (_i32, [_vp, ctypes.POINTER(_u32), _i32, _vp]),
     "ciera_encode": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64, _vp, _vp,
@@ -55,6 +56,7 @@ _SIGS = {
     "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _vp, _vp, _vp,
                                      _u64, _vp]),
     "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _vp, _u64, _vp]),
+    "ciera_ans_code": (_i32, [_vp, _u64, _u32, _vp, _vp, _u64, _vp]),
     "ciera_hash_blocks": (_i32, [_vp, _u64, _u32, _vp, _vp]),
     "ciera_encode_hashed": (_i32, [_vp, _vp, _vp, _u64, _u32, _vp, _u64, _vp,
                                    _vp, _u64, _vp]),
@@ -99,8 +101,8 @@ def ciera_encoded_bound(n_elems, block_elems):
     return lib().ciera_encoded_bound(n_elems, block_elems)
 
 
-def ciera_workspace_bytes(n_elems, nshards, block_elems):
-    return lib().ciera_workspace_bytes(n_elems, nshards, block_elems)
+def ciera_workspace_bytes(n_elems, nshards, block_elems, flags=0):
+    return lib().ciera_workspace_bytes(n_elems, nshards, block_elems, flags)
 
 
 def ciera_workspace_init(workspace, workspace_bytes, stream):
@@ -134,6 +136,12 @@ def ciera_update_cache(exp_cache, encoded, n_elems, block_elems, workspace,
                        workspace_bytes, stream):
     return lib().ciera_update_cache(exp_cache, encoded, n_elems, block_elems,
                                     workspace, workspace_bytes, stream)
+
+
+def ciera_ans_code(encoded, n_elems, block_elems, out_bytes, workspace,
+                   workspace_bytes, stream):
+    return lib().ciera_ans_code(encoded, n_elems, block_elems, out_bytes,
+                                workspace, workspace_bytes, stream)
 
 
 def ciera_hash_blocks(w, n_elems, block_elems, hash_cache, stream):
@@ -183,10 +191,13 @@ def _ptr(t):
 
 
 class Workspace:
-    """Device workspace sized for a shard size, shard count and B."""
+    """Device workspace sized for a shard size, shard count and B; with
+    ans=True also for rANS coding and decoding (CIERA_WS_ANS)."""
 
-    def __init__(self, n_elems, nshards, block_elems, device="cuda"):
-        self.nbytes = int(ciera_workspace_bytes(n_elems, nshards, block_elems))
+    def __init__(self, n_elems, nshards, block_elems, device="cuda",
+                 ans=False):
+        self.nbytes = int(ciera_workspace_bytes(n_elems, nshards, block_elems,
+                                                WS_ANS if ans else 0))
         if self.nbytes == 0:
             raise CieraError("ciera_workspace_bytes", EUNSUPPORTED)
         self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
@@ -225,6 +236,13 @@ def encode_hashed_t(w_bits, hash_in, hash_out, block_elems, ws, out,
                              out.numel(), _ptr(out_bytes), ws.ptr, ws.nbytes,
                              _stream())
     return _check("ciera_encode_hashed", rc)
+
+
+def ans_code_t(encoded, n_elems, block_elems, ws, out_bytes=None):
+    """rANS-code the exception section of an encoded shard in place."""
+    rc = ciera_ans_code(_ptr(encoded), n_elems, block_elems, _ptr(out_bytes),
+                        ws.ptr, ws.nbytes, _stream())
+    return _check("ciera_ans_code", rc)
 
 
 def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,

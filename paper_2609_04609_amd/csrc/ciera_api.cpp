@@ -39,9 +39,9 @@ uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems) {
 }
 
 uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
-                               uint32_t block_elems) {
+                               uint32_t block_elems, uint32_t flags) {
   const int l = log2_block(block_elems);
-  if (l < 0) return 0;
+  if (l < 0 || (flags & ~CIERA_WS_ANS)) return 0;
   // encode: one count per tile plus the total
   const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n_elems, uint32_t(l)) + 1);
   // decode at B = 1: the same per shard
@@ -49,7 +49,13 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
       l == 0 ? kWsCtlBytes + 4 * uint64_t(nshards ? nshards : 1) *
                                  dec_count_stride(dec_tiles(n_elems))
              : kWsCtlBytes;
-  const uint64_t need = enc > dec ? enc : dec;
+  uint64_t need = enc > dec ? enc : dec;
+  if ((flags & CIERA_WS_ANS) && l >= kAnsMinLog2B) {
+    const uint64_t e = ans_enc_bytes(n_elems);
+    const uint64_t d = ans_dec_bytes(n_elems, nshards ? nshards : 1);
+    const uint64_t ans = ans_ws_offset(n_elems, uint32_t(l)) + (e > d ? e : d);
+    need = ans > need ? ans : need;
+  }
   return (need + 255) & ~uint64_t(255);
 }
 
@@ -63,6 +69,14 @@ bool dec_workspace_ok(uint64_t n, uint32_t nshards, int l, uint64_t bytes) {
 uint32_t *tile_excl_of(void *workspace) {
   return reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
                                       kWsCtlBytes);
+}
+// Room for the exception lists of rANS-coded shards, or nullptr.
+uint8_t *ans_lists_of(void *workspace, uint64_t bytes, uint64_t n,
+                      uint32_t nshards, int l) {
+  if (l < kAnsMinLog2B) return nullptr;
+  const uint64_t off = ans_ws_offset(n, uint32_t(l));
+  if (bytes < off || bytes - off < ans_dec_bytes(n, nshards)) return nullptr;
+  return static_cast<uint8_t *>(workspace) + off;
 }
 }  // namespace
 
@@ -204,7 +218,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   if (!aligned(gathered, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
   if (!dec_workspace_ok(shard_elems, nshards, l, workspace_bytes))
     return CIERA_ENOSPC;
-  DecArgs a;
+  DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(gathered);
   a.offsets = shard_offsets;
   a.n = shard_elems;
@@ -214,8 +228,12 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
   a.tile_excl = tile_excl_of(workspace);
+  a.ans_exc =
+      ans_lists_of(workspace, workspace_bytes, shard_elems, nshards, l);
+  a.ans_stride = pad16(shard_elems);
   const bool vec =
       (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
+  if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
 
@@ -228,7 +246,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
   if (!dec_workspace_ok(n_elems, 1, l, workspace_bytes)) return CIERA_ENOSPC;
-  DecArgs a;
+  DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(encoded);
   a.offsets = nullptr;
   a.n = n_elems;
@@ -238,8 +256,41 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
   a.tile_excl = tile_excl_of(workspace);
+  a.ans_exc = ans_lists_of(workspace, workspace_bytes, n_elems, 1, l);
+  a.ans_stride = pad16(n_elems);
   const bool vec = aligned(exp_cache, 8);
+  if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
+                   uint64_t *out_bytes, void *workspace,
+                   uint64_t workspace_bytes, hipStream_t stream) {
+  const int l = log2_block(block_elems);
+  if (l < 0 || l < kAnsMinLog2B) return CIERA_EUNSUPPORTED;
+  if (!encoded || !workspace) return CIERA_EINVAL;
+  if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
+  const uint64_t off = ans_ws_offset(n_elems, uint32_t(l));
+  if (workspace_bytes < off || workspace_bytes - off < ans_enc_bytes(n_elems))
+    return CIERA_ENOSPC;
+  const uint64_t kmax = ans_kmax(n_elems);
+  uint8_t *base = static_cast<uint8_t *>(workspace) + off;
+  AnsEncArgs a{};
+  a.enc = static_cast<uint8_t *>(encoded);
+  a.n = n_elems;
+  a.log2B = uint32_t(l);
+  a.kmax = uint32_t(kmax);
+  a.out_bytes = out_bytes;
+  a.ctl = static_cast<WsCtl *>(workspace);
+  a.ans = reinterpret_cast<AnsCtl *>(base);
+  uint8_t *p = base + sizeof(AnsCtl);
+  a.counts = reinterpret_cast<uint32_t *>(p);
+  p += (4 * kmax + 255) & ~uint64_t(255);
+  a.states = reinterpret_cast<uint32_t *>(p);
+  p += 256 * kmax;
+  a.words = reinterpret_cast<uint16_t *>(p);
+  return launch_ans_code(a, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
 
 }  // extern "C"

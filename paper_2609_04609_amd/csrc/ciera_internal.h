@@ -13,7 +13,16 @@ constexpr uint32_t kMagic = 0x52454943u;  // "CIER" little-endian
 constexpr uint32_t kVersion = 1u;
 constexpr uint32_t kModeCompressed = 0u;
 constexpr uint32_t kModeRaw = 1u;
+constexpr uint32_t kModeAns = 2u;  // compressed, exception section rANS-coded
 constexpr uint64_t kHeaderBytes = 64u;
+
+// ---- rANS on the exception section (layout in include/ciera.h) ----
+constexpr uint32_t kAnsM = 4096u;       // frequency total, 2^12
+constexpr uint32_t kAnsScale = 12u;
+constexpr uint32_t kAnsL = 65536u;      // state lower bound
+constexpr uint32_t kAnsChunk = 4096u;   // symbols per chunk, 64 per lane
+constexpr uint64_t kAnsFixed = 520u;    // K, chunk size, 256 u16 frequencies
+constexpr uint32_t kAnsStreamMax = 256u + 2u * kAnsChunk;  // bytes per chunk
 
 __host__ __device__ constexpr inline uint64_t pad16(uint64_t x) {
   return (x + 15u) & ~uint64_t(15);
@@ -82,6 +91,10 @@ constexpr int kHashMinLog2B = 4;  // the block hash needs B >= 16
 
 struct DecArgs {
   const uint8_t *gathered;
+  // decoded exception lists of rANS-coded shards, shard j at
+  // ans_exc + j * ans_stride (nullptr: the workspace has no room for them)
+  uint8_t *ans_exc;
+  uint64_t ans_stride;
   const uint64_t *offsets;  // nullptr: one shard at gathered + 0
   uint64_t n;               // values per shard
   uint32_t log2B;
@@ -100,6 +113,48 @@ __host__ __device__ inline uint64_t dec_count_stride(uint64_t tiles) {
   return (tiles + 1 + 3) & ~uint64_t(3);
 }
 
+// ---- rANS workspace (B >= 16) ----
+// The area starts at ans_ws_offset(n, B), past everything else the calls use.
+struct AnsCtl {
+  uint32_t hist[256];  // exception byte counts
+  uint32_t freq[256];  // quantised frequencies (sum kAnsM)
+  uint32_t cum[256];   // their exclusive prefix sums
+  uint32_t K;          // chunks of the shard being coded
+  uint32_t coded;      // 1 when the coded section replaced the raw one
+  uint32_t reserved[254];
+};
+static_assert(sizeof(AnsCtl) == 4096, "rANS control block is 4 KB");
+constexpr int kAnsMinLog2B = 4;  // rANS-coded sections need B >= 16
+inline uint64_t ans_kmax(uint64_t n) { return (n + kAnsChunk - 1) / kAnsChunk; }
+// past the control block and the encode counts, which every B >= 16 call uses
+inline uint64_t ans_ws_offset(uint64_t n, uint32_t log2B) {
+  const uint64_t t = enc_tiles(n, log2B);
+  return (kWsCtlBytes + 4 * (t + 1) + 255) & ~uint64_t(255);
+}
+// coding one shard: control, words per chunk, final states, word slots
+inline uint64_t ans_enc_bytes(uint64_t n) {
+  const uint64_t k = ans_kmax(n);
+  return sizeof(AnsCtl) + ((4 * k + 255) & ~uint64_t(255)) + 256 * k +
+         2 * uint64_t(kAnsChunk) * k;
+}
+// decoding nshards shards: one exception list per shard
+inline uint64_t ans_dec_bytes(uint64_t n, uint32_t nshards) {
+  return uint64_t(nshards) * pad16(n);
+}
+
+struct AnsEncArgs {
+  uint8_t *enc;  // the encoded shard, recoded in place
+  uint64_t n;
+  uint32_t log2B;
+  uint32_t kmax;
+  uint64_t *out_bytes;
+  WsCtl *ctl;
+  AnsCtl *ans;
+  uint32_t *counts;  // words per chunk
+  uint32_t *states;  // 64 final states per chunk
+  uint16_t *words;   // kAnsChunk word slots per chunk, filled from the end
+};
+
 // Launchers (ciera_kernels.hip). Each returns the launch status.
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
 // pass 1 with the hash detector only: a.hash_out receives every block's hash
@@ -108,6 +163,9 @@ hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
                              uint8_t *out, uint64_t *out_bytes, bool vec,
                              hipStream_t s);
 hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s);
+// ciera_ans.hip
+hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s);
+hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s);
 hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s);
 
 }  // namespace ciera

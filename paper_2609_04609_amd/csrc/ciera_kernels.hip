@@ -823,6 +823,7 @@ __global__ __launch_bounds__(kThreads) void encode_raw_kernel(
 // ================================================================ decode ==
 struct ShardView {
   const uint8_t *enc;
+  const uint8_t *exc;  // the exception list (decoded, for rANS-coded shards)
   uint32_t mode;
   uint64_t E;
   bool ok;
@@ -836,6 +837,7 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   const uint64_t off = a.offsets ? a.offsets[j] : 0ull;
   v.enc = a.gathered + off;
   v.ok = false;
+  v.exc = nullptr;
   v.mode = 0;
   v.E = 0;
   if (off & 15ull) {
@@ -845,13 +847,24 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   const uint32_t *h32 = reinterpret_cast<const uint32_t *>(v.enc);
   const uint64_t *h64 = reinterpret_cast<const uint64_t *>(v.enc);
   const uint32_t magic = h32[0], vm = h32[1], hB = h32[2];
-  const uint64_t hn = h64[2], hE = h64[4], htotal = h64[6];
+  const uint64_t hn = h64[2], hE = h64[4], hP = h64[5], htotal = h64[6];
   const uint32_t mode = vm >> 16;
   bool ok = magic == kMagic && (vm & 0xFFFFu) == kVersion && hn == a.n;
+  const uint64_t bm = bitmap_bytes(hn, a.log2B);
   if (ok && mode == kModeCompressed) {
     ok = hB == (1u << a.log2B) && hE <= hn &&
-         htotal == kHeaderBytes + pad16(hn) +
-                       pad16(bitmap_bytes(hn, a.log2B)) + pad16(hE);
+         htotal == kHeaderBytes + pad16(hn) + pad16(bm) + pad16(hE);
+  } else if (ok && mode == kModeAns) {
+    // rANS-coded exceptions (B >= 16): the list was decoded into the
+    // workspace by ans_decode_kernel, which checks the coded section
+    ok = a.log2B >= uint32_t(kAnsMinLog2B) && hB == (1u << a.log2B) &&
+         hE <= hn && hP >= hn + bm + kAnsFixed &&
+         htotal == kHeaderBytes + pad16(hn) + pad16(bm) +
+                       pad16(hP - hn - bm);
+    if (ok && a.ans_exc == nullptr) {
+      if (report) set_error(a.ctl, CIERA_DEVERR_NOSPACE);
+      return v;
+    }
   } else if (ok && mode == kModeRaw) {
     ok = htotal == kHeaderBytes + pad16(2 * hn);
   } else {
@@ -864,6 +877,9 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   v.ok = true;
   v.mode = mode;
   v.E = hE;
+  v.exc = mode == kModeAns
+              ? a.ans_exc + uint64_t(j) * a.ans_stride
+              : v.enc + kHeaderBytes + pad16(hn) + pad16(bm);
   return v;
 }
 
@@ -935,7 +951,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   const uint8_t *const sm_in = sv.enc + kHeaderBytes;
   const uint8_t *const bmp = sm_in + pad16(n);
   const uint32_t *const bmp32 = reinterpret_cast<const uint32_t *>(bmp);
-  const uint8_t *const exc = bmp + pad16(bitmap_bytes(n, log2B));
+  const uint8_t *const exc = sv.exc;
 
   // sign|mantissa bytes first: they do not depend on the bitmap
   uint2 smv[OCT];

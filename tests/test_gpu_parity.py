@@ -34,7 +34,7 @@ def test_encode_matches_oracle(gu, orc, B):
         cache = gu.dev_u8(cache_h)
         from paper_2609_04609_amd import ciera
         ws = ws if ws is not None and ws.nbytes >= ciera.ciera_workspace_bytes(
-            n, 1, B) else ciera.Workspace(max(n, 262147), 1, B)
+            n, 1, B, 0) else ciera.Workspace(max(n, 262147), 1, B)
         out, total, ws = gu.gpu_encode(w2, cache, B, ws)
         expect = orc.encode(gu.host_u16(w2), cache_h, B)
         got = gu.host_u8(out)

@@ -50,6 +50,16 @@ def test_sizes_closed_form(cl, orc):
     for B in [0, 2, 3, 8, 24, 8192]:
         assert cl.ciera_encoded_bound(100, B) == 0
         assert cl.ciera_workspace_bytes(100, 1, B) == 0
+    # room for rANS coding and decoding: at least the coder's word slots
+    # (2 bytes per exception byte) and one list of n bytes per shard
+    for n in [1, 4096, 4097, 25165824]:
+        base = cl.ciera_workspace_bytes(n, 16, 512)
+        ans = cl.ciera_workspace_bytes(n, 16, 512, cl.WS_ANS)
+        assert ans >= base + max(2 * n, 16 * n) and ans % 256 == 0
+        # no rANS at B = 1: the flag adds nothing there
+        assert cl.ciera_workspace_bytes(n, 16, 1, cl.WS_ANS) == \
+            cl.ciera_workspace_bytes(n, 16, 1)
+    assert cl.ciera_workspace_bytes(100, 1, 512, 2) == 0  # unknown flag
 
 
 def test_host_argument_checks(cl):
@@ -108,6 +118,15 @@ def test_host_argument_checks(cl):
                                   bound - 1, 0, fake, ws_bytes, 0) == cl.ENOSPC
     assert cl.ciera_encode_hashed(fake, fake, fake, 1000, 512, fake, bound, 0,
                                   fake, 256, 0) == cl.ENOSPC
+    # rANS coding: B = 1, null, misaligned, workspace without the rANS room
+    ws_ans = cl.ciera_workspace_bytes(1000, 1, 512, cl.WS_ANS)
+    assert cl.ciera_ans_code(fake, 1000, 1, 0, fake, ws_ans, 0) == \
+        cl.EUNSUPPORTED
+    assert cl.ciera_ans_code(0, 1000, 512, 0, fake, ws_ans, 0) == cl.EINVAL
+    assert cl.ciera_ans_code(fake + 8, 1000, 512, 0, fake, ws_ans, 0) == \
+        cl.EINVAL
+    assert cl.ciera_ans_code(fake, 1000, 512, 0, fake, ws_bytes, 0) == \
+        cl.ENOSPC
     assert L is not None
 
 
