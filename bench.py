@@ -219,6 +219,88 @@ def time_encode_hashed(S, steps, stream, cache_is_w2):
                     "exponent cache; same wire bytes as the exact encode"}
 
 
+def time_ans(S, steps, stream, cache_is_w2):
+    """The exception sections rANS-coded (Section 3.1's ANS step): coding of
+    rank 0's freshly encoded shard (events around ciera_ans_code), and the
+    decode of gathered buffers in which every shard is coded, alternating
+    W -> W' and back like the timed step. Checked bit for bit."""
+    import torch
+    from paper_2609_04609_amd import ciera
+    n, B, R = S.n, S.B, S.R
+    ws1 = ciera.Workspace(n, 1, B, S.dev, ans=True)
+    wsR = ciera.Workspace(n, R, B, S.dev, ans=True)
+
+    def coded_gather(g, off):
+        parts, totals = [], []
+        buf = torch.empty(S.cap, dtype=torch.uint8, device=S.dev)
+        offs = off.cpu().numpy().astype(np.int64)
+        ends = list(offs[1:]) + [g.numel()]
+        for j in range(R):
+            buf[:ends[j] - offs[j]].copy_(g[offs[j]:ends[j]])
+            ciera.ans_code_t(buf, n, B, ws1, out_bytes=S.nbytes)
+            t = int(S.nbytes.item())
+            totals.append(t)
+            parts.append(buf[:t].clone())
+        o = np.cumsum([0] + totals[:-1]).astype(np.int64)
+        gg = torch.cat(parts)
+        return gg, torch.from_numpy(o).to(S.dev), totals
+
+    gA, oA, tA = coded_gather(S.gA, S.offA)
+    gB, oB, tB = coded_gather(S.gB, S.offB)
+    h = gA[:64].cpu().numpy()
+    mode0 = int(h[6:8].view(np.uint16)[0])
+    bm = -(-(-(-n // B)) // 8)
+    C0 = int(h[40:48].view(np.uint64)[0]) - n - bm if mode0 == 2 else None
+    # coding time: encode (fresh mode-0 bytes) then code, events between
+    w_in = S.W[:n] if cache_is_w2 else S.W2[:n]
+    out = torch.empty_like(S.tmp)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+           for _ in range(steps)]
+    for i in range(steps + 3):
+        e = evs[i - 3] if i >= 3 else None
+        if e: e[0].record(stream)
+        ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, out)
+        if e: e[1].record(stream)
+        ciera.ans_code_t(out, n, B, ws1)
+        if e: e[2].record(stream)
+    torch.cuda.synchronize()
+    t_code = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
+    # decode of the coded buffers, starting on the side the caches are at
+    pairs = [(gB, oB, S.W), (gA, oA, S.W2)] if cache_is_w2 else \
+        [(gA, oA, S.W2), (gB, oB, S.W)]
+    dev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+           for _ in range(steps)]
+    for i in range(steps):
+        g, o, _ = pairs[i % 2]
+        dev[i][0].record(stream)
+        ciera.decode_gathered_t(g, o, n, B, S.out, S.cache, wsR)
+        dev[i][1].record(stream)
+    torch.cuda.synchronize()
+    expect = pairs[(steps - 1) % 2][2]
+    if not torch.equal(S.out, expect) or wsR.error() != 0:
+        raise RuntimeError("rANS-coded decode is not exact")
+    # put the caches back on the side the rest of the bench expects
+    if steps % 2 == 1:
+        g, o, _ = pairs[1]
+        ciera.decode_gathered_t(g, o, n, B, S.out, S.cache, wsR)
+        torch.cuda.synchronize()
+    t_dec = np.mean([a.elapsed_time(b) for a, b in dev]) / 1e3
+    E0 = S.E0
+    q_eff = (C0 if C0 is not None else E0) / n
+    dec, gain = ciera.ciera_should_compress(n, B, q_eff, R, 10e-6, 8e9,
+                                            t_decmp_s=t_dec)
+    return {"wire_ratio": round(sum(tA) / (2.0 * R * n), 5),
+            "exceptions_local": E0,
+            "coded_exceptions_local": C0,
+            "code_us": round(t_code * 1e6, 2),
+            "decode_us": round(t_dec * 1e6, 2),
+            "decode_bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
+            "should_compress": {"decision": int(dec), "gain_s": gain,
+                                "q_effective": round(q_eff, 5)},
+            "note": "exception sections rANS-coded (mode 2); decode = "
+                    "ans_decode_kernel + decode_kernel"}
+
+
 def cpu_baseline(setup, min_s=10.0, max_s=30.0):
     """The oracle on the host cores, on the same bytes as the GPU step:
     encode of rank 0's shard (one thread), then decode of the R gathered
@@ -350,6 +432,8 @@ def run(args):
 
     hashed = (time_encode_hashed(S, args.steps, stream, last_even)
               if B >= 16 else None)
+    ans = (time_ans(S, args.steps, stream, last_even)
+           if B >= 16 and args.ans else None)
 
     t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
     t_upd = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
@@ -383,6 +467,7 @@ def run(args):
                    "hbm_frac": round(b_enc / t_enc / 1e9 / HBM_PEAK_GBPS, 4),
                    "alg_bytes": b_enc},
         "encode_hashed": hashed,
+        "ans": ans,
         "update_cache": {"us": round(t_upd * 1e6, 2),
                          "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
                          "alg_bytes": b_upd},
@@ -429,6 +514,8 @@ def main():
     ap.add_argument("--block", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline",
                     action="store_false")
+    ap.add_argument("--no-ans", dest="ans", action="store_false",
+                    help="skip the rANS-coded exception measurements")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")

@@ -401,22 +401,24 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
     const uint64_t lo = uint64_t(c) * kAnsChunk;
     const uint32_t len = uint32_t(E - lo < kAnsChunk ? E - lo : kAnsChunk);
     uint8_t *dst = list + lo;
+    // Branch-free steps: every lane decodes, lanes past the chunk's end keep
+    // their state; the word read is clamped into the stream and used only
+    // by the lanes that need one.
+    const uint32_t last = nwords ? nwords - 1u : 0u;
     for (uint32_t t = 0; t < (len + 63) / 64; ++t) {
       const uint32_t i = t * 64 + uint32_t(lane);
       const bool live = i < len;
       const uint32_t e = s_slot[x & (kAnsM - 1u)];
-      if (live) {
-        x = (((e >> 8) & 0xFFFu) + 1u) * (x >> kAnsScale) + (e >> 20);
-        dst[i] = uint8_t(e & 0xFFu);
-      }
+      const uint32_t xd =
+          (((e >> 8) & 0xFFFu) + 1u) * (x >> kAnsScale) + (e >> 20);
+      if (live) dst[i] = uint8_t(e & 0xFFu);
+      x = live ? xd : x;
       const bool need = live && x < kAnsL;
       const uint64_t m = __ballot(need);
-      if (need) {
-        const uint32_t idx = rd + lanes_below(m);
-        uint32_t w = 0;
-        if (idx < nwords) w = wq[idx]; else bad = true;
-        x = (x << 16) | w;
-      }
+      const uint32_t idx = rd + lanes_below(m);
+      const uint32_t w = wq[idx < last ? idx : last];
+      bad = bad || (need && idx >= nwords);
+      x = need ? ((x << 16) | w) : x;
       rd += uint32_t(__popcll(m));
     }
     // every state back at L, the words used up, only zero padding after
