@@ -301,6 +301,42 @@ def time_ans(S, steps, stream, cache_is_w2):
                     "ans_decode_kernel + decode_kernel"}
 
 
+XGMI_GATHER_BPS = 7 * 153e9  # one MI355X's 7 xGMI links, direct gather
+
+
+def time_overlap(S, layers, steps, cache_is_w2):
+    """Section 3.3 on one GPU: L layer groups, sequential vs overlapped
+    (sender, link, receiver and compute streams joined by events); the
+    Allgather is a spin kernel lasting its alpha-beta time on the xGMI
+    links. Every layer's output is checked bit for bit."""
+    from paper_2609_04609_amd.pipeline import OverlapPipeline
+    P = OverlapPipeline(S, layers, XGMI_GATHER_BPS,
+                        caches_hold_w2=cache_is_w2)
+    comp = P.component_us()
+    res = {}
+    for mode in (False, True):
+        P.step(mode)  # warm-up
+        P.step(mode)
+        ts = [P.step(mode) for _ in range(2 * steps)]
+        if not P.check():
+            raise RuntimeError("overlap schedule output is not exact")
+        res["overlapped" if mode else "sequential"] = float(np.median(ts))
+    link = float(np.mean(P.link_us))
+    floor = layers * link + comp["decode"] + comp["compute"]
+    out = {"layers": layers,
+           "link": (f"alpha 10 us + (R-1) x / {XGMI_GATHER_BPS / 1e9:.0f} "
+                    "GB/s (7 xGMI links of 153 GB/s, direct gather)"),
+           "sequential_us": round(res["sequential"], 1),
+           "overlapped_us": round(res["overlapped"], 1),
+           "speedup": round(res["sequential"] / res["overlapped"], 3),
+           "per_layer_us": comp,
+           "link_bound_us": round(floor, 1),
+           "note": "link_bound_us = L x link + one decode + one compute: "
+                   "the overlapped schedule's floor"}
+    del P
+    return out
+
+
 def cpu_baseline(setup, min_s=10.0, max_s=30.0):
     """The oracle on the host cores, on the same bytes as the GPU step:
     encode of rank 0's shard (one thread), then decode of the R gathered
@@ -434,6 +470,9 @@ def run(args):
               if B >= 16 else None)
     ans = (time_ans(S, args.steps, stream, last_even)
            if B >= 16 and args.ans else None)
+    overlap = (time_overlap(S, args.overlap_layers, 3, last_even)
+               if args.overlap_layers > 0 and wl.name.startswith("olmoe_layer")
+               else None)
 
     t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
     t_upd = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
@@ -468,6 +507,7 @@ def run(args):
                    "alg_bytes": b_enc},
         "encode_hashed": hashed,
         "ans": ans,
+        "overlap": overlap,
         "update_cache": {"us": round(t_upd * 1e6, 2),
                          "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
                          "alg_bytes": b_upd},
@@ -516,6 +556,8 @@ def main():
                     action="store_false")
     ap.add_argument("--no-ans", dest="ans", action="store_false",
                     help="skip the rANS-coded exception measurements")
+    ap.add_argument("--overlap-layers", type=int, default=4,
+                    help="layer groups in the overlap measurement (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")
