@@ -28,6 +28,8 @@
 #define OR_MODE_ANS 2u /* compressed, exception section rANS-coded */
 #define OR_HEADER 64u
 #define OR_ANS_FIXED 520u /* coded section: K, chunk size, 256 frequencies */
+#define OR_DTYPE_BF16 0u  /* header offset 12: the value format */
+#define OR_DTYPE_FP16 1u
 
 static uint64_t round16(uint64_t x) { return (x + 15u) / 16u * 16u; }
 
@@ -495,6 +497,7 @@ static int read_header(const uint8_t *enc, uint64_t n, uint32_t *mode,
     return -4;
   *B = get_u32(enc + 8);
   if (*B == 0) return -4;
+  if (get_u32(enc + 12) != OR_DTYPE_BF16) return -4;
   if (get_u64(enc + 16) != n) return -4;
   *E = get_u64(enc + 32);
   if (*E > n) return -4;
@@ -631,6 +634,182 @@ uint64_t oracle_ans_code_shard(uint8_t *enc, uint64_t n) {
   }
   free(section);
   return total;
+}
+
+/* ---- FP16 (the paper's second precision, Table 2) ----
+ * fp16 = sign (bit 15) | exponent (bits 14..10, 5 bits) | mantissa (bits
+ * 9..0). The paper's sizes generalise as S_e = 5n/8 and S_{s+m} = 11n/8
+ * bytes; the layout is a reading (the paper fixes none):
+ *   - the exponent cache keeps one byte per value (the 5-bit field);
+ *   - sign+mantissa section: the low 8 mantissa bits of every value (n
+ *     bytes), then for each octet j of values 3 bytes at n + 3j, byte p
+ *     holding bit p of (sign << 2 | mantissa bits 9..8) of value 8j + k in
+ *     bit k: n + 3 ceil(n/8) bytes;
+ *   - exceptions: the changed blocks' 5-bit exponents in block order, each
+ *     group g of 8 as 5 bytes at 5g, byte p holding bit p of exponent
+ *     8g + k in bit k: 5 ceil(E/8) bytes (E = number of exponents);
+ *   - the bitmap, header and alignment as for bf16, with 1 at offset 12.
+ * P = n + 3 ceil(n/8) + bitmap bytes + 5 ceil(E/8). Raw form as for bf16. */
+void oracle_split_f16(const uint16_t *w, uint64_t n, uint8_t *e, uint8_t *lo,
+                      uint8_t *hi3) {
+  for (uint64_t k = 0; k < n; k++) {
+    uint16_t x = w[k];
+    uint8_t sign = (uint8_t)(x >> 15);
+    e[k] = (uint8_t)((x >> 10) & 0x1Fu);
+    lo[k] = (uint8_t)(x & 0xFFu);
+    hi3[k] = (uint8_t)((sign << 2) | ((x >> 8) & 0x3u));
+  }
+}
+
+static uint16_t merge_one_f16(uint8_t expo, uint8_t lo, uint8_t hi3) {
+  uint16_t sign = (uint16_t)((hi3 >> 2) & 1u);
+  uint16_t mant = (uint16_t)(((uint16_t)(hi3 & 3u) << 8) | lo);
+  return (uint16_t)((sign << 15) | ((uint16_t)expo << 10) | mant);
+}
+
+static uint64_t f16_sm_bytes(uint64_t n) { return n + 3u * ceil_div(n, 8u); }
+
+uint64_t oracle_encoded_bound_f16(uint64_t n, uint64_t B) {
+  if (B == 0) return 0;
+  uint64_t compressed = OR_HEADER + round16(f16_sm_bytes(n)) +
+                        round16(bitmap_bytes(n, B)) +
+                        round16(5u * ceil_div(n, 8u));
+  uint64_t raw = OR_HEADER + round16(2u * n);
+  return compressed > raw ? compressed : raw;
+}
+
+uint64_t oracle_encode_f16(const uint16_t *w, const uint8_t *cache, uint64_t n,
+                           uint64_t B, int raw, uint8_t *out, uint64_t out_cap) {
+  if (B == 0 || B > 0xFFFFFFFFu) return 0;
+  if (out_cap < oracle_encoded_bound_f16(n, B)) return 0;
+  if (raw) {
+    uint64_t total = OR_HEADER + round16(2u * n);
+    memset(out, 0, total);
+    write_header(out, OR_MODE_RAW, B, n, 0, 0, 2u * n, total);
+    put_u32(out + 12, OR_DTYPE_FP16);
+    for (uint64_t k = 0; k < n; k++) put_u16(out + OR_HEADER + 2u * k, w[k]);
+    return total;
+  }
+  if (cache == NULL && n > 0) return 0;
+  uint8_t *expo = (uint8_t *)malloc(n ? n : 1);
+  uint8_t *lo = (uint8_t *)malloc(n ? n : 1);
+  uint8_t *hi3 = (uint8_t *)malloc(n ? n : 1);
+  oracle_split_f16(w, n, expo, lo, hi3);
+  /* block flags, exactly as for bf16 */
+  uint64_t nb = num_blocks(n, B);
+  uint8_t *flag = (uint8_t *)calloc(nb ? nb : 1, 1);
+  for (uint64_t b = 0; b < nb; b++) {
+    uint64_t a = b * B, z = a + B < n ? a + B : n;
+    for (uint64_t k = a; k < z; k++)
+      if (expo[k] != cache[k]) flag[b] = 1;
+  }
+  uint64_t bm = bitmap_bytes(n, B), changed = 0, E = 0;
+  uint8_t *list = (uint8_t *)malloc(n ? n : 1);
+  for (uint64_t b = 0; b < nb; b++) {
+    if (!flag[b]) continue;
+    changed++;
+    uint64_t a = b * B, z = a + B < n ? a + B : n;
+    for (uint64_t k = a; k < z; k++) list[E++] = expo[k];
+  }
+  uint64_t S_sm = f16_sm_bytes(n), S_exc = 5u * ceil_div(E, 8u);
+  uint64_t off_sm = OR_HEADER, off_bm = off_sm + round16(S_sm);
+  uint64_t off_exc = off_bm + round16(bm);
+  uint64_t total = off_exc + round16(S_exc);
+  memset(out, 0, total);
+  write_header(out, OR_MODE_COMPRESSED, B, n, changed, E, S_sm + bm + S_exc,
+               total);
+  put_u32(out + 12, OR_DTYPE_FP16);
+  uint8_t *sm = out + off_sm;
+  for (uint64_t k = 0; k < n; k++) {
+    sm[k] = lo[k];
+    for (uint32_t p = 0; p < 3u; p++)
+      sm[n + 3u * (k / 8u) + p] |= (uint8_t)(((hi3[k] >> p) & 1u) << (k % 8u));
+  }
+  for (uint64_t b = 0; b < nb; b++)
+    if (flag[b]) out[off_bm + b / 8u] |= (uint8_t)(1u << (b % 8u));
+  for (uint64_t i = 0; i < E; i++)
+    for (uint32_t p = 0; p < 5u; p++)
+      out[off_exc + 5u * (i / 8u) + p] |=
+          (uint8_t)(((list[i] >> p) & 1u) << (i % 8u));
+  free(expo);
+  free(lo);
+  free(hi3);
+  free(flag);
+  free(list);
+  return total;
+}
+
+/* Header check for an fp16 shard; *S_exc receives the exception section's
+ * bytes. */
+static int read_header_f16(const uint8_t *enc, uint64_t n, uint32_t *mode,
+                           uint64_t *B, uint64_t *E) {
+  if (get_u32(enc + 0) != OR_MAGIC || get_u16(enc + 4) != OR_VERSION)
+    return -4;
+  if (get_u32(enc + 12) != OR_DTYPE_FP16) return -4;
+  *mode = get_u16(enc + 6);
+  *B = get_u32(enc + 8);
+  *E = get_u64(enc + 32);
+  if (*B == 0 || get_u64(enc + 16) != n || *E > n) return -4;
+  if (*mode == OR_MODE_RAW)
+    return get_u64(enc + 48) == OR_HEADER + round16(2u * n) ? 0 : -4;
+  if (*mode != OR_MODE_COMPRESSED) return -4;
+  uint64_t bm = bitmap_bytes(n, *B), want = 0;
+  const uint8_t *bitmap = enc + OR_HEADER + round16(f16_sm_bytes(n));
+  for (uint64_t b = 0; b < num_blocks(n, *B); b++) {
+    if ((bitmap[b / 8u] >> (b % 8u)) & 1) {
+      uint64_t a = b * *B, z = a + *B < n ? a + *B : n;
+      want += z - a;
+    }
+  }
+  if (want != *E) return -4;
+  if (get_u64(enc + 48) != OR_HEADER + round16(f16_sm_bytes(n)) +
+                               round16(bm) + round16(5u * ceil_div(*E, 8u)))
+    return -4;
+  return 0;
+}
+
+int oracle_update_cache_f16(uint8_t *cache, const uint8_t *enc, uint64_t n) {
+  uint32_t mode;
+  uint64_t B, E;
+  int rc = read_header_f16(enc, n, &mode, &B, &E);
+  if (rc) return rc;
+  if (mode == OR_MODE_RAW) {
+    for (uint64_t k = 0; k < n; k++)
+      cache[k] = (uint8_t)((get_u16(enc + OR_HEADER + 2u * k) >> 10) & 0x1Fu);
+    return 0;
+  }
+  const uint8_t *bitmap = enc + OR_HEADER + round16(f16_sm_bytes(n));
+  const uint8_t *exc = bitmap + round16(bitmap_bytes(n, B));
+  uint64_t i = 0; /* next exception */
+  for (uint64_t b = 0; b < num_blocks(n, B); b++) {
+    if (!((bitmap[b / 8u] >> (b % 8u)) & 1)) continue;
+    uint64_t a = b * B, z = a + B < n ? a + B : n;
+    for (uint64_t k = a; k < z; k++, i++) {
+      uint8_t v = 0;
+      for (uint32_t p = 0; p < 5u; p++)
+        v |= (uint8_t)(((exc[5u * (i / 8u) + p] >> (i % 8u)) & 1u) << p);
+      cache[k] = v;
+    }
+  }
+  return 0;
+}
+
+int oracle_decode_f16(const uint8_t *enc, uint64_t n, uint8_t *cache,
+                      uint16_t *out) {
+  int rc = oracle_update_cache_f16(cache, enc, n);
+  if (rc) return rc;
+  if (get_u16(enc + 6) == OR_MODE_RAW) {
+    for (uint64_t k = 0; k < n; k++) out[k] = get_u16(enc + OR_HEADER + 2u * k);
+    return 0;
+  }
+  const uint8_t *sm = enc + OR_HEADER;
+  for (uint64_t k = 0; k < n; k++) {
+    uint8_t hi3 = 0;
+    for (uint32_t p = 0; p < 3u; p++)
+      hi3 |= (uint8_t)(((sm[n + 3u * (k / 8u) + p] >> (k % 8u)) & 1u) << p);
+    out[k] = merge_one_f16(cache[k], sm[k], hi3);
+  }
+  return 0;
 }
 
 /* Section 3.2 gain:

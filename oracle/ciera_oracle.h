@@ -98,6 +98,16 @@ int oracle_ans_decode_section(const uint8_t *section, uint64_t C, uint64_t E,
  * or 0 when the header does not describe an n-value shard. */
 uint64_t oracle_ans_code_shard(uint8_t *enc, uint64_t n);
 
+/* ---- FP16 shards (Table 2's second precision; layout in the .c file) ---- */
+void oracle_split_f16(const uint16_t *w, uint64_t n, uint8_t *e, uint8_t *lo,
+                      uint8_t *hi3);
+uint64_t oracle_encoded_bound_f16(uint64_t n, uint64_t B);
+uint64_t oracle_encode_f16(const uint16_t *w, const uint8_t *cache, uint64_t n,
+                           uint64_t B, int raw, uint8_t *out, uint64_t out_cap);
+int oracle_decode_f16(const uint8_t *enc, uint64_t n, uint8_t *cache,
+                      uint16_t *out);
+int oracle_update_cache_f16(uint8_t *cache, const uint8_t *enc, uint64_t n);
+
 /* Decode one encoded shard of n elements against cache (updated in place to
  * the exponents of the decoded values). Returns 0, or a negative code when
  * the header does not describe an n-element shard. */

@@ -91,6 +91,18 @@ def _bind(lib):
                                               ctypes.c_uint64, _u8p]
     lib.oracle_ans_code_shard.restype = ctypes.c_uint64
     lib.oracle_ans_code_shard.argtypes = [_u8p, ctypes.c_uint64]
+    lib.oracle_split_f16.restype = None
+    lib.oracle_split_f16.argtypes = [_u16p, ctypes.c_uint64, _u8p, _u8p, _u8p]
+    lib.oracle_encoded_bound_f16.restype = ctypes.c_uint64
+    lib.oracle_encoded_bound_f16.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+    lib.oracle_encode_f16.restype = ctypes.c_uint64
+    lib.oracle_encode_f16.argtypes = [_u16p, _u8p, ctypes.c_uint64,
+                                      ctypes.c_uint64, ctypes.c_int, _u8p,
+                                      ctypes.c_uint64]
+    lib.oracle_decode_f16.restype = ctypes.c_int
+    lib.oracle_decode_f16.argtypes = [_u8p, ctypes.c_uint64, _u8p, _u16p]
+    lib.oracle_update_cache_f16.restype = ctypes.c_int
+    lib.oracle_update_cache_f16.argtypes = [_u8p, _u8p, ctypes.c_uint64]
     lib.oracle_encode_hashed.restype = ctypes.c_uint64
     lib.oracle_encode_hashed.argtypes = [_u16p, _u64p, _u64p, ctypes.c_uint64,
                                          ctypes.c_uint64, _u8p,
@@ -292,6 +304,61 @@ class Oracle:
             raise ValueError("oracle_ans_code_shard: bad shard")
         return buf[:total].copy()
 
+    # ---- FP16 shards (Table 2's second precision) ----
+
+    def split_f16(self, w):
+        """(5-bit exponents, low mantissa bytes, sign<<2 | mantissa bits 9..8)"""
+        w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
+        e, lo, hi = (np.empty(w.size, np.uint8) for _ in range(3))
+        self._lib.oracle_split_f16(_ptr(w, _u16p), w.size, _ptr(e, _u8p),
+                                   _ptr(lo, _u8p), _ptr(hi, _u8p))
+        return e, lo, hi
+
+    def encoded_bound_f16(self, n, B):
+        return int(self._lib.oracle_encoded_bound_f16(n, B))
+
+    def encode_f16(self, w, cache, B, raw=False):
+        w = np.ascontiguousarray(w, dtype=np.uint16).ravel()
+        n = w.size
+        cap = self.encoded_bound_f16(n, B)
+        out = np.full(cap, 0xA5, np.uint8)
+        if cache is None:
+            cptr = ctypes.cast(None, _u8p)
+        else:
+            cache = np.ascontiguousarray(cache, dtype=np.uint8).ravel()
+            assert cache.size == n
+            cptr = _ptr(cache, _u8p)
+        total = self._lib.oracle_encode_f16(_ptr(w, _u16p), cptr, n, B,
+                                            int(raw), _ptr(out, _u8p), cap)
+        if total == 0 or total > cap:
+            raise ValueError("oracle_encode_f16 rejected its arguments")
+        return out[:total].copy()
+
+    def decode_f16(self, enc, n, cache):
+        enc = np.ascontiguousarray(enc, dtype=np.uint8)
+        assert cache.dtype == np.uint8 and cache.flags["C_CONTIGUOUS"]
+        out = np.empty(n, np.uint16)
+        if self._lib.oracle_decode_f16(_ptr(enc, _u8p), n, _ptr(cache, _u8p),
+                                       _ptr(out, _u16p)):
+            raise ValueError("oracle_decode_f16: bad shard")
+        return out
+
+    def update_cache_f16(self, cache, enc, n):
+        enc = np.ascontiguousarray(enc, dtype=np.uint8)
+        if self._lib.oracle_update_cache_f16(_ptr(cache, _u8p),
+                                             _ptr(enc, _u8p), n):
+            raise ValueError("oracle_update_cache_f16: bad shard")
+
+    def decode_gathered_f16(self, gathered, offsets, n_s, cache):
+        out = np.empty(len(offsets) * n_s, np.uint16)
+        for j, off in enumerate(offsets):
+            c = cache[j * n_s:(j + 1) * n_s]
+            cj = np.ascontiguousarray(c)
+            out[j * n_s:(j + 1) * n_s] = self.decode_f16(
+                np.asarray(gathered)[int(off):], n_s, cj)
+            cache[j * n_s:(j + 1) * n_s] = cj
+        return out
+
     header = staticmethod(lambda enc: header(enc))
 
 
@@ -393,9 +460,34 @@ def header(enc: np.ndarray) -> dict:
         "version": int(h[4:6].view(np.uint16)[0]),
         "mode": int(h[6:8].view(np.uint16)[0]),
         "B": int(h[8:12].view(np.uint32)[0]),
+        "dtype": int(h[12:16].view(np.uint32)[0]),
         "n": int(u64[2]),
         "changed_blocks": int(u64[3]),
         "E": int(u64[4]),
         "P": int(u64[5]),
         "total": int(u64[6]),
     }
+
+
+def split_f16(w):
+    return _oracle().split_f16(w)
+
+
+def encoded_bound_f16(n, B):
+    return _oracle().encoded_bound_f16(n, B)
+
+
+def encode_f16(w, cache, B, raw=False):
+    return _oracle().encode_f16(w, cache, B, raw)
+
+
+def decode_f16(enc, n, cache):
+    return _oracle().decode_f16(enc, n, cache)
+
+
+def update_cache_f16(cache, enc, n):
+    return _oracle().update_cache_f16(cache, enc, n)
+
+
+def decode_gathered_f16(gathered, offsets, n_s, cache):
+    return _oracle().decode_gathered_f16(gathered, offsets, n_s, cache)

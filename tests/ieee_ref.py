@@ -57,3 +57,46 @@ def mantissa7(bits: np.ndarray) -> np.ndarray:
 
 def all_bf16_patterns() -> np.ndarray:
     return np.arange(65536, dtype=np.uint32).astype(np.uint16)
+
+
+# ---- binary16 (fp16) ----
+
+def f16_values(bits: np.ndarray) -> np.ndarray:
+    b = np.asarray(bits).astype(np.uint16)
+    return b.view(np.float16).astype(np.float64)
+
+
+def exponent_field_f16(bits: np.ndarray) -> np.ndarray:
+    """Biased 5-bit exponent from the value: 0 for zero and subnormals, 31
+    for Inf/NaN, otherwise floor(log2|x|) + 15."""
+    with np.errstate(invalid="ignore"):
+        x = f16_values(bits)
+    out = np.zeros(x.shape, np.int64)
+    special = ~np.isfinite(x)
+    out[special] = 31
+    ax = np.abs(np.where(special, 0.0, x))
+    normal = ax >= 2.0 ** -14
+    _, ex = np.frexp(ax[normal])
+    out[normal] = ex - 1 + 15
+    return out.astype(np.uint8)
+
+
+def mantissa10_f16(bits: np.ndarray) -> np.ndarray:
+    """The 10 stored fraction bits of finite values, from the magnitude
+    (normal: (1 + m/1024) 2^(e-15); subnormal: m 2^-24); -1 otherwise."""
+    with np.errstate(invalid="ignore"):
+        x = f16_values(bits)
+    out = np.full(x.shape, -1, np.int64)
+    fin = np.isfinite(x)
+    ax = np.abs(np.where(fin, x, 0.0))
+    e = exponent_field_f16(bits).astype(np.int64)
+    normal = fin & (e > 0)
+    sub = fin & (e == 0)
+    out[normal] = np.rint((ax[normal] / 2.0 ** (e[normal] - 15) - 1.0) * 1024)
+    out[sub] = np.rint(ax[sub] * 2.0 ** 24)
+    return out
+
+
+def sign_f16(bits: np.ndarray) -> np.ndarray:
+    with np.errstate(invalid="ignore"):
+        return np.signbit(f16_values(bits)).astype(np.uint8)

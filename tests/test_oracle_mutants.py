@@ -4,8 +4,8 @@ Each case plants one mistake in a copy of oracle/ciera_oracle.c (on the CPU
 only), builds it with gcc, and runs a condensed set of the pins against it:
 IEEE-semantics field extraction, brute force over old exponents, the
 hand-worked wire fixtures, closed-form sizes and zero padding, the raw form,
-a hand-computed gain and a hand-ranked selection, the block-hash pins and
-the rANS pins. Every mutant must fail at
+a hand-computed gain and a hand-ranked selection, the block-hash pins,
+the rANS pins and the fp16 pins. Every mutant must fail at
 least one of them; the real oracle must pass all of them.
 """
 import os
@@ -84,6 +84,15 @@ MUTANTS = [
      "uint64_t words = len / 8u;"),
     ("finaliser shift", "z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;",
      "z = (z ^ (z >> 28)) * 0x94D049BB133111EBull;"),
+    ("fp16 exponent shift", "e[k] = (uint8_t)((x >> 10) & 0x1Fu);",
+     "e[k] = (uint8_t)((x >> 11) & 0x1Fu);"),
+    ("fp16 high mantissa bits", "hi3[k] = (uint8_t)((sign << 2) | ((x >> 8) & 0x3u));",
+     "hi3[k] = (uint8_t)((sign << 2) | ((x >> 9) & 0x3u));"),
+    ("fp16 exception group stride", "out[off_exc + 5u * (i / 8u) + p] |=",
+     "out[off_exc + 4u * (i / 8u) + p] |="),
+    ("fp16 sign+mantissa size floors",
+     "static uint64_t f16_sm_bytes(uint64_t n) { return n + 3u * ceil_div(n, 8u); }",
+     "static uint64_t f16_sm_bytes(uint64_t n) { return n + 3u * (n / 8u); }"),
     ("select sorts ascending", "if (ry >= rx) break;", "if (ry <= rx) break;"),
     ("select keeps non-positive gains", "if (gain[i] > 0.0) order[m++] = i;",
      "if (gain[i] >= 0.0) order[m++] = i;"),
@@ -299,6 +308,38 @@ def _pins(o):
                 return False
         return True
     check("ans", ans_pins)
+
+    def f16_pins():
+        from tests.test_oracle_f16_pins import ALL, _unpack_groups
+        e, lo, hi = o.split_f16(ALL)
+        if not np.array_equal(e, ieee_ref.exponent_field_f16(ALL)):
+            return False
+        f, expect = _read_golden("worked_example_f16_b2.txt")
+        w = np.array([int(t, 16) for t in f["values_bits"].split()],
+                     np.uint16)
+        cache = np.array([int(t, 16) for t in f["cache"].split()], np.uint8)
+        if not np.array_equal(o.encode_f16(w, cache, 2), expect):
+            return False
+        rng = np.random.default_rng(42)
+        n = 20013
+        w = rng.integers(0, 65536, n, dtype=np.uint32).astype(np.uint16)
+        c = ieee_ref.exponent_field_f16(w)
+        c[rng.random(n) < 0.01] ^= 1
+        for B in (1, 64):
+            enc = o.encode_f16(w, c, B)
+            h = o.header(enc)
+            S_sm = n + 3 * (-(-n // 8))
+            if h["P"] != S_sm + (-(-(-(-n // B)) // 8)) + 5 * (-(-h["E"] // 8)):
+                return False
+            hi3 = _unpack_groups(enc[64 + n:64 + S_sm], n, 3)
+            if not np.array_equal(hi3, (ieee_ref.sign_f16(w).astype(
+                    np.int64) << 2) | ((w.astype(np.int64) >> 8) & 3)):
+                return False
+            c2 = c.copy()
+            if not np.array_equal(o.decode_f16(enc, n, c2), w):
+                return False
+        return True
+    check("fp16", f16_pins)
 
     def select_hand():
         # budget 6.5 MB: 3, 4, 0 fill 6 MB; the zero-gain shard 5 would fit
