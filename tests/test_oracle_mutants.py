@@ -45,8 +45,9 @@ MUTANTS = [
      "static uint64_t round16(uint64_t x) { return (x + 16u) / 16u * 16u; }"),
     ("payload omits the bitmap", "uint64_t P = n + bm + E;", "uint64_t P = n + E;"),
     ("header swaps E and count", "put_u64(out + 32, E);", "put_u64(out + 32, changed);"),
-    ("padding left unwritten", "  memset(out, 0, total);\n  write_header(out, OR_MODE_COMPRESSED",
-     "  write_header(out, OR_MODE_COMPRESSED"),
+    ("padding left unwritten",
+     "  memset(out, 0, total);\n  write_header(out, OR_MODE_COMPRESSED, B, n, nchanged",
+     "  write_header(out, OR_MODE_COMPRESSED, B, n, nchanged"),
     ("decode patches only the first value of a block",
      "for (uint64_t k = lo; k < hi; k++) cache[k] = exc[j++];",
      "cache[lo] = exc[j]; j += hi - lo;"),
