@@ -27,7 +27,7 @@
  * An encoded shard starts with a 64-byte little-endian header:
  *    0 magic u32 0x52454943 ("CIER")  4 version u16 = 1  6 mode u16
  *      (0 compressed, 1 raw, 2 compressed with rANS-coded exceptions)
- *    8 B u32   12 reserved u32 = 0
+ *    8 B u32   12 value format u32 (0 bf16, 1 fp16)
  *   16 n u64 (values)   24 changed blocks u64   32 exception bytes E u64
  *   40 payload bytes P u64   48 total bytes u64   56 reserved u64 = 0
  * compressed body: sign+mantissa plane (n bytes: sign in bit 7, mantissa in
@@ -49,6 +49,17 @@
  *   (x mod M) - c_s and, if x < L, x = 65536 x + the next word; words are
  *   read in step order (step t decodes bytes 64t .. 64t + 63), lanes in
  *   ascending order within a step. Every state ends at L. Only B >= 16.
+ * fp16 shards (CIERA_FP16; the paper's second precision, Table 2), B >= 16:
+ *   the same header, bitmap and modes 0 and 1 (no mode 2). The exponent is 5
+ *   bits (bits 14..10) and the cache keeps one byte per value. The
+ *   sign+mantissa section is the low 8 mantissa bits of every value (n
+ *   bytes), then for every octet j of values 3 bytes at n + 3j, byte q
+ *   holding bit q of (sign << 2 | mantissa bits 9..8) of value 8j + k in bit
+ *   k: n + 3 ceil(n/8) bytes. The exceptions are the changed exponents in
+ *   block order, each group g of 8 as 5 bytes at 5g (byte q: bit q of
+ *   exponent 8g + k in bit k): 5 ceil(E/8) bytes; E counts exponents. P =
+ *   n + 3 ceil(n/8) + bitmap bytes + 5 ceil(E/8), the paper's S_{s+m} =
+ *   11n/8 and S_e = 5n/8.
  * total = 64 + the padded sections, always a multiple of 16, so shards
  * placed back to back keep every shard 16-byte aligned.
  *
@@ -99,10 +110,14 @@ enum ciera_status {
 /* ciera_encode flags */
 #define CIERA_ENC_RAW 0x1u /* emit the uncompressed form (first gather after
                               warm-up; tensors the selection rule leaves out) */
+#define CIERA_FP16 0x2u    /* fp16 values (format above; B >= 16); also the
+                              flag of the fp16 decode, cache update and bound */
 
-/* Largest encoded size of an n-value shard at block size B (host). It covers
- * both the compressed form with every block changed and the raw form. */
-uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems);
+/* Largest encoded size of an n-value shard at block size B (host; flags 0
+ * or CIERA_FP16). It covers both the compressed form with every block
+ * changed and the raw form. 0 for an unsupported B or flag. */
+uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems,
+                             uint32_t flags);
 
 /* Workspace bytes for encoding an n-value shard and for decoding (or cache
  * updating) `nshards` such shards at block size B (host). With
@@ -123,7 +138,8 @@ int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
 int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
                           hipStream_t stream);
 
-/* Sender side of Algorithm 1 for one shard (Section 3.1).
+/* Sender side of Algorithm 1 for one shard (Section 3.1). flags: 0,
+ * CIERA_ENC_RAW, CIERA_FP16 or both.
  *   w_new      n bf16 values as 16-bit patterns.
  *   exp_cache  n exponent bytes from the previous iteration (read only; NULL
  *              allowed only with CIERA_ENC_RAW).
@@ -147,13 +163,15 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
  * For every shard j it patches exp_cache[j*shard_elems ...] with the changed
  * blocks' exponents and writes the exact values to out[j*shard_elems ...]
  * (the Merge step); raw shards are copied and seed the cache. Compressed
- * shards must have been encoded with block_elems. rANS-coded shards (mode 2)
+ * shards must have been encoded with block_elems; flags is 0 for bf16 shards
+ * or CIERA_FP16 for fp16 ones (a shard of the other format is a
+ * CIERA_DEVERR_FORMAT error). rANS-coded shards (mode 2)
  * are decoded first into the workspace, which must then be sized with
  * CIERA_WS_ANS (else CIERA_DEVERR_NOSPACE). Decoding is idempotent: a
  * second call with the same gathered buffer gives the same out and cache. */
 int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
-                          uint32_t block_elems, uint16_t *out,
+                          uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream);
 
@@ -161,8 +179,8 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
  * exponents travel ANS-coded), in place on an encoded shard of n values at
  * block size B >= 16: when the rANS-coded section (format above) is smaller
  * than the E raw exception bytes, the shard becomes mode 2 and its total
- * shrinks; otherwise, and for raw or already coded shards, it is left as it
- * is. *out_bytes (device, may be NULL) receives the total afterwards. Bytes
+ * shrinks; otherwise, and for raw, fp16 or already coded shards, it is left
+ * as it is. *out_bytes (device, may be NULL) receives the total afterwards. Bytes
  * of the buffer past the new total are unspecified. The workspace must hold
  * ciera_workspace_bytes(n, 1, B, CIERA_WS_ANS). Deterministic: the same shard
  * always gives the same bytes. */
@@ -175,7 +193,7 @@ int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
  * blocks are overwritten from the exception list; a raw shard sets every
  * byte). This is how a sender brings its own cache forward. */
 int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
-                       uint64_t n_elems, uint32_t block_elems,
+                       uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                        void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream);
 
@@ -190,7 +208,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
  * GAMMA = 0x9E3779B97F4A7C15, s_0 = 0x243F6A8885A308D3,
  * s_1 = 0x13198A2E03707344 (pi), mix = the SplitMix64 finaliser. A block is
  * reused only when both halves match. HashCache layout: u64[2 * ceil(n/B)],
- * (H_0, H_1) of block b at [2b], [2b + 1], 8-byte aligned. B >= 16 (a hash per
+ * (H_0, H_1) of block b at [2b], [2b + 1], 8-byte aligned. bf16 only. B >= 16 (a hash per
  * value would outweigh the exponent it stands for); B = 1 returns
  * CIERA_EUNSUPPORTED. The hashes never travel: the wire is unchanged. */
 

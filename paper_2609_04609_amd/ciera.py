@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libciera.so")
 OK, EINVAL, ENOSPC, EUNSUPPORTED, EFORMAT, EHIP = 0, -1, -2, -3, -4, -5
 DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS, DEVERR_NOSPACE = 1, 2, 4, 8
 ENC_RAW = 0x1
+FP16 = 0x2
 WS_ANS = 0x1
 SELECT_STOP_AT_MISFIT = 0x1
 HEADER_BYTES = 64
@@ -47,15 +48,16 @@ class CostModel(ctypes.Structure):
 
 _vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
 _SIGS = {
-    "ciera_encoded_bound": (_u64, [_u64, _u32]),
+    "ciera_encoded_bound": (_u64, [_u64, _u32, _u32]),
     "ciera_workspace_bytes": (_u64, [_u64, _u32, _u32, _u32]),
     "ciera_workspace_init": (_i32, [_vp, _u64, _vp]),
     "ciera_workspace_error": (_i32, [_vp, ctypes.POINTER(_u32), _i32, _vp]),
     "ciera_encode": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64, _vp, _vp,
                             _u64, _vp]),
-    "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _vp, _vp, _vp,
-                                     _u64, _vp]),
-    "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _vp, _u64, _vp]),
+    "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _u32, _vp,
+                                     _vp, _vp, _u64, _vp]),
+    "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64,
+                                  _vp]),
     "ciera_ans_code": (_i32, [_vp, _u64, _u32, _vp, _vp, _u64, _vp]),
     "ciera_hash_blocks": (_i32, [_vp, _u64, _u32, _vp, _vp]),
     "ciera_encode_hashed": (_i32, [_vp, _vp, _vp, _u64, _u32, _vp, _u64, _vp,
@@ -97,8 +99,8 @@ def _check(fn, rc):
 
 # ---- the C ABI, name for name (pointers and the stream as integers) ----
 
-def ciera_encoded_bound(n_elems, block_elems):
-    return lib().ciera_encoded_bound(n_elems, block_elems)
+def ciera_encoded_bound(n_elems, block_elems, flags=0):
+    return lib().ciera_encoded_bound(n_elems, block_elems, flags)
 
 
 def ciera_workspace_bytes(n_elems, nshards, block_elems, flags=0):
@@ -125,17 +127,19 @@ def ciera_encode(w_new, exp_cache, n_elems, block_elems, flags, out,
 
 def ciera_decode_gathered(gathered, shard_offsets, nshards, shard_elems,
                           block_elems, out, exp_cache, workspace,
-                          workspace_bytes, stream):
+                          workspace_bytes, stream, flags=0):
+    """The C call of the same name; `flags` (0 or FP16) comes last here."""
     return lib().ciera_decode_gathered(gathered, shard_offsets, nshards,
-                                       shard_elems, block_elems, out,
+                                       shard_elems, block_elems, flags, out,
                                        exp_cache, workspace, workspace_bytes,
                                        stream)
 
 
 def ciera_update_cache(exp_cache, encoded, n_elems, block_elems, workspace,
-                       workspace_bytes, stream):
+                       workspace_bytes, stream, flags=0):
+    """The C call of the same name; `flags` (0 or FP16) comes last here."""
     return lib().ciera_update_cache(exp_cache, encoded, n_elems, block_elems,
-                                    workspace, workspace_bytes, stream)
+                                    flags, workspace, workspace_bytes, stream)
 
 
 def ciera_ans_code(encoded, n_elems, block_elems, out_bytes, workspace,
@@ -213,12 +217,14 @@ class Workspace:
         return ciera_workspace_error(self.ptr, int(clear), _stream())
 
 
-def encode_t(w_bits, cache, block_elems, ws, out, raw=False, out_bytes=None):
+def encode_t(w_bits, cache, block_elems, ws, out, raw=False, out_bytes=None,
+             fp16=False):
     """Encode a 1-D int16 bit tensor into ``out`` (uint8, bound-sized)."""
     n = w_bits.numel()
-    rc = ciera_encode(_ptr(w_bits), _ptr(cache), n, block_elems,
-                      ENC_RAW if raw else 0, _ptr(out), out.numel(),
-                      _ptr(out_bytes), ws.ptr, ws.nbytes, _stream())
+    flags = (ENC_RAW if raw else 0) | (FP16 if fp16 else 0)
+    rc = ciera_encode(_ptr(w_bits), _ptr(cache), n, block_elems, flags,
+                      _ptr(out), out.numel(), _ptr(out_bytes), ws.ptr,
+                      ws.nbytes, _stream())
     return _check("ciera_encode", rc)
 
 
@@ -246,14 +252,15 @@ def ans_code_t(encoded, n_elems, block_elems, ws, out_bytes=None):
 
 
 def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,
-                      ws):
+                      ws, fp16=False):
     rc = ciera_decode_gathered(_ptr(gathered), _ptr(offsets), offsets.numel(),
                                shard_elems, block_elems, _ptr(out),
-                               _ptr(cache), ws.ptr, ws.nbytes, _stream())
+                               _ptr(cache), ws.ptr, ws.nbytes, _stream(),
+                               FP16 if fp16 else 0)
     return _check("ciera_decode_gathered", rc)
 
 
-def update_cache_t(cache, encoded, n_elems, block_elems, ws):
+def update_cache_t(cache, encoded, n_elems, block_elems, ws, fp16=False):
     rc = ciera_update_cache(_ptr(cache), _ptr(encoded), n_elems, block_elems,
-                            ws.ptr, ws.nbytes, _stream())
+                            ws.ptr, ws.nbytes, _stream(), FP16 if fp16 else 0)
     return _check("ciera_update_cache", rc)

@@ -111,7 +111,9 @@ __global__ __launch_bounds__(kThreads) void ans_hist_kernel(AnsEncArgs a) {
   const uint8_t *enc = a.enc;
   const uint32_t mode = ld32(enc + 4) >> 16;
   const uint64_t E = ld64(enc + 32);
-  if (mode != kModeCompressed || E == 0 || E > a.n) return;
+  if (mode != kModeCompressed || ld32(enc + 12) != kDtypeBf16 || E == 0 ||
+      E > a.n)
+    return;
   const int tid = threadIdx.x, wave = tid >> 6;
   for (int i = tid; i < kWaves * 256; i += kThreads) (&s_h[0][0])[i] = 0u;
   __syncthreads();
@@ -149,7 +151,8 @@ __global__ __launch_bounds__(kThreads) void ans_table_kernel(AnsEncArgs a) {
   const uint32_t s = threadIdx.x;
   const uint32_t mode = ld32(a.enc + 4) >> 16;
   const uint64_t E = ld64(a.enc + 32);
-  if (mode != kModeCompressed || E == 0 || E > a.n) {
+  if (mode != kModeCompressed || ld32(a.enc + 12) != kDtypeBf16 || E == 0 ||
+      E > a.n) {
     if (s == 0) a.ans->K = 0;
     return;
   }
@@ -333,7 +336,8 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   const uint64_t n = a.n;
   const uint32_t vm = ld32(enc + 4);
   if (ld32(enc) != kMagic || (vm & 0xFFFFu) != kVersion ||
-      (vm >> 16) != kModeAns || ld64(enc + 16) != n ||
+      (vm >> 16) != kModeAns || ld32(enc + 12) != kDtypeBf16 ||
+      ld64(enc + 16) != n ||
       ld32(enc + 8) != (1u << a.log2B) || a.log2B < 4)
     return;
   const uint64_t E = ld64(enc + 32), P = ld64(enc + 40);

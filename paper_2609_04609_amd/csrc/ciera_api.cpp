@@ -28,12 +28,15 @@ bool aligned(const void *p, uintptr_t a) {
 
 extern "C" {
 
-uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems) {
+uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems,
+                             uint32_t flags) {
   const int l = log2_block(block_elems);
-  if (l < 0) return 0;
-  const uint64_t compressed = kHeaderBytes + pad16(n_elems) +
+  if (l < 0 || (flags & ~CIERA_FP16)) return 0;
+  const bool f16 = flags & CIERA_FP16;
+  if (f16 && l < kF16MinLog2B) return 0;
+  const uint64_t compressed = kHeaderBytes + pad16(sm_bytes(n_elems, f16)) +
                               pad16(bitmap_bytes(n_elems, uint32_t(l))) +
-                              pad16(n_elems);
+                              pad16(exc_bytes(n_elems, f16));
   const uint64_t raw = kHeaderBytes + pad16(2 * n_elems);
   return compressed > raw ? compressed : raw;
 }
@@ -111,7 +114,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
                       uint64_t n_elems, uint32_t l, void *out,
                       uint64_t *out_bytes, void *workspace,
                       uint64_t workspace_bytes, hipStream_t stream,
-                      bool hashed) {
+                      bool hashed, bool f16) {
   if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
   const uint64_t tiles = enc_tiles(n_elems, l);
   if (workspace_bytes < kWsCtlBytes + 4 * (tiles + 1)) return CIERA_ENOSPC;
@@ -130,6 +133,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   a.hash_in = hash_in;
   a.hash_out = hash_out;
   a.hashed = hashed;
+  a.f16 = f16;
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
@@ -143,25 +147,28 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                  hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
-  if (flags & ~CIERA_ENC_RAW) return CIERA_EINVAL;
+  if (flags & ~(CIERA_ENC_RAW | CIERA_FP16)) return CIERA_EINVAL;
   const bool raw = flags & CIERA_ENC_RAW;
+  const bool f16 = flags & CIERA_FP16;
+  if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
   if (!out || (n_elems && !w_new) || (!raw && n_elems && !exp_cache))
     return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(out, 16)) return CIERA_EINVAL;
-  if (out_capacity < ciera_encoded_bound(n_elems, block_elems))
+  if (out_capacity <
+      ciera_encoded_bound(n_elems, block_elems, f16 ? CIERA_FP16 : 0))
     return CIERA_ENOSPC;
   if (raw) {
     const bool vec = aligned(w_new, 16);
     return launch_encode_raw(w_new, n_elems, block_elems,
-                             static_cast<uint8_t *>(out), out_bytes, vec,
+                             static_cast<uint8_t *>(out), out_bytes, vec, f16,
                              stream) == hipSuccess
                ? CIERA_OK
                : CIERA_EHIP;
   }
   return encode_compressed(w_new, exp_cache, nullptr, nullptr, n_elems,
                            uint32_t(l), out, out_bytes, workspace,
-                           workspace_bytes, stream, false);
+                           workspace_bytes, stream, false, f16);
 }
 
 int ciera_hash_blocks(const uint16_t *w, uint64_t n_elems,
@@ -197,20 +204,23 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(out, 16) || !aligned(hash_in, 8) || !aligned(hash_out, 8))
     return CIERA_EINVAL;
-  if (out_capacity < ciera_encoded_bound(n_elems, block_elems))
+  if (out_capacity < ciera_encoded_bound(n_elems, block_elems, 0))
     return CIERA_ENOSPC;
   return encode_compressed(w_new, nullptr, hash_in, hash_out, n_elems,
                            uint32_t(l), out, out_bytes, workspace,
-                           workspace_bytes, stream, true);
+                           workspace_bytes, stream, true, false);
 }
 
 int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
-                          uint32_t block_elems, uint16_t *out,
+                          uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
+  if (flags & ~CIERA_FP16) return CIERA_EINVAL;
+  const bool f16 = flags & CIERA_FP16;
+  if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
   if (!gathered || !shard_offsets || !out || !exp_cache || !workspace)
     return CIERA_EINVAL;
   if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
@@ -228,9 +238,11 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
   a.tile_excl = tile_excl_of(workspace);
-  a.ans_exc =
-      ans_lists_of(workspace, workspace_bytes, shard_elems, nshards, l);
+  a.ans_exc = f16 ? nullptr
+                  : ans_lists_of(workspace, workspace_bytes, shard_elems,
+                                 nshards, l);
   a.ans_stride = pad16(shard_elems);
+  a.f16 = f16;
   const bool vec =
       (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
@@ -238,10 +250,14 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
 }
 
 int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
-                       uint64_t n_elems, uint32_t block_elems, void *workspace,
-                       uint64_t workspace_bytes, hipStream_t stream) {
+                       uint64_t n_elems, uint32_t block_elems, uint32_t flags,
+                       void *workspace, uint64_t workspace_bytes,
+                       hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
+  if (flags & ~CIERA_FP16) return CIERA_EINVAL;
+  const bool f16 = flags & CIERA_FP16;
+  if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
   if (!encoded || (n_elems && !exp_cache) || !workspace) return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
@@ -256,8 +272,10 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   a.cache = exp_cache;
   a.ctl = static_cast<WsCtl *>(workspace);
   a.tile_excl = tile_excl_of(workspace);
-  a.ans_exc = ans_lists_of(workspace, workspace_bytes, n_elems, 1, l);
+  a.ans_exc =
+      f16 ? nullptr : ans_lists_of(workspace, workspace_bytes, n_elems, 1, l);
   a.ans_stride = pad16(n_elems);
+  a.f16 = f16;
   const bool vec = aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;

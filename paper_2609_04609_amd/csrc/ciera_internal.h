@@ -35,6 +35,17 @@ __host__ __device__ constexpr inline uint64_t bitmap_bytes(uint64_t n,
                                                           uint32_t log2B) {
   return (blocks_of(n, log2B) + 7u) >> 3;
 }
+// fp16 shards (header offset 12 = 1): the sign+mantissa section is the low
+// mantissa bytes and 3 bit-plane bytes per octet; exceptions are 5 bit-plane
+// bytes per group of 8 exponents
+constexpr uint32_t kDtypeBf16 = 0u, kDtypeFp16 = 1u;
+constexpr int kF16MinLog2B = 4;  // fp16 shards need B >= 16
+__host__ __device__ constexpr inline uint64_t sm_bytes(uint64_t n, bool f16) {
+  return f16 ? n + 3u * ((n + 7u) >> 3) : n;
+}
+__host__ __device__ constexpr inline uint64_t exc_bytes(uint64_t E, bool f16) {
+  return f16 ? 5u * ((E + 7u) >> 3) : E;
+}
 
 // ---- workspace ----
 // [0, 256): control words; [256, ...): 32-bit per-tile counts (encode: one
@@ -82,6 +93,7 @@ struct EncArgs {
   uint64_t *out_bytes;
   WsCtl *ctl;
   uint32_t *counts;  // num_tiles + 1 words
+  bool f16;  // fp16 values (B >= 16)
   // block-hash detector (B >= 16) in place of exact compare with `cache`
   bool hashed;
   const uint64_t *hash_in;
@@ -95,6 +107,7 @@ struct DecArgs {
   // ans_exc + j * ans_stride (nullptr: the workspace has no room for them)
   uint8_t *ans_exc;
   uint64_t ans_stride;
+  bool f16;  // fp16 shards (B >= 16)
   const uint64_t *offsets;  // nullptr: one shard at gathered + 0
   uint64_t n;               // values per shard
   uint32_t log2B;
@@ -161,7 +174,7 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
 hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s);
 hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
                              uint8_t *out, uint64_t *out_bytes, bool vec,
-                             hipStream_t s);
+                             bool f16, hipStream_t s);
 hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s);
 // ciera_ans.hip
 hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s);

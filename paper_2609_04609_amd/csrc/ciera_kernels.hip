@@ -57,6 +57,55 @@ __device__ __forceinline__ void merge4(uint32_t e, uint32_t sm, uint32_t &a,
   b = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
 }
 
+// fp16 (sign bit 15, exponent bits 14..10, mantissa bits 9..0): four values
+// (a: values 0,1; b: values 2,3) become four 5-bit exponents, four low
+// mantissa bytes and four (sign << 2 | mantissa bits 9..8) fields.
+__device__ __forceinline__ void split4_f16(uint32_t a, uint32_t b, uint32_t &e,
+                                           uint32_t &lo, uint32_t &hi3) {
+  const uint32_t hb = __builtin_amdgcn_perm(b, a, 0x07050301u);
+  lo = __builtin_amdgcn_perm(b, a, 0x06040200u);
+  e = (hb >> 2) & 0x1F1F1F1Fu;
+  hi3 = ((hb >> 5) & 0x04040404u) | (hb & 0x03030303u);
+}
+
+// Inverse of split4_f16.
+__device__ __forceinline__ void merge4_f16(uint32_t e, uint32_t lo,
+                                           uint32_t hi3, uint32_t &a,
+                                           uint32_t &b) {
+  const uint32_t hb = ((hi3 & 0x04040404u) << 5) |
+                      ((e & 0x1F1F1F1Fu) << 2) | (hi3 & 0x03030303u);
+  a = __builtin_amdgcn_perm(hb, lo, 0x05010400u);
+  b = __builtin_amdgcn_perm(hb, lo, 0x07030602u);
+}
+
+// Bit p of the eight byte fields of an octet (bytes of x: values 0..3, of
+// y: 4..7) gathered into one byte, value k in bit k. The multiply moves the
+// bit at 8i to 24 + i; no two partial products share a bit.
+__device__ __forceinline__ uint32_t plane_byte(uint32_t x, uint32_t y,
+                                               uint32_t p) {
+  const uint32_t t0 = (x >> p) & 0x01010101u, t1 = (y >> p) & 0x01010101u;
+  return ((t0 * 0x01020408u) >> 24) | (((t1 * 0x01020408u) >> 24) << 4);
+}
+
+// Bits 0..3 of x to bit 0 of bytes 0..3 (the inverse gather).
+__device__ __forceinline__ uint32_t spread4(uint32_t x) {
+  return ((x & 0xFu) * 0x00204081u) & 0x01010101u;
+}
+
+// Eight byte fields of an octet from Q plane bytes (byte q: bit q of value
+// k in bit k), as two words (values 0..3, 4..7).
+template <int Q>
+__device__ __forceinline__ uint2 unplane(const uint8_t *g) {
+  uint2 v = make_uint2(0u, 0u);
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const uint32_t b = g[q];
+    v.x |= spread4(b) << q;
+    v.y |= spread4(b >> 4) << q;
+  }
+  return v;
+}
+
 // ------------------------------------------------- octet loads and stores --
 // `valid` is the number of in-range values of the octet (1..8). VEC means the
 // base pointers are aligned for vector accesses; the ragged last octet and
@@ -167,13 +216,14 @@ __device__ __forceinline__ void put_header(uint8_t *out, uint32_t mode,
                                            uint32_t B, uint64_t n,
                                            uint64_t changed, uint64_t E,
                                            uint64_t P, uint64_t total,
-                                           uint32_t i) {
+                                           uint32_t i, uint32_t dtype = 0) {
   if (i >= 16) return;
   uint32_t v = 0;
   switch (i) {
     case 0: v = kMagic; break;
     case 1: v = kVersion | (mode << 16); break;
     case 2: v = B; break;
+    case 3: v = dtype; break;
     case 4: v = uint32_t(n); break;
     case 5: v = uint32_t(n >> 32); break;
     case 6: v = uint32_t(changed); break;
@@ -231,11 +281,12 @@ __device__ __forceinline__ uint64_t sm64_mix(uint64_t z) {
 enum : int { kDetExact = 0, kDetHash = 1, kDetHashOnly = 2 };
 
 // Pass 1. Everything but the exception list.
-template <bool VEC, bool ELEMS, int DET>
+template <bool VEC, bool ELEMS, int DET, bool F16 = false>
 __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   constexpr bool HASH = DET != kDetExact;
   constexpr bool OUT = DET != kDetHashOnly;
   static_assert(!(HASH && ELEMS), "the block hash needs B >= 16");
+  static_assert(!(F16 && (HASH || ELEMS)), "fp16: exact compare, B >= 16");
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t tile = blockIdx.x * 4u + (threadIdx.x >> 6);
   if (tile >= a.num_tiles) return;
@@ -243,7 +294,8 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   const uint32_t log2B = a.log2B;
   const uint64_t T = a.tile_elems;
   const uint64_t tbase = uint64_t(tile) * T;
-  const uint64_t n16 = pad16(n);
+  const uint64_t S_sm = sm_bytes(n, F16);  // sign+mantissa section
+  const uint64_t n16 = pad16(S_sm);
   const uint64_t bm = bitmap_bytes(n, log2B);
   const uint64_t bm16 = pad16(bm);
   uint8_t *const sm_out = OUT ? a.out + kHeaderBytes : nullptr;
@@ -407,8 +459,18 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
       for (int u = 0; u < 8; ++u) {
         const uint64_t elem = cbase + (uint64_t(u) * 64 + lane) * 8;
         uint2 e, sm;
-        split4(wv[u].x, wv[u].y, e.x, sm.x);
-        split4(wv[u].z, wv[u].w, e.y, sm.y);
+        if (F16) {
+          uint2 hi;
+          split4_f16(wv[u].x, wv[u].y, e.x, sm.x, hi.x);
+          split4_f16(wv[u].z, wv[u].w, e.y, sm.y, hi.y);
+          uint8_t *pl = sm_out + n + 3 * (elem >> 3);
+#pragma unroll
+          for (uint32_t q = 0; q < 3; ++q)
+            pl[q] = uint8_t(plane_byte(hi.x, hi.y, q));
+        } else {
+          split4(wv[u].x, wv[u].y, e.x, sm.x);
+          split4(wv[u].z, wv[u].w, e.y, sm.y);
+        }
         if (OUT) *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
         if (HASH) {
           hash_terms(uint32_t(u), cbase,
@@ -430,8 +492,19 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
         if (valid) {
           const uint4 wv = load_w8<VEC>(a.w + elem, valid);
           uint2 e, sm;
-          split4(wv.x, wv.y, e.x, sm.x);
-          split4(wv.z, wv.w, e.y, sm.y);
+          if (F16) {
+            // load_w8 zero-fills past n: those fields are 0 in the planes
+            uint2 hi;
+            split4_f16(wv.x, wv.y, e.x, sm.x, hi.x);
+            split4_f16(wv.z, wv.w, e.y, sm.y, hi.y);
+            uint8_t *pl = sm_out + n + 3 * (elem >> 3);
+#pragma unroll
+            for (uint32_t q = 0; q < 3; ++q)
+              pl[q] = uint8_t(plane_byte(hi.x, hi.y, q));
+          } else {
+            split4(wv.x, wv.y, e.x, sm.x);
+            split4(wv.z, wv.w, e.y, sm.y);
+          }
           if (OUT) store_b8<VEC>(sm_out + elem, sm, valid);
           if (HASH) {
             // load_w8 zero-fills past n: those bytes are 0 in the word
@@ -513,7 +586,7 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   // the last tile zeroes the padding of the first two sections, before the
   // exception pass reads the bitmap back
   if (tile == a.num_tiles - 1) {
-    for (uint64_t i = n + lane; i < n16; i += 64) sm_out[i] = 0;
+    for (uint64_t i = S_sm + lane; i < n16; i += 64) sm_out[i] = 0;
     uint64_t written = bm;
     if (!ELEMS)
       written = log2B <= 9 ? uint64_t(a.num_tiles) * ((kEncChunk >> log2B) >> 3)
@@ -602,7 +675,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_counts_kernel(
 // re-read of W' depends only on the tile's own flags, so it is issued before
 // that count and the two overlap. At B = 1 the offsets come from the scanned
 // per-tile counts.
-template <bool VEC, bool ELEMS>
+template <bool VEC, bool ELEMS, bool F16 = false>
 __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   __shared__ uint32_t s_red[4];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -613,11 +686,28 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   const uint32_t B = 1u << log2B;
   const uint64_t T = a.tile_elems;
   const uint64_t tbase = uint64_t(tile) * T;
-  const uint64_t n16 = pad16(n);
+  const uint64_t S_sm = sm_bytes(n, F16);
+  const uint64_t n16 = pad16(S_sm);
   const uint64_t bm = bitmap_bytes(n, log2B);
   const uint64_t bm16 = pad16(bm);
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
   uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
+  // the exponents of one octet of the list, at exception index pos: bf16
+  // bytes at pos, fp16 5 bit-plane bytes at 5 (pos / 8)
+  auto put_exc = [&](uint64_t pos, const uint4 &wv, uint32_t valid) {
+    uint2 e, t0, t1;
+    if (F16) {
+      split4_f16(wv.x, wv.y, e.x, t0.x, t1.x);
+      split4_f16(wv.z, wv.w, e.y, t0.y, t1.y);
+      uint8_t *g = exc_out + 5 * (pos >> 3);
+#pragma unroll
+      for (uint32_t q = 0; q < 5; ++q) g[q] = uint8_t(plane_byte(e.x, e.y, q));
+    } else {
+      split4(wv.x, wv.y, e.x, t0.x);
+      split4(wv.z, wv.w, e.y, t0.y);
+      store_b8<VEC>(exc_out + pos, e, valid);
+    }
+  };
   // bitmap bytes per tile (B >= 16)
   const uint64_t per_tile = log2B <= 9 ? (kEncChunk >> log2B) >> 3 : 1u;
 
@@ -733,10 +823,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         if (uint32_t(k) < (bl >> 6)) rank += uint32_t(__popcll(fw[k]));
       const uint64_t pos =
           (uint64_t(prefix + rank) << log2B) | ((o << 3) & (B - 1u));
-      uint2 e, sm;
-      split4(wv[u].x, wv[u].y, e.x, sm.x);
-      split4(wv[u].z, wv[u].w, e.y, sm.y);
-      if (pos + valid <= n) store_b8<VEC>(exc_out + pos, e, valid);
+      if (pos + valid <= n) put_exc(pos, wv[u], valid);
     }
   } else {
     // 8 blocks of B > 512 values; the wave copies each changed block's
@@ -756,11 +843,8 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         const uint32_t valid = octet_valid(elem, n);
         if (!valid) continue;
         const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-        uint2 e, sm;
-        split4(wv.x, wv.y, e.x, sm.x);
-        split4(wv.z, wv.w, e.y, sm.y);
         const uint64_t pos = dst + c + uint64_t(lane) * 8;
-        if (pos + valid <= n) store_b8<VEC>(exc_out + pos, e, valid);
+        if (pos + valid <= n) put_exc(pos, wv, valid);
       }
       ++rank;
     }
@@ -789,11 +873,13 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
       if (lane == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
       E = n;
     }
-    const uint64_t P = n + bm + E;
-    const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(E);
-    put_header(a.out, kModeCompressed, B, n, total_changed, E, P, total, lane);
+    const uint64_t S_exc = exc_bytes(E, F16);
+    const uint64_t P = S_sm + bm + S_exc;
+    const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(S_exc);
+    put_header(a.out, kModeCompressed, B, n, total_changed, E, P, total, lane,
+               F16 ? kDtypeFp16 : kDtypeBf16);
     if (lane == 16 && a.out_bytes) *a.out_bytes = total;
-    for (uint64_t i = E + lane; i < pad16(E); i += 64) exc_out[i] = 0;
+    for (uint64_t i = S_exc + lane; i < pad16(S_exc); i += 64) exc_out[i] = 0;
   }
 }
 
@@ -801,7 +887,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void encode_raw_kernel(
     const uint16_t *w, uint64_t n, uint32_t B, uint8_t *out,
-    uint64_t *out_bytes) {
+    uint64_t *out_bytes, uint32_t dtype) {
   const uint64_t total = kHeaderBytes + pad16(2 * n);
   const uint64_t octets = (n + 7) / 8;
   const uint64_t o = uint64_t(blockIdx.x) * kThreads + threadIdx.x;
@@ -813,7 +899,7 @@ __global__ __launch_bounds__(kThreads) void encode_raw_kernel(
   }
   if (blockIdx.x == 0) {
     const uint32_t tid = threadIdx.x;
-    put_header(out, kModeRaw, B, n, 0, 0, 2 * n, total, tid);
+    put_header(out, kModeRaw, B, n, 0, 0, 2 * n, total, tid, dtype);
     if (tid == 16 && out_bytes) *out_bytes = total;
     uint8_t *bytes = out + kHeaderBytes;
     for (uint64_t i = 2 * n + tid; i < pad16(2 * n); i += kThreads) bytes[i] = 0;
@@ -849,12 +935,15 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   const uint32_t magic = h32[0], vm = h32[1], hB = h32[2];
   const uint64_t hn = h64[2], hE = h64[4], hP = h64[5], htotal = h64[6];
   const uint32_t mode = vm >> 16;
-  bool ok = magic == kMagic && (vm & 0xFFFFu) == kVersion && hn == a.n;
+  bool ok = magic == kMagic && (vm & 0xFFFFu) == kVersion && hn == a.n &&
+            h32[3] == (a.f16 ? kDtypeFp16 : kDtypeBf16);
   const uint64_t bm = bitmap_bytes(hn, a.log2B);
+  const uint64_t sm16 = pad16(sm_bytes(hn, a.f16));
   if (ok && mode == kModeCompressed) {
     ok = hB == (1u << a.log2B) && hE <= hn &&
-         htotal == kHeaderBytes + pad16(hn) + pad16(bm) + pad16(hE);
-  } else if (ok && mode == kModeAns) {
+         htotal == kHeaderBytes + sm16 + pad16(bm) +
+                       pad16(exc_bytes(hE, a.f16));
+  } else if (ok && mode == kModeAns && !a.f16) {
     // rANS-coded exceptions (B >= 16): the list was decoded into the
     // workspace by ans_decode_kernel, which checks the coded section
     ok = a.log2B >= uint32_t(kAnsMinLog2B) && hB == (1u << a.log2B) &&
@@ -877,9 +966,8 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   v.ok = true;
   v.mode = mode;
   v.E = hE;
-  v.exc = mode == kModeAns
-              ? a.ans_exc + uint64_t(j) * a.ans_stride
-              : v.enc + kHeaderBytes + pad16(hn) + pad16(bm);
+  v.exc = mode == kModeAns ? a.ans_exc + uint64_t(j) * a.ans_stride
+                           : v.enc + kHeaderBytes + sm16 + pad16(bm);
   return v;
 }
 
@@ -888,7 +976,7 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
 // with the bitmap words, then one cache-or-exception load per octet, chosen
 // by address rather than by branch); the ragged last tile and unaligned
 // buffers go element by element.
-template <int OCT, bool VEC, bool UPDATE_ONLY>
+template <int OCT, bool VEC, bool UPDATE_ONLY, bool F16 = false>
 __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   constexpr uint32_t T = kThreads * 8 * OCT;
   // tile bitmap words (32 blocks each) covering at most T/16 blocks + 1 word
@@ -921,9 +1009,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
       for (int u = 0; u < OCT; ++u) {
         const uint64_t elem =
             base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-        uint2 e, sm;
-        split4(wv[u].x, wv[u].y, e.x, sm.x);
-        split4(wv[u].z, wv[u].w, e.y, sm.y);
+        uint2 e, sm, hi;
+        if (F16) {
+          split4_f16(wv[u].x, wv[u].y, e.x, sm.x, hi.x);
+          split4_f16(wv[u].z, wv[u].w, e.y, sm.y, hi.y);
+        } else {
+          split4(wv[u].x, wv[u].y, e.x, sm.x);
+          split4(wv[u].z, wv[u].w, e.y, sm.y);
+        }
         if (!UPDATE_ONLY) *reinterpret_cast<uint4 *>(out + elem) = wv[u];
         *reinterpret_cast<uint2 *>(cache + elem) = e;
       }
@@ -937,9 +1030,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
       if (!valid) continue;
       // the raw body is 16-byte aligned whenever the shard is
       const uint4 wv = load_w8<true>(body + elem, valid);
-      uint2 e, sm;
-      split4(wv.x, wv.y, e.x, sm.x);
-      split4(wv.z, wv.w, e.y, sm.y);
+      uint2 e, sm, hi;
+      if (F16) {
+        split4_f16(wv.x, wv.y, e.x, sm.x, hi.x);
+        split4_f16(wv.z, wv.w, e.y, sm.y, hi.y);
+      } else {
+        split4(wv.x, wv.y, e.x, sm.x);
+        split4(wv.z, wv.w, e.y, sm.y);
+      }
       if (!UPDATE_ONLY) store_w8<VEC>(out + elem, wv, valid);
       store_b8<VEC>(cache + elem, e, valid);
     }
@@ -949,12 +1047,22 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   const uint32_t log2B = a.log2B;
   const uint32_t B = 1u << log2B;
   const uint8_t *const sm_in = sv.enc + kHeaderBytes;
-  const uint8_t *const bmp = sm_in + pad16(n);
+  const uint8_t *const bmp = sm_in + pad16(sm_bytes(n, F16));
   const uint32_t *const bmp32 = reinterpret_cast<const uint32_t *>(bmp);
   const uint8_t *const exc = sv.exc;
 
-  // sign|mantissa bytes first: they do not depend on the bitmap
-  uint2 smv[OCT];
+  // sign|mantissa bytes first: they do not depend on the bitmap (fp16: the
+  // low mantissa bytes, and the sign and top mantissa bits from 3 planes)
+  uint2 smv[OCT], hiv[OCT];
+  if (F16 && !UPDATE_ONLY) {
+#pragma unroll
+    for (int u = 0; u < OCT; ++u) {
+      const uint64_t elem =
+          base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+      hiv[u] = elem < n ? unplane<3>(sm_in + n + 3 * (elem >> 3))
+                        : make_uint2(0u, 0u);
+    }
+  }
   if (!UPDATE_ONLY) {
     if (full) {
 #pragma unroll
@@ -1025,20 +1133,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
         bad = true;
         ch[u] = false;
       }
-      src[u] = ch[u] ? exc + pos : cache + elem;
+      // fp16: the octet's exponents are the 5 plane bytes of group pos / 8
+      src[u] = ch[u] ? (F16 ? exc + 5 * (pos >> 3) : exc + pos) : cache + elem;
     }
     uint2 ev[OCT];
 #pragma unroll
-    for (int u = 0; u < OCT; ++u)
-      if (!UPDATE_ONLY || ch[u]) ev[u] = *reinterpret_cast<const uint2 *>(src[u]);
+    for (int u = 0; u < OCT; ++u) {
+      if (F16 && ch[u])
+        ev[u] = unplane<5>(src[u]);
+      else if (!UPDATE_ONLY || ch[u])
+        ev[u] = *reinterpret_cast<const uint2 *>(src[u]);
+    }
 #pragma unroll
     for (int u = 0; u < OCT; ++u) {
       const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
       if (ch[u]) *reinterpret_cast<uint2 *>(cache + elem) = ev[u];
       if (!UPDATE_ONLY) {
         uint4 wv;
-        merge4(ev[u].x, smv[u].x, wv.x, wv.y);
-        merge4(ev[u].y, smv[u].y, wv.z, wv.w);
+        if (F16) {
+          merge4_f16(ev[u].x, smv[u].x, hiv[u].x, wv.x, wv.y);
+          merge4_f16(ev[u].y, smv[u].y, hiv[u].y, wv.z, wv.w);
+        } else {
+          merge4(ev[u].x, smv[u].x, wv.x, wv.y);
+          merge4(ev[u].y, smv[u].y, wv.z, wv.w);
+        }
         *reinterpret_cast<uint4 *>(out + elem) = wv;
       }
     }
@@ -1061,7 +1179,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
           bad = true;
           continue;
         }
-        ev = load_b8<true>(exc + pos, valid);
+        ev = F16 ? unplane<5>(exc + 5 * (pos >> 3))
+                 : load_b8<true>(exc + pos, valid);
         store_b8<VEC>(cache + elem, ev, valid);
       } else {
         if (UPDATE_ONLY) continue;
@@ -1069,8 +1188,13 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
       }
       if (!UPDATE_ONLY) {
         uint4 wv;
-        merge4(ev.x, smv[u].x, wv.x, wv.y);
-        merge4(ev.y, smv[u].y, wv.z, wv.w);
+        if (F16) {
+          merge4_f16(ev.x, smv[u].x, hiv[u].x, wv.x, wv.y);
+          merge4_f16(ev.y, smv[u].y, hiv[u].y, wv.z, wv.w);
+        } else {
+          merge4(ev.x, smv[u].x, wv.x, wv.y);
+          merge4(ev.y, smv[u].y, wv.z, wv.w);
+        }
         store_w8<VEC>(out + elem, wv, valid);
       }
     }
@@ -1259,6 +1383,13 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     else
       hipLaunchKernelGGL((encode_pass_kernel<false, true, kDetExact>), grid,
                          block, 0, s, a);
+  } else if (a.f16) {
+    if (vec)
+      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetExact, true>),
+                         grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetExact, true>),
+                         grid, block, 0, s, a);
   } else if (a.hashed) {
     if (vec)
       hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHash>), grid,
@@ -1282,6 +1413,13 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
       hipLaunchKernelGGL((encode_exc_kernel<true, true>), grid, block, 0, s, a);
     else
       hipLaunchKernelGGL((encode_exc_kernel<false, true>), grid, block, 0, s, a);
+  } else if (a.f16) {
+    if (vec)
+      hipLaunchKernelGGL((encode_exc_kernel<true, false, true>), grid, block,
+                         0, s, a);
+    else
+      hipLaunchKernelGGL((encode_exc_kernel<false, false, true>), grid, block,
+                         0, s, a);
   } else {
     if (vec)
       hipLaunchKernelGGL((encode_exc_kernel<true, false>), grid, block, 0, s,
@@ -1306,16 +1444,19 @@ hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s) {
 
 hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
                              uint8_t *out, uint64_t *out_bytes, bool vec,
-                             hipStream_t s) {
+                             bool f16, hipStream_t s) {
+  const uint32_t dtype = f16 ? kDtypeFp16 : kDtypeBf16;
   const uint64_t octets = (n + 7) / 8;
   uint64_t blocks = (octets + kThreads - 1) / kThreads;
   if (blocks == 0) blocks = 1;
   if (vec)
     hipLaunchKernelGGL((encode_raw_kernel<true>), dim3(uint32_t(blocks)),
-                       dim3(kThreads), 0, s, w, n, B, out, out_bytes);
+                       dim3(kThreads), 0, s, w, n, B, out, out_bytes,
+                       dtype);
   else
     hipLaunchKernelGGL((encode_raw_kernel<false>), dim3(uint32_t(blocks)),
-                       dim3(kThreads), 0, s, w, n, B, out, out_bytes);
+                       dim3(kThreads), 0, s, w, n, B, out, out_bytes,
+                       dtype);
   return hipGetLastError();
 }
 
@@ -1345,6 +1486,25 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
                            0, s, a);
       else
         hipLaunchKernelGGL((decode_elems_kernel<O, false, false>), grid,
+                           block, 0, s, a);
+    }
+    return hipGetLastError();
+  }
+  if (a.f16) {
+    constexpr int O = int(kDecOct);
+    if (upd) {
+      if (vec)
+        hipLaunchKernelGGL((decode_kernel<O, true, true, true>), grid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((decode_kernel<O, false, true, true>), grid, block,
+                           0, s, a);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((decode_kernel<O, true, false, true>), grid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((decode_kernel<O, false, false, true>), grid,
                            block, 0, s, a);
     }
     return hipGetLastError();

@@ -97,6 +97,32 @@ def forced_bernoulli_bits(w_bits: torch.Tensor, c: float,
     return _shift_exponents(w_bits, u < c, up)
 
 
+def normal_f16_bits(numel: int, std: float, seed: int,
+                    device="cuda") -> torch.Tensor:
+    """fp16 bit patterns of N(0, std) weights (fp32 draw, rounded to fp16)."""
+    g = _gen(device, seed)
+    x = torch.randn(numel, generator=g, device=device, dtype=torch.float32)
+    x.mul_(std)
+    return x.to(torch.float16).view(torch.int16)
+
+
+def forced_bernoulli_f16_bits(w_bits: torch.Tensor, c: float,
+                              seed: int) -> torch.Tensor:
+    """fp16: each element's 5-bit exponent (bits 14..10) moves by +-1 with
+    probability c (up from 0, down from 30 and 31)."""
+    g = _gen(w_bits.device, seed)
+    u = torch.rand(w_bits.numel(), generator=g, device=w_bits.device)
+    up = torch.rand(w_bits.numel(), generator=g, device=w_bits.device) < 0.5
+    w = w_bits.to(torch.int32) & 0xFFFF
+    field_ = (w >> 10) & 0x1F
+    go_up = torch.where(field_ == 0, torch.ones_like(up),
+                        torch.where(field_ >= 30, torch.zeros_like(up), up))
+    step = torch.where(go_up, 1 << 10, -(1 << 10)).to(torch.int32)
+    w = torch.where(u < c, w + step, w)
+    w = torch.where(w >= 0x8000, w - 0x10000, w)
+    return w.to(torch.int16)
+
+
 def forced_exact_k_bits(w_bits: torch.Tensor, k: int, seed: int):
     """Exactly k distinct elements, uniform at random, move by +-1.
 

@@ -47,6 +47,14 @@ def test_sizes_closed_form(cl, orc):
             expect = max(64 + a16(n) + a16(bm) + a16(n), 64 + a16(2 * n))
             assert cl.ciera_encoded_bound(n, B) == expect
             assert orc.encoded_bound(n, B) == expect
+    # fp16: sign+mantissa n + 3 ceil(n/8), exceptions 5 ceil(n/8) at most
+    for n in [0, 1, 15, 16, 17, 4096, 4097, 25165824]:
+        for B in [16, 512, 4096]:
+            bm = -(-(-(-n // B)) // 8)
+            a16 = lambda x: -(-x // 16) * 16
+            c = 64 + a16(n + 3 * (-(-n // 8))) + a16(bm) + a16(5 * (-(-n // 8)))
+            assert cl.ciera_encoded_bound(n, B, cl.FP16) == \
+                max(c, 64 + a16(2 * n)) == orc.encoded_bound_f16(n, B)
     for B in [0, 2, 3, 8, 24, 8192]:
         assert cl.ciera_encoded_bound(100, B) == 0
         assert cl.ciera_workspace_bytes(100, 1, B) == 0
@@ -78,8 +86,19 @@ def test_host_argument_checks(cl):
     assert cl.ciera_encode(fake, 0, 1000, 512, 0, fake, 1 << 20, 0, fake,
                            ws_bytes, 0) == cl.EINVAL
     # unknown flag, unaligned output, too-large shard
-    assert cl.ciera_encode(fake, fake, 1000, 512, 2, fake, 1 << 20, 0, fake,
+    assert cl.ciera_encode(fake, fake, 1000, 512, 4, fake, 1 << 20, 0, fake,
                            ws_bytes, 0) == cl.EINVAL
+    # fp16 needs B >= 16 (encode, decode, cache update, bound)
+    assert cl.ciera_encode(fake, fake, 1000, 1, cl.FP16, fake, 1 << 20, 0,
+                           fake, ws_bytes, 0) == cl.EUNSUPPORTED
+    assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 1, fake, fake, fake,
+                                    ws_bytes, 0, cl.FP16) == cl.EUNSUPPORTED
+    assert cl.ciera_update_cache(fake, fake, 1000, 1, fake, ws_bytes, 0,
+                                 cl.FP16) == cl.EUNSUPPORTED
+    assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 512, fake, fake,
+                                    fake, ws_bytes, 0, 4) == cl.EINVAL
+    assert cl.ciera_encoded_bound(1000, 1, cl.FP16) == 0
+    assert cl.ciera_encoded_bound(1000, 512, 4) == 0
     assert cl.ciera_encode(fake, fake, 1000, 512, 0, fake + 8, 1 << 20, 0,
                            fake, ws_bytes, 0) == cl.EINVAL
     assert cl.ciera_encode(fake, fake, 1 << 32, 512, 0, fake, 1 << 40, 0,
