@@ -40,8 +40,8 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
 MEASURED_TRAFFIC = {
     ("olmoe_layer_c0.1", 512): (
-        "a57d94fd033a8de8fd695b084c8834f464670219f8e3bc228de5059d60189627",
-        1779235297),
+        "886db9add6058ca7cbdd2ff8ee4f23f5c2311f03ba864c6340a63d01d7bec8ef",
+        1779225185),
 }
 
 
@@ -301,6 +301,96 @@ def time_ans(S, steps, stream, cache_is_w2):
                     "ans_decode_kernel + decode_kernel"}
 
 
+def time_f16(wl, B, dev, steps, stream):
+    """The same layer geometry in fp16 (the paper's second precision, Table
+    2): N(0, std) weights rounded to fp16, the workload's forced exponent
+    change rate, R encoded shards gathered in HBM; encode of rank 0's shard
+    and decode of all R, alternating W -> W' and back, checked exact."""
+    import torch
+    from paper_2609_04609_amd import ciera, synth
+    R, n = wl.shards, wl.shard_elems
+    c = wl.rate if wl.rate else 0.001
+    W = torch.empty(R * n, dtype=torch.int16, device=dev)
+    W2 = torch.empty_like(W)
+    for j in range(R):
+        w = synth.normal_f16_bits(n, wl.std, synth.seed_for(wl.name + "f16",
+                                                               j, 0), dev)
+        W[j * n:(j + 1) * n].copy_(w)
+        W2[j * n:(j + 1) * n].copy_(
+            synth.forced_bernoulli_f16_bits(w, c, synth.seed_for(
+                wl.name + "f16", j, 1)))
+    cap = int(ciera.ciera_encoded_bound(n, B, ciera.FP16))
+    ws_e = ciera.Workspace(n, 1, B, dev)
+    ws_d = ciera.Workspace(n, R, B, dev)
+    tmp = torch.empty(cap, dtype=torch.uint8, device=dev)
+    nb = torch.zeros(1, dtype=torch.int64, device=dev)
+    out = torch.empty_like(W)
+    cache = torch.empty(R * n, dtype=torch.uint8, device=dev)
+
+    def gather(src, raw):
+        parts, tots = [], []
+        for j in range(R):
+            ciera.encode_t(src[j * n:(j + 1) * n],
+                           None if raw else cache[j * n:(j + 1) * n], B, ws_e,
+                           tmp, raw=raw, out_bytes=nb, fp16=True)
+            t = int(nb.item())
+            tots.append(t)
+            parts.append(tmp[:t].clone())
+        offs = np.cumsum([0] + tots[:-1]).astype(np.int64)
+        return torch.cat(parts), torch.from_numpy(offs).to(dev), tots
+
+    g0, o0, _ = gather(W, True)
+    ciera.decode_gathered_t(g0, o0, n, B, out, cache, ws_d, fp16=True)
+    del g0
+    gA, oA, tA = gather(W2, False)
+    ciera.decode_gathered_t(gA, oA, n, B, out, cache, ws_d, fp16=True)
+    gB, oB, _ = gather(W, False)
+    ciera.decode_gathered_t(gB, oB, n, B, out, cache, ws_d, fp16=True)
+    torch.cuda.synchronize()
+    send = cache[:n].clone()  # exp(W)
+    hA = gA[:64].cpu().numpy()
+    E0 = int(hA[32:40].view(np.uint64)[0])
+    pairs = [(W2, gA, oA), (W, gB, oB)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
+           for _ in range(steps)]
+    for i in range(steps + 2):
+        w_in, g, o = pairs[i % 2]
+        e = evs[i - 2] if i >= 2 else None
+        if e: e[0].record(stream)
+        ciera.encode_t(w_in[:n], send, B, ws_e, tmp, fp16=True)
+        if e: e[1].record(stream)
+        ciera.update_cache_t(send, tmp, n, B, ws_e, fp16=True)
+        if e: e[2].record(stream)
+        ciera.decode_gathered_t(g, o, n, B, out, cache, ws_d, fp16=True)
+        if e: e[3].record(stream)
+    torch.cuda.synchronize()
+    last = (steps + 1) % 2
+    if not torch.equal(out, pairs[last][0]) or ws_d.error() or ws_e.error():
+        raise RuntimeError("fp16 steps are not exact")
+    t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
+    t_dec = np.mean([e[2].elapsed_time(e[3]) for e in evs]) / 1e3
+    nbk = -(-n // B)
+    bm = -(-nbk // 8)
+    S_sm = n + 3 * (-(-n // 8))
+    exc = lambda E: 5 * (-(-E // 8))
+    E_list = []
+    for j in range(R):
+        h = gA[int(oA[j]):int(oA[j]) + 64].cpu().numpy()
+        E_list.append(int(h[32:40].view(np.uint64)[0]))
+    alg_enc = 2 * n + n + S_sm + bm + exc(E0) + 64
+    alg_dec = sum(64 + S_sm + bm + (n - E) + exc(E) + 2 * n + E
+                  for E in E_list)
+    return {"workload": f"{wl.name} geometry in fp16, forced c={c * 100:g}%",
+            "wire_ratio": round(sum(tA) / (2.0 * R * n), 5),
+            "encode_us": round(t_enc * 1e6, 2),
+            "encode_hbm_frac": round(alg_enc / t_enc / 1e9 / HBM_PEAK_GBPS, 4),
+            "decode_us": round(t_dec * 1e6, 2),
+            "decode_bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
+            "decode_hbm_gbps": round(alg_dec / t_dec / 1e9, 1),
+            "decode_hbm_frac": round(alg_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
+            "exceptions_local": E0}
+
+
 XGMI_GATHER_BPS = 7 * 153e9  # one MI355X's 7 xGMI links, direct gather
 
 
@@ -470,6 +560,9 @@ def run(args):
               if B >= 16 else None)
     ans = (time_ans(S, args.steps, stream, last_even)
            if B >= 16 and args.ans else None)
+    f16 = (time_f16(wl, B, dev, args.steps, stream)
+           if args.fp16 and B >= 16 and wl.name.startswith("olmoe_layer")
+           else None)
     overlap = (time_overlap(S, args.overlap_layers, 3, last_even)
                if args.overlap_layers > 0 and wl.name.startswith("olmoe_layer")
                else None)
@@ -508,6 +601,7 @@ def run(args):
         "encode_hashed": hashed,
         "ans": ans,
         "overlap": overlap,
+        "fp16": f16,
         "update_cache": {"us": round(t_upd * 1e6, 2),
                          "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
                          "alg_bytes": b_upd},
@@ -556,6 +650,8 @@ def main():
                     action="store_false")
     ap.add_argument("--no-ans", dest="ans", action="store_false",
                     help="skip the rANS-coded exception measurements")
+    ap.add_argument("--no-fp16", dest="fp16", action="store_false",
+                    help="skip the fp16 measurement")
     ap.add_argument("--overlap-layers", type=int, default=4,
                     help="layer groups in the overlap measurement (0: skip)")
     ap.add_argument("--copy-calibration", action="store_true",
