@@ -318,16 +318,19 @@ __global__ __launch_bounds__(kThreads) void ans_copy_kernel(AnsEncArgs a) {
 // ============================================================== decoding ==
 
 // Grid (workgroups per shard, shards). A workgroup checks its shard's coded
-// section, builds the slot table (symbol | (f - 1) << 8 | (slot - cum) << 20)
-// and then decodes chunks round by round, each wave staging its chunk's
-// stream in LDS. Any inconsistency sets CIERA_DEVERR_FORMAT; every access
-// stays inside the section and the shard's exception list.
+// section and builds the slot table (symbol | (f - 1) << 8 | (slot - cum)
+// << 20) in LDS; then every wave decodes chunks on its own (no further
+// barrier). A wave keeps its stream's words in registers: three blocks of
+// 128 words, lane l holding words 2l and 2l + 1 of each; the words a step
+// needs lie in the first two blocks and are fetched with a cross-lane read,
+// the third is the next block loaded ahead. Any inconsistency sets
+// CIERA_DEVERR_FORMAT; every access stays inside the section and the shard's
+// exception list.
 __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   __shared__ uint32_t s_slot[kAnsM];
   __shared__ uint32_t s_freq[256];
   __shared__ uint32_t s_cum[256];
   __shared__ uint32_t s_red[kWaves];
-  __shared__ __align__(16) uint32_t s_st[kWaves][kAnsStreamMax / 4];
   const uint32_t j = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint64_t off = a.offsets ? a.offsets[j] : 0ull;
@@ -368,47 +371,36 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
     }
     s_slot[slot] = lo | ((s_freq[lo] - 1u) << 8) | ((slot - s_cum[lo]) << 20);
   }
+  __syncthreads();
   const uint32_t *ends = reinterpret_cast<const uint32_t *>(sec + kAnsFixed);
   const uint8_t *streams = sec + kAnsFixed + 4ull * K;
   const uint64_t avail = C - kAnsFixed - 4ull * K;
   uint8_t *const list = a.ans_exc + uint64_t(j) * a.ans_stride;
-  const uint32_t per_round = gridDim.x * kWaves;
-  const uint32_t rounds = (K + per_round - 1) / per_round;
-  for (uint32_t r = 0; r < rounds; ++r) {
-    const uint32_t c = (r * gridDim.x + blockIdx.x) * kWaves + wave;
-    const bool act = c < K;
-    uint32_t start = 0, end = 0;
-    bool good = act;
-    if (act) {
-      start = c ? ends[c - 1] : 0u;
-      end = ends[c];
-      good = start <= end && end <= avail && ((start | end) & 3u) == 0 &&
-             end - start >= 256u && end - start <= kAnsStreamMax;
-    }
-    __syncthreads();  // the previous round's streams are consumed
-    if (good) {
-      const uint32_t *src = reinterpret_cast<const uint32_t *>(streams + start);
-      for (uint32_t k = uint32_t(lane); k < (end - start) / 4; k += 64)
-        s_st[wave][k] = src[k];
-    }
-    __syncthreads();
-    if (!act) continue;
-    if (!good) {
+  for (uint32_t c = blockIdx.x * kWaves + uint32_t(wave); c < K;
+       c += gridDim.x * kWaves) {
+    const uint32_t start = c ? ends[c - 1] : 0u;
+    const uint32_t end = ends[c];
+    if (!(start <= end && end <= avail && ((start | end) & 3u) == 0 &&
+          end - start >= 256u && end - start <= kAnsStreamMax)) {
       if (lane == 0) set_err(a.ctl, CIERA_DEVERR_FORMAT);
       continue;
     }
-    uint32_t x = s_st[wave][lane];
+    const uint8_t *st = streams + start;
+    const uint32_t wbytes = end - start - 256u;  // words and padding
+    const uint32_t nwords = wbytes / 2u;
+    const uint8_t *wsrc = st + 256;
+    auto block = [&](uint32_t b) -> uint32_t {
+      const uint32_t o = b * 256u + 4u * uint32_t(lane);
+      return o < wbytes ? ld32(wsrc + o) : 0u;
+    };
+    uint32_t x = ld32(st + 4u * uint32_t(lane));
+    uint32_t w0 = block(0), w1 = block(1), w2 = block(2);
+    uint32_t next = 3, base = 0;  // word index of w0's first word
     bool bad = x < kAnsL;
-    const uint16_t *wq = reinterpret_cast<const uint16_t *>(&s_st[wave][64]);
-    const uint32_t nwords = (end - start - 256u) / 2u;
     uint32_t rd = 0;
     const uint64_t lo = uint64_t(c) * kAnsChunk;
     const uint32_t len = uint32_t(E - lo < kAnsChunk ? E - lo : kAnsChunk);
     uint8_t *dst = list + lo;
-    // Branch-free steps: every lane decodes, lanes past the chunk's end keep
-    // their state; the word read is clamped into the stream and used only
-    // by the lanes that need one.
-    const uint32_t last = nwords ? nwords - 1u : 0u;
     for (uint32_t t = 0; t < (len + 63) / 64; ++t) {
       const uint32_t i = t * 64 + uint32_t(lane);
       const bool live = i < len;
@@ -420,16 +412,29 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
       const bool need = live && x < kAnsL;
       const uint64_t m = __ballot(need);
       const uint32_t idx = rd + lanes_below(m);
-      const uint32_t w = wq[idx < last ? idx : last];
+      const uint32_t rel = idx - base;  // < 192: rd - base < 128
+      const int src = int((rel & 127u) >> 1);
+      const uint32_t pa = uint32_t(__shfl(int(w0), src, 64));
+      const uint32_t pb = uint32_t(__shfl(int(w1), src, 64));
+      const uint32_t pair = rel < 128u ? pa : pb;
+      const uint32_t w = (rel & 1u) ? (pair >> 16) : (pair & 0xFFFFu);
       bad = bad || (need && idx >= nwords);
       x = need ? ((x << 16) | w) : x;
       rd += uint32_t(__popcll(m));
+      if (rd - base >= 128u) {  // uniform: slide the window by one block
+        w0 = w1;
+        w1 = w2;
+        w2 = block(next++);
+        base += 128u;
+      }
     }
     // every state back at L, the words used up, only zero padding after
     bad = bad || x != kAnsL;
     const uint32_t used = 256u + 2u * rd;
     if (((used + 3u) & ~3u) != end - start) bad = true;
-    else if (rd < nwords && wq[rd] != 0) bad = true;
+    else if (rd < nwords &&
+             reinterpret_cast<const uint16_t *>(wsrc)[rd] != 0)
+      bad = true;
     if (__ballot(bad) != 0ull && lane == 0) set_err(a.ctl, CIERA_DEVERR_FORMAT);
   }
 }
@@ -453,7 +458,7 @@ hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s) {
   if (a.ans_exc == nullptr || a.nshards == 0) return hipSuccess;
   const uint64_t kmax = ans_kmax(a.n);
   if (kmax == 0) return hipSuccess;
-  uint64_t g = (1024 + a.nshards - 1) / a.nshards;
+  uint64_t g = (2048 + a.nshards - 1) / a.nshards;
   const uint64_t need = (kmax + kWaves - 1) / kWaves;
   if (g > need) g = need;
   if (g == 0) g = 1;
