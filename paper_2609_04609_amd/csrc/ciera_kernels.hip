@@ -1205,7 +1205,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
 // ============================================== element exceptions (B = 1) ==
 // At B = 1 the bitmap has one bit per value: octet o of the shard owns bitmap
 // byte o, and the exception list holds the changed exponent bytes in value
-// order (the encoder is encode_wave_kernel<..., true>). Within a decode tile
+// order (the encoder is encode_pass_kernel<..., true, ...>). Within a decode tile
 // the octets are ranked by a wave scan per 64-octet segment and a scan of the
 // segment totals; a per-shard scan of per-tile counts gives the tile start.
 
