@@ -112,6 +112,10 @@ enum ciera_status {
                               warm-up; tensors the selection rule leaves out) */
 #define CIERA_FP16 0x2u    /* fp16 values (format above; B >= 16); also the
                               flag of the fp16 decode, cache update and bound */
+#define CIERA_ENC_UPDATE_CACHE 0x4u /* also bring exp_cache forward in place
+                              (the "cache is updated" step of the sender),
+                              as ciera_update_cache on the output would; not
+                              with CIERA_ENC_RAW */
 
 /* Largest encoded size of an n-value shard at block size B (host; flags 0
  * or CIERA_FP16). It covers both the compressed form with every block
@@ -138,8 +142,8 @@ int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
 int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
                           hipStream_t stream);
 
-/* Sender side of Algorithm 1 for one shard (Section 3.1). flags: 0,
- * CIERA_ENC_RAW, CIERA_FP16 or both.
+/* Sender side of Algorithm 1 for one shard (Section 3.1). flags: any of
+ * CIERA_ENC_RAW, CIERA_FP16, CIERA_ENC_UPDATE_CACHE (not with RAW).
  *   w_new      n bf16 values as 16-bit patterns.
  *   exp_cache  n exponent bytes from the previous iteration (read only; NULL
  *              allowed only with CIERA_ENC_RAW).
@@ -147,10 +151,12 @@ int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
  *              shard (header + sections + zero padding).
  *   out_bytes  optional device u64 that receives the total encoded size (the
  *              same value as the header's `total`); may be NULL.
- * Encoding is a pure function of (w_new, exp_cache, B, flags): calling it
- * twice gives identical bytes. The sender's own cache is brought forward
- * separately (ciera_update_cache), or is the own-rank slot of the caches
- * ciera_decode_gathered updates. n_elems must be below 2^32. */
+ * Without CIERA_ENC_UPDATE_CACHE encoding is a pure function of (w_new,
+ * exp_cache, B, flags): calling it twice gives identical bytes, and the
+ * sender's cache is brought forward separately (ciera_update_cache) or is the
+ * own-rank slot of the caches ciera_decode_gathered updates. With it, pass 1
+ * writes the new exponents of every changed value into exp_cache (which
+ * nothing else may read during the call). n_elems must be below 2^32. */
 int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                  uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                  void *out, uint64_t out_capacity, uint64_t *out_bytes,

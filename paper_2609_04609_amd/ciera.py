@@ -20,6 +20,7 @@ OK, EINVAL, ENOSPC, EUNSUPPORTED, EFORMAT, EHIP = 0, -1, -2, -3, -4, -5
 DEVERR_FORMAT, DEVERR_ALIGN, DEVERR_BOUNDS, DEVERR_NOSPACE = 1, 2, 4, 8
 ENC_RAW = 0x1
 FP16 = 0x2
+ENC_UPDATE_CACHE = 0x4
 WS_ANS = 0x1
 SELECT_STOP_AT_MISFIT = 0x1
 HEADER_BYTES = 64
@@ -218,10 +219,12 @@ class Workspace:
 
 
 def encode_t(w_bits, cache, block_elems, ws, out, raw=False, out_bytes=None,
-             fp16=False):
-    """Encode a 1-D int16 bit tensor into ``out`` (uint8, bound-sized)."""
+             fp16=False, update_cache=False):
+    """Encode a 1-D int16 bit tensor into ``out`` (uint8, bound-sized); with
+    update_cache the cache is brought forward in place."""
     n = w_bits.numel()
-    flags = (ENC_RAW if raw else 0) | (FP16 if fp16 else 0)
+    flags = ((ENC_RAW if raw else 0) | (FP16 if fp16 else 0) |
+             (ENC_UPDATE_CACHE if update_cache else 0))
     rc = ciera_encode(_ptr(w_bits), _ptr(cache), n, block_elems, flags,
                       _ptr(out), out.numel(), _ptr(out_bytes), ws.ptr,
                       ws.nbytes, _stream())

@@ -110,7 +110,8 @@ namespace {
 // Shared by both compressed encoders: `hashed` selects the HashCache detector
 // (hash_in, hash_out) over exact compare with exp_cache.
 int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
-                      const uint64_t *hash_in, uint64_t *hash_out,
+                      uint8_t *cache_out, const uint64_t *hash_in,
+                      uint64_t *hash_out,
                       uint64_t n_elems, uint32_t l, void *out,
                       uint64_t *out_bytes, void *workspace,
                       uint64_t workspace_bytes, hipStream_t stream,
@@ -121,6 +122,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   EncArgs a{};
   a.w = w_new;
   a.cache = exp_cache;
+  a.cache_out = cache_out;
   a.n = n_elems;
   a.log2B = l;
   a.num_tiles = uint32_t(tiles);
@@ -147,9 +149,12 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                  hipStream_t stream) {
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
-  if (flags & ~(CIERA_ENC_RAW | CIERA_FP16)) return CIERA_EINVAL;
+  if (flags & ~(CIERA_ENC_RAW | CIERA_FP16 | CIERA_ENC_UPDATE_CACHE))
+    return CIERA_EINVAL;
   const bool raw = flags & CIERA_ENC_RAW;
   const bool f16 = flags & CIERA_FP16;
+  const bool upd = flags & CIERA_ENC_UPDATE_CACHE;
+  if (upd && raw) return CIERA_EINVAL;
   if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
   if (!out || (n_elems && !w_new) || (!raw && n_elems && !exp_cache))
     return CIERA_EINVAL;
@@ -166,9 +171,11 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                ? CIERA_OK
                : CIERA_EHIP;
   }
-  return encode_compressed(w_new, exp_cache, nullptr, nullptr, n_elems,
-                           uint32_t(l), out, out_bytes, workspace,
-                           workspace_bytes, stream, false, f16);
+  return encode_compressed(w_new, exp_cache,
+                           upd ? const_cast<uint8_t *>(exp_cache) : nullptr,
+                           nullptr, nullptr, n_elems, uint32_t(l), out,
+                           out_bytes, workspace, workspace_bytes, stream, false,
+                           f16);
 }
 
 int ciera_hash_blocks(const uint16_t *w, uint64_t n_elems,
@@ -206,7 +213,7 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
     return CIERA_EINVAL;
   if (out_capacity < ciera_encoded_bound(n_elems, block_elems, 0))
     return CIERA_ENOSPC;
-  return encode_compressed(w_new, nullptr, hash_in, hash_out, n_elems,
+  return encode_compressed(w_new, nullptr, nullptr, hash_in, hash_out, n_elems,
                            uint32_t(l), out, out_bytes, workspace,
                            workspace_bytes, stream, true, false);
 }

@@ -87,6 +87,7 @@ inline uint64_t enc_tiles(uint64_t n, uint32_t log2B) {
 struct EncArgs {
   const uint16_t *w;
   const uint8_t *cache;
+  uint8_t *cache_out;  // == cache to bring the cache forward in pass 1, or null
   uint64_t n;
   uint32_t log2B;
   uint32_t num_tiles;

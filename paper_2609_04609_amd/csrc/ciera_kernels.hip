@@ -480,6 +480,9 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
           mask[u] = ELEMS ? (bytes_ne4(e.x, cv[u].x) |
                              (bytes_ne4(e.y, cv[u].y) << 4))
                           : uint32_t((e.x != cv[u].x) || (e.y != cv[u].y));
+          // the sender's cache brought forward: only octets that differ
+          if (a.cache_out && mask[u])
+            *reinterpret_cast<uint2 *>(a.cache_out + elem) = e;
         }
       }
     } else {
@@ -515,6 +518,8 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
             mask[u] = ELEMS ? (bytes_ne4(e.x, cv.x) |
                                (bytes_ne4(e.y, cv.y) << 4))
                             : uint32_t((e.x != cv.x) || (e.y != cv.y));
+            if (a.cache_out && mask[u])
+              store_b8<VEC>(a.cache_out + elem, e, valid);
           }
         }
         if (HASH) hash_terms(uint32_t(u), cbase, word, ta[u], tb[u]);

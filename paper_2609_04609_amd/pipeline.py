@@ -96,9 +96,7 @@ class OverlapPipeline:
         n, B = self.n, self.B
         with torch.cuda.stream(st_send):
             ciera.encode_t(w_in, self.send[i], B, self.ws_enc[i],
-                           self.enc_out[i])
-            ciera.update_cache_t(self.send[i], self.enc_out[i], n, B,
-                                 self.ws_enc[i])
+                           self.enc_out[i], update_cache=True)
             if ev is not None:
                 ev["enc"][i].record(st_send)
         with torch.cuda.stream(st_link):
@@ -163,15 +161,13 @@ class OverlapPipeline:
         main = torch.cuda.current_stream()
         w_in, g, off, link_us = self._inputs()
         out = {}
-        names = ["encode+update", "link", "decode", "compute"]
+        names = ["encode", "link", "decode", "compute"]
         acc = {k: [] for k in names}
         for _ in range(reps):
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
             ev[0].record(main)
             ciera.encode_t(w_in, self.send[0], self.B, self.ws_enc[0],
-                           self.enc_out[0])
-            ciera.update_cache_t(self.send[0], self.enc_out[0], self.n,
-                                 self.B, self.ws_enc[0])
+                           self.enc_out[0], update_cache=True)
             ev[1].record(main)
             torch.cuda._sleep(int(link_us / self.us_per_cycle))
             ev[2].record(main)
@@ -197,9 +193,7 @@ class OverlapPipeline:
         w_back, g, off = ((S.W[:self.n], S.gB, S.offB) if self.parity == 0
                           else (S.W2[:self.n], S.gA, S.offA))
         ciera.encode_t(w_back, self.send[i], self.B, self.ws_enc[i],
-                       self.enc_out[i])
-        ciera.update_cache_t(self.send[i], self.enc_out[i], self.n, self.B,
-                             self.ws_enc[i])
+                       self.enc_out[i], update_cache=True)
         ciera.decode_gathered_t(g, off, self.n, self.B, self.outs[i],
                                 self.caches[i], self.ws_dec[i])
         torch.cuda.synchronize()

@@ -152,3 +152,24 @@ def test_value_format_is_checked(gu, orc):
     torch.cuda.synchronize()
     assert ws.error() == ciera.DEVERR_FORMAT
     assert torch.all(out == 5)
+
+
+def test_encode_f16_with_cache_update(gu, orc):
+    from paper_2609_04609_amd import ciera
+    B, n = 512, 3 * 16384 + 17
+    ws = ciera.Workspace(n, 1, B)
+    w, w2 = _pair(n, 21, 0.004)
+    cache_h = orc.split_f16(gu.host_u16(w))[0]
+    expect = orc.encode_f16(gu.host_u16(w2), cache_h, B)
+    c_o = cache_h.copy()
+    orc.update_cache_f16(c_o, expect, n)
+    cache = gu.dev_u8(cache_h)
+    cap = int(ciera.ciera_encoded_bound(n, B, ciera.FP16))
+    out = torch.full((cap,), 0xA5, dtype=torch.uint8, device="cuda")
+    nbytes = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ciera.encode_t(w2, cache, B, ws, out, out_bytes=nbytes, fp16=True,
+                   update_cache=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u8(out)[:int(nbytes.item())],
+                                  expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), c_o)

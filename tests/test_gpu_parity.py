@@ -265,3 +265,34 @@ def test_round_trip_chain_on_gpu(gu, orc, B):
         ws = [synth.forced_bernoulli_bits(x, 0.002, 7000 + 10 * t + j)
               for j, x in enumerate(ws)]
     assert ws_e.error() == 0 and ws_d.error() == 0
+
+
+@pytest.mark.parametrize("B", [1, 16, 512, 4096])
+def test_encode_with_cache_update(gu, orc, B):
+    """CIERA_ENC_UPDATE_CACHE: the same bytes as the pure encode, and the
+    cache afterwards equals the oracle's update of it from those bytes (the
+    exponents of W'); also with a cache pointer off the 8-byte grid."""
+    from paper_2609_04609_amd import ciera
+    ws = ciera.Workspace(262147, 1, B)
+    for i, n in enumerate([1, 9, 4097, 16385, 3 * 16384 + 17, 262147]):
+        w, w2 = gu.pair(n, 600 * B + i, c=0.003)
+        cache_h, _ = orc.split(gu.host_u16(w))
+        expect = orc.encode(gu.host_u16(w2), cache_h, B)
+        c_o = cache_h.copy()
+        orc.update_cache(c_o, expect, n)
+        for shift in (0, 3):
+            buf = torch.zeros(n + 8, dtype=torch.uint8, device="cuda")
+            cache = buf[shift:shift + n]
+            cache.copy_(gu.dev_u8(cache_h))
+            cap = int(ciera.ciera_encoded_bound(n, B))
+            out = torch.full((cap,), 0xA5, dtype=torch.uint8, device="cuda")
+            nbytes = torch.zeros(1, dtype=torch.int64, device="cuda")
+            ciera.encode_t(w2, cache, B, ws, out, out_bytes=nbytes,
+                           update_cache=True)
+            torch.cuda.synchronize()
+            total = int(nbytes.item())
+            np.testing.assert_array_equal(gu.host_u8(out)[:total], expect,
+                                          err_msg=f"n={n} B={B}")
+            np.testing.assert_array_equal(gu.host_u8(cache), c_o,
+                                          err_msg=f"n={n} B={B} s={shift}")
+            assert ws.error() == 0

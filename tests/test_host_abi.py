@@ -86,8 +86,14 @@ def test_host_argument_checks(cl):
     assert cl.ciera_encode(fake, 0, 1000, 512, 0, fake, 1 << 20, 0, fake,
                            ws_bytes, 0) == cl.EINVAL
     # unknown flag, unaligned output, too-large shard
-    assert cl.ciera_encode(fake, fake, 1000, 512, 4, fake, 1 << 20, 0, fake,
-                           ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_encode(fake, fake, 1000, 512, 0x80000000, fake, 1 << 20,
+                           0, fake, ws_bytes, 0) == cl.EINVAL
+    # the fused cache update needs a cache and no raw form
+    assert cl.ciera_encode(fake, fake, 1000, 512,
+                           cl.ENC_RAW | cl.ENC_UPDATE_CACHE, fake, 1 << 20, 0,
+                           fake, ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_encode(fake, 0, 1000, 512, cl.ENC_UPDATE_CACHE, fake,
+                           1 << 20, 0, fake, ws_bytes, 0) == cl.EINVAL
     # fp16 needs B >= 16 (encode, decode, cache update, bound)
     assert cl.ciera_encode(fake, fake, 1000, 1, cl.FP16, fake, 1 << 20, 0,
                            fake, ws_bytes, 0) == cl.EUNSUPPORTED
@@ -96,9 +102,9 @@ def test_host_argument_checks(cl):
     assert cl.ciera_update_cache(fake, fake, 1000, 1, fake, ws_bytes, 0,
                                  cl.FP16) == cl.EUNSUPPORTED
     assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 512, fake, fake,
-                                    fake, ws_bytes, 0, 4) == cl.EINVAL
+                                    fake, ws_bytes, 0, 0x80000000) == cl.EINVAL
     assert cl.ciera_encoded_bound(1000, 1, cl.FP16) == 0
-    assert cl.ciera_encoded_bound(1000, 512, 4) == 0
+    assert cl.ciera_encoded_bound(1000, 512, 0x80000000) == 0
     assert cl.ciera_encode(fake, fake, 1000, 512, 0, fake + 8, 1 << 20, 0,
                            fake, ws_bytes, 0) == cl.EINVAL
     assert cl.ciera_encode(fake, fake, 1 << 32, 512, 0, fake, 1 << 40, 0,
