@@ -41,8 +41,8 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
 MEASURED_TRAFFIC = {
     ("olmoe_layer_c0.1", 512): (
-        "886db9add6058ca7cbdd2ff8ee4f23f5c2311f03ba864c6340a63d01d7bec8ef",
-        1779225185),
+        "3ee5f7a4d34310e6607cf35ddae0ad565fabb15b0d560da7a4bdaea6a9881709",
+        1776379973),
 }
 
 
