@@ -39,21 +39,23 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
+_SRC_SHA = "c3785c7d001ed3568516470f698e7891fc1e3fb9e0db0ab18fa6ae8008d472cc"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512): (
-        "3ee5f7a4d34310e6607cf35ddae0ad565fabb15b0d560da7a4bdaea6a9881709",
-        1776379973),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1776362911),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1869983938),
 }
 
 
-def measured_traffic(name, B):
+def measured_traffic(name, B, dtype="bf16"):
     import hashlib
-    rec = MEASURED_TRAFFIC.get((name, B))
+    rec = MEASURED_TRAFFIC.get((name, B, dtype))
     if rec is None:
         return None
     with open(KERNEL_SRC, "rb") as f:
         digest = hashlib.sha256(f.read()).hexdigest()
     return rec[1] if digest == rec[0] else None
+
+
 METRIC = ("encode & N-shard decode GB/s (bf16 weights), % HBM peak, "
           "wire-bytes ratio")
 
@@ -410,6 +412,8 @@ def time_f16(wl, B, dev, steps, stream):
             "decode_bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
             "decode_hbm_gbps": round(alg_dec / t_dec / 1e9, 1),
             "decode_hbm_frac": round(alg_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
+            "decode_alg_bytes": alg_dec,
+            "decode_traffic": measured_traffic(wl.name, B, "fp16"),
             "exceptions_local": E0}
 
 

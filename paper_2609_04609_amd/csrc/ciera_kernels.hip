@@ -989,6 +989,10 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   __shared__ uint32_t s_bits[kBitWords];
   __shared__ uint32_t s_pre[kBitWords];
   __shared__ uint32_t s_red[4];
+  // fp16 whole tiles: the tile's sign/top-mantissa planes (3 bytes per
+  // octet) come through LDS in 8-byte loads instead of 3 byte loads a lane
+  constexpr uint32_t kHiPairs = F16 && !UPDATE_ONLY ? 3 * T / 64 : 1;
+  __shared__ uint2 s_hi[kHiPairs];
 
   const uint32_t j = blockIdx.y;
   const uint64_t base = uint64_t(blockIdx.x) * T;
@@ -1060,12 +1064,20 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   // low mantissa bytes, and the sign and top mantissa bits from 3 planes)
   uint2 smv[OCT], hiv[OCT];
   if (F16 && !UPDATE_ONLY) {
+    if (full) {
+      // n % 8 == 0 on this path, so the tile's planes are 8-byte aligned;
+      // the barriers of the prefix sum below order these stores
+      const uint2 *hp =
+          reinterpret_cast<const uint2 *>(sm_in + n + 3 * (base >> 3));
+      for (uint32_t i = tid; i < kHiPairs; i += kThreads) s_hi[i] = hp[i];
+    } else {
 #pragma unroll
-    for (int u = 0; u < OCT; ++u) {
-      const uint64_t elem =
-          base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-      hiv[u] = elem < n ? unplane<3>(sm_in + n + 3 * (elem >> 3))
-                        : make_uint2(0u, 0u);
+      for (int u = 0; u < OCT; ++u) {
+        const uint64_t elem =
+            base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
+        hiv[u] = elem < n ? unplane<3>(sm_in + n + 3 * (elem >> 3))
+                          : make_uint2(0u, 0u);
+      }
     }
   }
   if (!UPDATE_ONLY) {
@@ -1156,8 +1168,11 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
       if (!UPDATE_ONLY) {
         uint4 wv;
         if (F16) {
-          merge4_f16(ev[u].x, smv[u].x, hiv[u].x, wv.x, wv.y);
-          merge4_f16(ev[u].y, smv[u].y, hiv[u].y, wv.z, wv.w);
+          const uint32_t o = uint32_t(wave * OCT + u) * 64u + lane;
+          const uint2 hv = unplane<3>(
+              reinterpret_cast<const uint8_t *>(s_hi) + 3 * o);
+          merge4_f16(ev[u].x, smv[u].x, hv.x, wv.x, wv.y);
+          merge4_f16(ev[u].y, smv[u].y, hv.y, wv.z, wv.w);
         } else {
           merge4(ev[u].x, smv[u].x, wv.x, wv.y);
           merge4(ev[u].y, smv[u].y, wv.z, wv.w);

@@ -81,7 +81,8 @@ def test_encode_f16_unaligned_and_every_exponent(gu, orc):
 
 
 @pytest.mark.parametrize("B", [16, 512, 4096])
-@pytest.mark.parametrize("R,n", [(1, 1), (3, 16385), (4, 40000), (5, 262147)])
+@pytest.mark.parametrize("R,n", [(1, 1), (3, 16385), (4, 40000), (3, 81928),
+                                 (5, 262147)])
 def test_decode_gathered_f16_matches_oracle(gu, orc, B, R, n):
     from paper_2609_04609_amd import ciera
     ws_e = ciera.Workspace(n, 1, B)
