@@ -39,10 +39,10 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "c3785c7d001ed3568516470f698e7891fc1e3fb9e0db0ab18fa6ae8008d472cc"
+_SRC_SHA = "af57e59ada2a49c52b8f475e3386c21cfdb2654f963a93ce581b92c1fe337c7c"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1776362911),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1869983938),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780043599),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1870211476),
 }
 
 

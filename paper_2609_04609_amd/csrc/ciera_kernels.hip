@@ -106,6 +106,39 @@ __device__ __forceinline__ uint2 unplane(const uint8_t *g) {
   return v;
 }
 
+// ---------------------------------------------------- streaming accesses --
+// Bytes that a call reads or writes once (the sign|mantissa plane, the
+// exception list, the decoded values, the cache bytes a pass compares) go
+// through non-temporal loads and stores (the nt bit), so that they do not
+// push out what is read again: the bitmap words every decode tile counts in
+// front of it, and the W' lines the exception pass of the encode re-reads
+// (pass 1 loads W' normally for that reason). Measured on the codec step of
+// the OLMoE layer: decode 316 -> 279 us, encode 39 -> 32 us.
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 ld_nt8(const uint8_t *p) {
+  const u32x2_t x =
+      __builtin_nontemporal_load(reinterpret_cast<const u32x2_t *>(p));
+  return make_uint2(x.x, x.y);
+}
+
+__device__ __forceinline__ uint4 ld_nt16(const uint16_t *p) {
+  const u32x4_t x =
+      __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(x.x, x.y, x.z, x.w);
+}
+
+__device__ __forceinline__ void st_nt8(uint8_t *p, uint2 v) {
+  const u32x2_t x = {v.x, v.y};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x2_t *>(p));
+}
+
+__device__ __forceinline__ void st_nt16(uint16_t *p, uint4 v) {
+  const u32x4_t x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t *>(p));
+}
+
 // ------------------------------------------------- octet loads and stores --
 // `valid` is the number of in-range values of the octet (1..8). VEC means the
 // base pointers are aligned for vector accesses; the ragged last octet and
@@ -118,6 +151,13 @@ __device__ __forceinline__ uint4 load_w8(const uint16_t *p, uint32_t valid) {
   for (uint32_t i = 0; i < 8; ++i)
     if (i < valid) v[i >> 1] |= uint32_t(p[i]) << ((i & 1) * 16);
   return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// load_w8 for the encode's second read of W' (non-temporal: its last use)
+template <bool VEC>
+__device__ __forceinline__ uint4 reread_w8(const uint16_t *p, uint32_t valid) {
+  if (VEC && valid == 8) return ld_nt16(p);
+  return load_w8<VEC>(p, valid);
 }
 
 template <bool VEC>
@@ -452,8 +492,7 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
       if (!HASH) {
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-          cv[u] = *reinterpret_cast<const uint2 *>(
-              a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
+          cv[u] = ld_nt8(a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -471,7 +510,7 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
           split4(wv[u].x, wv[u].y, e.x, sm.x);
           split4(wv[u].z, wv[u].w, e.y, sm.y);
         }
-        if (OUT) *reinterpret_cast<uint2 *>(sm_out + elem) = sm;
+        if (OUT) st_nt8(sm_out + elem, sm);
         if (HASH) {
           hash_terms(uint32_t(u), cbase,
                      uint64_t(e.x) | (uint64_t(e.y) << 32), ta[u], tb[u]);
@@ -710,7 +749,10 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
     } else {
       split4(wv.x, wv.y, e.x, t0.x);
       split4(wv.z, wv.w, e.y, t0.y);
-      store_b8<VEC>(exc_out + pos, e, valid);
+      if (VEC && valid == 8)
+        st_nt8(exc_out + pos, e);
+      else
+        store_b8<VEC>(exc_out + pos, e, valid);
     }
   };
   // bitmap bytes per tile (B >= 16)
@@ -759,7 +801,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
-      if (mask[u]) wv[u] = load_w8<VEC>(a.w + elem, octet_valid(elem, n));
+      if (mask[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -806,7 +848,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
       const uint64_t elem = tbase + uint64_t(o) * 8;
       const uint32_t bl = (o << 3) >> log2B;
       ch[u] = live && elem < n && ((pick<4>(fw, bl >> 6) >> (bl & 63u)) & 1ull);
-      if (ch[u]) wv[u] = load_w8<VEC>(a.w + elem, octet_valid(elem, n));
+      if (ch[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
     }
     // (3) the offset, overlapping the loads above
     const uint32_t sib =
@@ -1084,8 +1126,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
     if (full) {
 #pragma unroll
       for (int u = 0; u < OCT; ++u)
-        smv[u] = *reinterpret_cast<const uint2 *>(
-            sm_in + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
+        smv[u] =
+            ld_nt8(sm_in + base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u);
     } else {
 #pragma unroll
       for (int u = 0; u < OCT; ++u) {
@@ -1158,7 +1200,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
     for (int u = 0; u < OCT; ++u) {
       if (F16 && ch[u])
         ev[u] = unplane<5>(src[u]);
-      else if (!UPDATE_ONLY || ch[u])
+      else if (!UPDATE_ONLY)
+        ev[u] = ld_nt8(src[u]);
+      else if (ch[u])  // the cache update alone: plain loads measured faster
         ev[u] = *reinterpret_cast<const uint2 *>(src[u]);
     }
 #pragma unroll
@@ -1177,7 +1221,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
           merge4(ev[u].x, smv[u].x, wv.x, wv.y);
           merge4(ev[u].y, smv[u].y, wv.z, wv.w);
         }
-        *reinterpret_cast<uint4 *>(out + elem) = wv;
+        st_nt16(out + elem, wv);
       }
     }
   } else {
