@@ -47,27 +47,36 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
   if (l < 0 || (flags & ~CIERA_WS_ANS)) return 0;
   // encode: one count per tile plus the total
   const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n_elems, uint32_t(l)) + 1);
-  // decode at B = 1: the same per shard
-  const uint64_t dec =
-      l == 0 ? kWsCtlBytes + 4 * uint64_t(nshards ? nshards : 1) *
-                                 dec_count_stride(dec_tiles(n_elems))
-             : kWsCtlBytes;
+  // decode: the offset of every tile of every shard
+  const uint32_t ns = nshards ? nshards : 1;
+  const uint64_t dec = dec_ws_bytes(n_elems, ns);
   uint64_t need = enc > dec ? enc : dec;
   if ((flags & CIERA_WS_ANS) && l >= kAnsMinLog2B) {
-    const uint64_t e = ans_enc_bytes(n_elems);
-    const uint64_t d = ans_dec_bytes(n_elems, nshards ? nshards : 1);
-    const uint64_t ans = ans_ws_offset(n_elems, uint32_t(l)) + (e > d ? e : d);
+    // coding one shard, decoding ns shards
+    const uint64_t e = ans_ws_offset(n_elems, uint32_t(l), 1) +
+                       ans_enc_bytes(n_elems);
+    const uint64_t d = ans_ws_offset(n_elems, uint32_t(l), ns) +
+                       ans_dec_bytes(n_elems, ns);
+    const uint64_t ans = e > d ? e : d;
     need = ans > need ? ans : need;
   }
   return (need + 255) & ~uint64_t(255);
 }
 
 namespace {
-bool dec_workspace_ok(uint64_t n, uint32_t nshards, int l, uint64_t bytes) {
-  if (bytes < kWsCtlBytes) return false;
-  if (l != 0) return true;
-  return (bytes - kWsCtlBytes) / 4 >=
-         uint64_t(nshards) * dec_count_stride(dec_tiles(n));
+bool dec_workspace_ok(uint64_t n, uint32_t nshards, uint64_t bytes) {
+  return bytes >= dec_ws_bytes(n, nshards);
+}
+// Every decode tile needs the flagged blocks in front of it. Counting them in
+// the tile re-reads half the shard's bitmap per tile on average, which grows
+// with tiles x bitmap; past about 20 us of such reads (128 MB) one prefix
+// pass over the bitmaps is cheaper than its extra launch.
+constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
+bool use_prefix_pass(uint64_t n, uint32_t nshards, int l) {
+  if (l == 0) return false;
+  const uint64_t inline_bytes = uint64_t(nshards) * dec_tiles(n) *
+                                bitmap_bytes(n, uint32_t(l)) / 2;
+  return inline_bytes > kPrefixPassBytes;
 }
 uint32_t *tile_excl_of(void *workspace) {
   return reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
@@ -77,7 +86,7 @@ uint32_t *tile_excl_of(void *workspace) {
 uint8_t *ans_lists_of(void *workspace, uint64_t bytes, uint64_t n,
                       uint32_t nshards, int l) {
   if (l < kAnsMinLog2B) return nullptr;
-  const uint64_t off = ans_ws_offset(n, uint32_t(l));
+  const uint64_t off = ans_ws_offset(n, uint32_t(l), nshards);
   if (bytes < off || bytes - off < ans_dec_bytes(n, nshards)) return nullptr;
   return static_cast<uint8_t *>(workspace) + off;
 }
@@ -233,7 +242,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
   if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(gathered, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
-  if (!dec_workspace_ok(shard_elems, nshards, l, workspace_bytes))
+  if (!dec_workspace_ok(shard_elems, nshards, workspace_bytes))
     return CIERA_ENOSPC;
   DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(gathered);
@@ -250,6 +259,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
                                  nshards, l);
   a.ans_stride = pad16(shard_elems);
   a.f16 = f16;
+  a.prefix_pass = use_prefix_pass(shard_elems, nshards, l);
   const bool vec =
       (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
@@ -268,7 +278,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   if (!encoded || (n_elems && !exp_cache) || !workspace) return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
-  if (!dec_workspace_ok(n_elems, 1, l, workspace_bytes)) return CIERA_ENOSPC;
+  if (!dec_workspace_ok(n_elems, 1, workspace_bytes)) return CIERA_ENOSPC;
   DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(encoded);
   a.offsets = nullptr;
@@ -283,6 +293,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
       f16 ? nullptr : ans_lists_of(workspace, workspace_bytes, n_elems, 1, l);
   a.ans_stride = pad16(n_elems);
   a.f16 = f16;
+  a.prefix_pass = use_prefix_pass(n_elems, 1, l);
   const bool vec = aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
@@ -296,7 +307,7 @@ int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
   if (!encoded || !workspace) return CIERA_EINVAL;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
   if (!aligned(encoded, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
-  const uint64_t off = ans_ws_offset(n_elems, uint32_t(l));
+  const uint64_t off = ans_ws_offset(n_elems, uint32_t(l), 1);
   if (workspace_bytes < off || workspace_bytes - off < ans_enc_bytes(n_elems))
     return CIERA_ENOSPC;
   const uint64_t kmax = ans_kmax(n_elems);

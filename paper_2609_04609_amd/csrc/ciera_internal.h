@@ -70,6 +70,9 @@ constexpr int kThreads = 256;  // 4 wave64 per workgroup
 #endif
 constexpr uint32_t kDecOct = CIERA_DEC_OCT;
 constexpr uint64_t kDecTile = uint64_t(kThreads) * 8 * kDecOct;
+constexpr uint32_t kDecTileLog2 = uint32_t(__builtin_ctzll(kDecTile));
+static_assert((kDecTile & (kDecTile - 1)) == 0 && kDecTile >= 4096,
+              "a decode tile holds whole blocks of up to 4096 values");
 
 // Encode: one wave per tile. A tile is one 4096-value chunk (eight octets per
 // lane) when B <= 512, and 8 blocks (8B values, several chunks) when B > 512,
@@ -118,19 +121,26 @@ struct DecArgs {
   uint16_t *out;            // nullptr for the cache-update-only pass
   uint8_t *cache;
   WsCtl *ctl;
-  uint32_t *tile_excl;      // B = 1: first exception of every decode tile
+  // per shard and decode tile: the flagged blocks (B >= 16) or changed values
+  // (B = 1) in front of the tile, dec_count_stride(tiles) words per shard
+  uint32_t *tile_excl;
+  bool prefix_pass;  // B >= 16: tile_excl was filled by tile_prefix_kernel
 };
 
 __host__ __device__ inline uint64_t dec_tiles(uint64_t n) {
   return (n + kDecTile - 1) / kDecTile;
 }
-// B = 1 decode: per-shard count segments (tiles + total), 16-byte aligned
+// decode: per-shard count segments (tiles + total), 16-byte aligned
 __host__ __device__ inline uint64_t dec_count_stride(uint64_t tiles) {
   return (tiles + 1 + 3) & ~uint64_t(3);
 }
+inline uint64_t dec_ws_bytes(uint64_t n, uint32_t nshards) {
+  return kWsCtlBytes + 4 * uint64_t(nshards) * dec_count_stride(dec_tiles(n));
+}
 
 // ---- rANS workspace (B >= 16) ----
-// The area starts at ans_ws_offset(n, B), past everything else the calls use.
+// The area starts at ans_ws_offset(n, B, nshards), past everything else the
+// calls use.
 struct AnsCtl {
   uint32_t hist[256];  // exception byte counts
   uint32_t freq[256];  // quantised frequencies (sum kAnsM)
@@ -142,10 +152,12 @@ struct AnsCtl {
 static_assert(sizeof(AnsCtl) == 4096, "rANS control block is 4 KB");
 constexpr int kAnsMinLog2B = 4;  // rANS-coded sections need B >= 16
 inline uint64_t ans_kmax(uint64_t n) { return (n + kAnsChunk - 1) / kAnsChunk; }
-// past the control block and the encode counts, which every B >= 16 call uses
-inline uint64_t ans_ws_offset(uint64_t n, uint32_t log2B) {
-  const uint64_t t = enc_tiles(n, log2B);
-  return (kWsCtlBytes + 4 * (t + 1) + 255) & ~uint64_t(255);
+// past the control block, the encode counts and the decode tile offsets of
+// nshards shards
+inline uint64_t ans_ws_offset(uint64_t n, uint32_t log2B, uint32_t nshards) {
+  const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n, log2B) + 1);
+  const uint64_t dec = dec_ws_bytes(n, nshards);
+  return ((enc > dec ? enc : dec) + 255) & ~uint64_t(255);
 }
 // coding one shard: control, words per chunk, final states, word slots
 inline uint64_t ans_enc_bytes(uint64_t n) {

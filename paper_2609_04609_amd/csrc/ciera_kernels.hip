@@ -1018,6 +1018,57 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   return v;
 }
 
+// Decode, B >= 16, step 1: for every shard the flagged blocks in front of
+// each decode tile, an exclusive scan of the tiles' bitmap counts (one
+// 1024-thread workgroup per shard; the bitmap is 1/(8B) of the shard). Raw
+// and malformed shards write nothing: their decode tiles do not read it.
+__global__ __launch_bounds__(kScanThreads) void tile_prefix_kernel(DecArgs a) {
+  __shared__ uint32_t s_wave[kScanThreads / 64];
+  __shared__ uint32_t s_total;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t j = blockIdx.x;
+  const ShardView sv = read_shard(a, j, false);
+  if (!sv.ok || sv.mode == kModeRaw) return;
+  const uint64_t n = a.n;
+  const uint32_t tiles = uint32_t(dec_tiles(n));
+  const uint32_t *bmp32 = reinterpret_cast<const uint32_t *>(
+      sv.enc + kHeaderBytes + pad16(sm_bytes(n, a.f16)));
+  // the bitmap section holds pad16(bm) bytes, zero past the last block
+  const uint64_t words = pad16(bitmap_bytes(n, a.log2B)) >> 2;
+  const uint32_t tb = kDecTileLog2 - a.log2B;  // log2 of the blocks per tile
+  uint32_t *c = a.tile_excl + uint64_t(j) * dec_count_stride(tiles);
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < tiles; base += kScanThreads) {
+    const uint32_t t = base + tid;
+    uint32_t cnt = 0;
+    if (t < tiles) {
+      const uint64_t b0 = uint64_t(t) << tb;  // the tile's first block
+      if (tb >= 5) {
+        const uint64_t w0 = b0 >> 5, w1 = w0 + (uint64_t(1) << (tb - 5));
+        for (uint64_t w = w0; w < w1 && w < words; ++w) cnt += __popc(bmp32[w]);
+      } else if ((b0 >> 5) < words) {
+        cnt = __popc((bmp32[b0 >> 5] >> (b0 & 31u)) & ((1u << (1u << tb)) - 1u));
+      }
+    }
+    const uint32_t incl = wave_incl_scan(cnt);
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t run = 0;
+      for (int w = 0; w < kScanThreads / 64; ++w) {
+        const uint32_t x = s_wave[w];
+        s_wave[w] = run;
+        run += x;
+      }
+      s_total = run;
+    }
+    __syncthreads();
+    if (t < tiles) c[t] = carry + s_wave[wave] + incl - cnt;
+    carry += s_total;
+    __syncthreads();
+  }
+}
+
 // UPDATE_ONLY: the ExpCache patch alone (no sign+mantissa, no output).
 // A whole tile issues its loads in two batches (sign|mantissa bytes together
 // with the bitmap words, then one cache-or-exception load per octet, chosen
@@ -1151,8 +1202,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
     if (i == 0) word &= ~((1u << (fb & 31u)) - 1u);
     s_bits[i] = word;
   }
-  uint32_t cnt = 0;
-  {
+  // flagged blocks in front of the tile: from tile_prefix_kernel, or
+  // counted here straight from the bitmap
+  uint32_t prefix;
+  if (a.prefix_pass) {
+    prefix = a.tile_excl[uint64_t(j) * dec_count_stride(gridDim.x) + blockIdx.x];
+    __syncthreads();  // s_bits, and the fp16 planes in s_hi
+  } else {
+    uint32_t cnt = 0;
     const uint64_t full4 = w0 >> 2;  // whole 16-byte chunks before word w0
     const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
     for (uint64_t i = tid; i < full4; i += kThreads) {
@@ -1163,8 +1220,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
     if (tid < 4 && wr < w0) cnt += __popc(bmp32[wr]);
     if (tid == 4 && (fb & 31u))
       cnt += __popc(bmp32[w0] & ((1u << (fb & 31u)) - 1u));
+    prefix = block_sum(cnt, s_red);  // also orders s_bits and s_hi
   }
-  const uint32_t prefix = block_sum(cnt, s_red);  // also orders s_bits
   if (tid == 0) {
     uint32_t run = 0;
     for (uint32_t i = 0; i < nw; ++i) {
@@ -1554,6 +1611,9 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
     }
     return hipGetLastError();
   }
+  if (a.prefix_pass)
+    hipLaunchKernelGGL(tile_prefix_kernel, dim3(a.nshards), dim3(kScanThreads),
+                       0, s, a);
   if (a.f16) {
     constexpr int O = int(kDecOct);
     if (upd) {

@@ -84,6 +84,10 @@ def test_encode_f16_unaligned_and_every_exponent(gu, orc):
 @pytest.mark.parametrize("R,n", [(1, 1), (3, 16385), (4, 40000), (3, 81928),
                                  (5, 262147)])
 def test_decode_gathered_f16_matches_oracle(gu, orc, B, R, n):
+    _decode_f16_case(gu, orc, B, R, n)
+
+
+def _decode_f16_case(gu, orc, B, R, n):
     from paper_2609_04609_amd import ciera
     ws_e = ciera.Workspace(n, 1, B)
     encs, caches, vals = [], [], []
@@ -109,6 +113,13 @@ def test_decode_gathered_f16_matches_oracle(gu, orc, B, R, n):
     np.testing.assert_array_equal(gu.host_u16(out), expect)
     np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
     assert ws.error() == 0
+
+
+def test_decode_f16_with_prefix_pass(gu, orc):
+    """16 fp16 shards of 6,000,008 values at B = 16: large enough bitmaps
+    that the decode scans the tile offsets in a pass of its own; equal to
+    the oracle's decode of the same bytes and to W'."""
+    _decode_f16_case(gu, orc, 16, 16, 6_000_008)
 
 
 @pytest.mark.parametrize("B", [16, 512, 4096])

@@ -166,6 +166,45 @@ def test_decode_gathered_matches_oracle(gu, orc, B, R, n_s):
     assert ws.error() == 0
 
 
+@pytest.mark.parametrize("n_s", [6_000_008, 6_000_003])
+def test_decode_with_prefix_pass(gu, orc, n_s):
+    """16 shards of about 6M values at B = 16: counting each tile's offset in
+    the tile would re-read about 138 MB of bitmap per call, so the decode
+    scans every shard's tile counts in a pass of its own first. One raw shard
+    in the middle; n % 8 == 0 takes the vector path, the other size the
+    element-wise one. Values and caches equal the oracle's; the cache update
+    of one 24M-value shard takes the same pass."""
+    from paper_2609_04609_amd import ciera
+    R, B = 16, 16
+    raw_mask = [j == 7 for j in range(R)]
+    gathered, offs, cache0, values = _decode_case(gu, orc, R, n_s, B,
+                                                  raw_mask, 31337 + n_s % 8)
+    cache_o = cache0.copy()
+    expect = orc.decode_gathered(gathered, offs, n_s, cache_o)
+    np.testing.assert_array_equal(expect, values)
+    out = torch.empty(R * n_s, dtype=torch.int16, device="cuda")
+    cache = gu.dev_u8(cache0)
+    ws = ciera.Workspace(n_s, R, B)
+    ciera.decode_gathered_t(gu.dev_u8(gathered),
+                            torch.from_numpy(offs.view(np.int64)).to("cuda"),
+                            n_s, B, out, cache, ws)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u16(out), expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+    assert ws.error() == 0
+    del gathered, cache0, values, out, cache
+    n1 = 4 * n_s
+    g1, o1, c1, _ = _decode_case(gu, orc, 1, n1, B, [False], 99 + n_s % 8)
+    c1_o = c1.copy()
+    orc.update_cache(c1_o, g1, n1)
+    c1_d = gu.dev_u8(c1)
+    ws1 = ciera.Workspace(n1, 1, B)
+    ciera.update_cache_t(c1_d, gu.dev_u8(g1), n1, B, ws1)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u8(c1_d), c1_o)
+    assert ws1.error() == 0
+
+
 @pytest.mark.parametrize("B", [1, 16, 512, 4096])
 def test_update_cache_matches_oracle(gu, orc, B):
     from paper_2609_04609_amd import ciera
