@@ -39,10 +39,10 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "af57e59ada2a49c52b8f475e3386c21cfdb2654f963a93ce581b92c1fe337c7c"
+_SRC_SHA = "6d3124b809544fbe7a7baa70b595d87e7e921d3147bf0ae9e0b40c1cf9b15500"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780043599),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1870211476),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780015440),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1870176021),
 }
 
 
