@@ -107,11 +107,13 @@ class Setup:
         self.nbytes = torch.zeros(1, dtype=torch.int64, device=dev)
         self.out = torch.empty(R * n, dtype=torch.int16, device=dev)
         self.cache = torch.empty(R * n, dtype=torch.uint8, device=dev)
-        # first gather after warm-up is raw: it seeds every receiver cache
-        g0, off0, _ = self._gather(self.W, None, raw=True)
-        ciera.decode_gathered_t(g0, off0, n, B, self.out, self.cache,
-                                self.ws_dec)
-        del g0
+        # the first gather after warm-up is raw: it seeds every receiver
+        # cache (shard by shard, so no raw copy of the layer is held)
+        for j in range(R):
+            ciera.encode_t(self.W[j * n:(j + 1) * n], None, B, self.ws_enc,
+                           self.tmp, raw=True, out_bytes=self.nbytes)
+            ciera.update_cache_t(self.cache[j * n:(j + 1) * n], self.tmp, n,
+                                 B, self.ws_enc)
         # A: W -> W' against exp(W);  B: W' -> W against exp(W')
         self.gA, self.offA, self.totA = self._gather(self.W2, self.cache)
         ciera.decode_gathered_t(self.gA, self.offA, n, B, self.out,
@@ -130,25 +132,30 @@ class Setup:
         log(f"encoded 2 x {R} shards; setup {time.time() - t0:.1f}s")
 
     def _gather(self, src, cache, raw=False):
-        """Encode every rank's shard on the GPU and place them back to back."""
+        """Encode every rank's shard on the GPU and place them back to back:
+        one pass for the sizes, then each shard straight into its place (the
+        encoding is deterministic)."""
         import torch
         from paper_2609_04609_amd import ciera
         R, n, B = self.R, self.n, self.B
         totals = []
-        parts = []
         for j in range(R):
             ciera.encode_t(src[j * n:(j + 1) * n],
                            None if raw else cache[j * n:(j + 1) * n], B,
                            self.ws_enc, self.tmp, raw=raw,
                            out_bytes=self.nbytes)
-            t = int(self.nbytes.item())
-            totals.append(t)
-            parts.append(self.tmp[:t].clone())
+            totals.append(int(self.nbytes.item()))
         offs = np.cumsum([0] + totals[:-1]).astype(np.uint64)
-        g = torch.empty(int(sum(totals)), dtype=torch.uint8, device=self.dev)
-        for j, p in enumerate(parts):
-            g[int(offs[j]):int(offs[j]) + totals[j]].copy_(p)
-        del parts
+        # room for a bound-sized write at the last offset
+        g = torch.empty(int(sum(totals)) + self.cap, dtype=torch.uint8,
+                        device=self.dev)
+        for j in range(R):
+            ciera.encode_t(src[j * n:(j + 1) * n],
+                           None if raw else cache[j * n:(j + 1) * n], B,
+                           self.ws_enc, g[int(offs[j]):], raw=raw,
+                           out_bytes=self.nbytes)
+            if int(self.nbytes.item()) != totals[j]:
+                raise RuntimeError("encode is not deterministic")
         off_t = torch.from_numpy(offs.view(np.int64)).to(self.dev)
         return g, off_t, totals
 
@@ -254,13 +261,12 @@ def time_ans(S, steps, stream, cache_is_w2):
     ws1 = ciera.Workspace(n, 1, B, S.dev, ans=True)
     wsR = ciera.Workspace(n, R, B, S.dev, ans=True)
 
-    def coded_gather(g, off):
+    def coded_gather(g, off, tots):
         parts, totals = [], []
         buf = torch.empty(S.cap, dtype=torch.uint8, device=S.dev)
         offs = off.cpu().numpy().astype(np.int64)
-        ends = list(offs[1:]) + [g.numel()]
         for j in range(R):
-            buf[:ends[j] - offs[j]].copy_(g[offs[j]:ends[j]])
+            buf[:tots[j]].copy_(g[offs[j]:offs[j] + tots[j]])
             ciera.ans_code_t(buf, n, B, ws1, out_bytes=S.nbytes)
             t = int(S.nbytes.item())
             totals.append(t)
@@ -269,8 +275,8 @@ def time_ans(S, steps, stream, cache_is_w2):
         gg = torch.cat(parts)
         return gg, torch.from_numpy(o).to(S.dev), totals
 
-    gA, oA, tA = coded_gather(S.gA, S.offA)
-    gB, oB, tB = coded_gather(S.gB, S.offB)
+    gA, oA, tA = coded_gather(S.gA, S.offA, S.totA)
+    gB, oB, tB = coded_gather(S.gB, S.offB, S.totB)
     h = gA[:64].cpu().numpy()
     mode0 = int(h[6:8].view(np.uint16)[0])
     bm = -(-(-(-n // B)) // 8)
