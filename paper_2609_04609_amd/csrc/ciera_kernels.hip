@@ -1160,9 +1160,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
     if (full) {
       // n % 8 == 0 on this path, so the tile's planes are 8-byte aligned;
       // the barriers of the prefix sum below order these stores
-      const uint2 *hp =
-          reinterpret_cast<const uint2 *>(sm_in + n + 3 * (base >> 3));
-      for (uint32_t i = tid; i < kHiPairs; i += kThreads) s_hi[i] = hp[i];
+      const uint8_t *hp = sm_in + n + 3 * (base >> 3);
+      for (uint32_t i = tid; i < kHiPairs; i += kThreads)
+        s_hi[i] = ld_nt8(hp + 8 * i);
     } else {
 #pragma unroll
       for (int u = 0; u < OCT; ++u) {
