@@ -72,6 +72,10 @@ bool dec_workspace_ok(uint64_t n, uint32_t nshards, uint64_t bytes) {
 // with tiles x bitmap; past about 20 us of such reads (128 MB) one prefix
 // pass over the bitmaps is cheaper than its extra launch.
 constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
+// Large layers also walk their tiles in runs of 32 per XCD (measured on the
+// DeepSeek-style layer: 2-5% faster than in order; the OLMoE layer, which
+// counts in the tile, is fastest in order).
+constexpr uint32_t kXcdRunLog2 = 5;
 bool use_prefix_pass(uint64_t n, uint32_t nshards, int l) {
   if (l == 0) return false;
   const uint64_t inline_bytes = uint64_t(nshards) * dec_tiles(n) *
@@ -260,6 +264,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
   a.ans_stride = pad16(shard_elems);
   a.f16 = f16;
   a.prefix_pass = use_prefix_pass(shard_elems, nshards, l);
+  a.xcd_run_log2 = a.prefix_pass ? kXcdRunLog2 : 0u;
   const bool vec =
       (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
@@ -294,6 +299,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   a.ans_stride = pad16(n_elems);
   a.f16 = f16;
   a.prefix_pass = use_prefix_pass(n_elems, 1, l);
+  a.xcd_run_log2 = a.prefix_pass ? kXcdRunLog2 : 0u;
   const bool vec = aligned(exp_cache, 8);
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;

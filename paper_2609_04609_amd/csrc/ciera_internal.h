@@ -125,6 +125,7 @@ struct DecArgs {
   // (B = 1) in front of the tile, dec_count_stride(tiles) words per shard
   uint32_t *tile_excl;
   bool prefix_pass;  // B >= 16: tile_excl was filled by tile_prefix_kernel
+  uint32_t xcd_run_log2;  // B >= 16: log2 of the tiles per XCD turn (0: in order)
 };
 
 __host__ __device__ inline uint64_t dec_tiles(uint64_t n) {

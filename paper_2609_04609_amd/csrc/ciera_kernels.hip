@@ -1087,10 +1087,27 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   constexpr uint32_t kHiPairs = F16 && !UPDATE_ONLY ? 3 * T / 64 : 1;
   __shared__ uint2 s_hi[kHiPairs];
 
-  const uint32_t j = blockIdx.y;
-  const uint64_t base = uint64_t(blockIdx.x) * T;
+  // Workgroups go to the 8 XCDs in turn: workgroup L = 8k + x is XCD x's
+  // k-th. With runs of G = 2^a.xcd_run_log2 tiles it takes tile
+  // (k / G) 8G + x G + k mod G of the (shard, tile) order, so each XCD walks
+  // G neighbouring tiles at a time; the tail short of 8G tiles keeps the
+  // plain order.
+  const uint32_t ntiles = gridDim.x;
+  uint32_t j = blockIdx.y, tix = blockIdx.x;
+  if (a.xcd_run_log2) {
+    const uint32_t g = a.xcd_run_log2;
+    const uint64_t total = uint64_t(ntiles) * gridDim.y;
+    uint64_t L = uint64_t(blockIdx.y) * ntiles + blockIdx.x;
+    if (L < ((total >> (g + 3)) << (g + 3))) {
+      const uint64_t k = L >> 3;
+      L = ((k >> g) << (g + 3)) | ((L & 7u) << g) | (k & ((1u << g) - 1u));
+      j = uint32_t(L / ntiles);
+      tix = uint32_t(L % ntiles);
+    }
+  }
+  const uint64_t base = uint64_t(tix) * T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const ShardView sv = read_shard(a, j, blockIdx.x == 0 && tid == 0);
+  const ShardView sv = read_shard(a, j, tix == 0 && tid == 0);
   if (!sv.ok) return;
   const uint64_t n = a.n;
   if (base >= n) return;
@@ -1206,7 +1223,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   // counted here straight from the bitmap
   uint32_t prefix;
   if (a.prefix_pass) {
-    prefix = a.tile_excl[uint64_t(j) * dec_count_stride(gridDim.x) + blockIdx.x];
+    prefix = a.tile_excl[uint64_t(j) * dec_count_stride(ntiles) + tix];
     __syncthreads();  // s_bits, and the fp16 planes in s_hi
   } else {
     uint32_t cnt = 0;
