@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "ciera.h"
 #include "ciera_internal.h"
 
@@ -320,10 +322,11 @@ __global__ __launch_bounds__(kThreads) void ans_copy_kernel(AnsEncArgs a) {
 // Grid (workgroups per shard, shards). A workgroup checks its shard's coded
 // section and builds the slot table (symbol | (f - 1) << 8 | (slot - cum)
 // << 20) in LDS; then every wave decodes chunks on its own (no further
-// barrier). A wave keeps its stream's words in registers: three blocks of
-// 128 words, lane l holding words 2l and 2l + 1 of each; the words a step
-// needs lie in the first two blocks and are fetched with a cross-lane read,
-// the third is the next block loaded ahead. Any inconsistency sets
+// barrier). A wave keeps a window of its stream's words in a ring of two
+// 128-word blocks in LDS (each lane writes words 2l and 2l + 1 of a block);
+// the words a step needs lie in that window and each lane that renormalises
+// reads its own, and the next block is loaded ahead into a register and
+// written over the block the window leaves. Any inconsistency sets
 // CIERA_DEVERR_FORMAT; every access stays inside the section and the shard's
 // exception list.
 __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
@@ -331,8 +334,13 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   __shared__ uint32_t s_freq[256];
   __shared__ uint32_t s_cum[256];
   __shared__ uint32_t s_red[kWaves];
+  __shared__ uint32_t s_ring[kWaves][128];  // two blocks of 128 words a wave
   const uint32_t j = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // wave-uniform, so that the chunk loop and its lengths stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  uint32_t *const ring = s_ring[wave];
+  const uint16_t *const ring16 = reinterpret_cast<const uint16_t *>(ring);
   const uint64_t off = a.offsets ? a.offsets[j] : 0ull;
   if (off & 15ull) return;  // the decode kernel reports it
   const uint8_t *enc = a.gathered + off;
@@ -394,40 +402,53 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
       return o < wbytes ? ld32(wsrc + o) : 0u;
     };
     uint32_t x = ld32(st + 4u * uint32_t(lane));
-    uint32_t w0 = block(0), w1 = block(1), w2 = block(2);
-    uint32_t next = 3, base = 0;  // word index of w0's first word
+    __builtin_amdgcn_wave_barrier();  // the previous chunk's reads are done
+    ring[lane] = block(0);
+    ring[64 + lane] = block(1);
+    uint32_t pre = block(2);      // the block after the window
+    uint32_t next = 3, base = 0;  // word index of the window's first word
+    uint32_t wlim = nwords;       // words left in the stream from base
+    __builtin_amdgcn_wave_barrier();
     bool bad = x < kAnsL;
     uint32_t rd = 0;
     const uint64_t lo = uint64_t(c) * kAnsChunk;
     const uint32_t len = uint32_t(E - lo < kAnsChunk ? E - lo : kAnsChunk);
     uint8_t *dst = list + lo;
-    for (uint32_t t = 0; t < (len + 63) / 64; ++t) {
+    // 64 symbols a step, one per lane; only the last step of the last chunk
+    // can be partial (TAIL)
+    auto step = [&](uint32_t t, auto tail) {
+      constexpr bool TAIL = decltype(tail)::value;
       const uint32_t i = t * 64 + uint32_t(lane);
-      const bool live = i < len;
+      const bool live = !TAIL || i < len;
       const uint32_t e = s_slot[x & (kAnsM - 1u)];
       const uint32_t xd =
           (((e >> 8) & 0xFFFu) + 1u) * (x >> kAnsScale) + (e >> 20);
-      if (live) dst[i] = uint8_t(e & 0xFFu);
+      if (live) dst[i] = uint8_t(e);
       x = live ? xd : x;
       const bool need = live && x < kAnsL;
       const uint64_t m = __ballot(need);
-      const uint32_t idx = rd + lanes_below(m);
-      const uint32_t rel = idx - base;  // < 192: rd - base < 128
-      const int src = int((rel & 127u) >> 1);
-      const uint32_t pa = uint32_t(__shfl(int(w0), src, 64));
-      const uint32_t pb = uint32_t(__shfl(int(w1), src, 64));
-      const uint32_t pair = rel < 128u ? pa : pb;
-      const uint32_t w = (rel & 1u) ? (pair >> 16) : (pair & 0xFFFFu);
-      bad = bad || (need && idx >= nwords);
+      // the lane's word relative to the window (< 192: rd - base < 128),
+      // counted by mbcnt on top of rd - base
+      const uint32_t rel = __builtin_amdgcn_mbcnt_hi(
+          uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), rd - base));
+      // word base + rel of the stream sits at (base + rel) mod 256 of the ring
+      const uint32_t w = ring16[(base + rel) & 255u];
+      bad = bad || (need && rel >= wlim);
       x = need ? ((x << 16) | w) : x;
       rd += uint32_t(__popcll(m));
       if (rd - base >= 128u) {  // uniform: slide the window by one block
-        w0 = w1;
-        w1 = w2;
-        w2 = block(next++);
+        __builtin_amdgcn_wave_barrier();
+        ring[((base >> 7) & 1u) * 64u + uint32_t(lane)] = pre;
+        __builtin_amdgcn_wave_barrier();
+        pre = block(next++);
         base += 128u;
+        wlim = nwords > base ? nwords - base : 0u;
       }
-    }
+    };
+    const uint32_t full = len / 64;
+    for (uint32_t t = 0; t < full; ++t)
+      step(t, std::integral_constant<bool, false>{});
+    if (len % 64) step(full, std::integral_constant<bool, true>{});
     // every state back at L, the words used up, only zero padding after
     bad = bad || x != kAnsL;
     const uint32_t used = 256u + 2u * rd;
