@@ -124,7 +124,9 @@ uint64_t ciera_encoded_bound(uint64_t n_elems, uint32_t block_elems,
                              uint32_t flags);
 
 /* Workspace bytes for encoding an n-value shard and for decoding (or cache
- * updating) `nshards` such shards at block size B (host). With
+ * updating) `nshards` such shards at block size B (host): a 256-byte control
+ * block, one 32-bit count per 4096-value encode tile and one 32-bit offset
+ * per 16384-value decode tile of every shard. With
  * CIERA_WS_ANS (B >= 16) it also covers ciera_ans_code on such a shard and
  * decoding rANS-coded shards: about 2.1 n bytes for coding, n per shard for
  * decoding. Returns 0 for an unsupported B or flag. */

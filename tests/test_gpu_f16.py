@@ -122,10 +122,11 @@ def test_decode_f16_with_prefix_pass(gu, orc):
     _decode_f16_case(gu, orc, 16, 16, 6_000_008)
 
 
-@pytest.mark.parametrize("B", [16, 512, 4096])
-def test_update_cache_f16(gu, orc, B):
+@pytest.mark.parametrize("B,n", [(16, 3 * 16384 + 17), (512, 3 * 16384 + 17),
+                                 (4096, 3 * 16384 + 17),
+                                 (16, 24_000_008)])  # the prefix pass
+def test_update_cache_f16(gu, orc, B, n):
     from paper_2609_04609_amd import ciera
-    n = 3 * 16384 + 17
     ws = ciera.Workspace(n, 1, B)
     w, w2 = _pair(n, 9 + B, 0.004)
     cache_h = orc.split_f16(gu.host_u16(w))[0]

@@ -68,6 +68,17 @@ def test_sizes_closed_form(cl, orc):
         assert cl.ciera_workspace_bytes(n, 16, 1, cl.WS_ANS) == \
             cl.ciera_workspace_bytes(n, 16, 1)
     assert cl.ciera_workspace_bytes(100, 1, 512, 2) == 0  # unknown flag
+    # every B: the control block, one count per 4096-value encode tile plus
+    # the total, and for each shard one offset per 16384-value decode tile
+    # plus the total (segments 16-byte aligned)
+    for n in [1, 16384, 16385, 88080384]:
+        for R in [1, 16, 128]:
+            for B in [1, 16, 512, 4096]:
+                t_enc = max(1, -(-n // (4096 if B <= 512 else 8 * B)))
+                t_dec = -(-n // 16384)
+                stride = -(-(t_dec + 1) // 4) * 4
+                need = max(256 + 4 * (t_enc + 1), 256 + 4 * R * stride)
+                assert cl.ciera_workspace_bytes(n, R, B) >= need, (n, R, B)
 
 
 def test_host_argument_checks(cl):
