@@ -839,16 +839,19 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
           fw[i >> 3] |= uint64_t(bmp[byte0 + i]) << (8u * (i & 7u));
       }
     }
-    // (2) W' of the changed octets
+    // (2) W' of the changed octets, the first four now, overlapping the
+    // offset; holding all eight across it costs a wave per SIMD (88 VGPRs,
+    // and the OLMoE shard's 1536 workgroups no longer fit in one round)
     bool ch[8];
-    uint4 wv[8];
+    uint4 wv[4];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint32_t o = uint32_t(u) * 64u + lane;
       const uint64_t elem = tbase + uint64_t(o) * 8;
       const uint32_t bl = (o << 3) >> log2B;
       ch[u] = live && elem < n && ((pick<4>(fw, bl >> 6) >> (bl & 63u)) & 1ull);
-      if (ch[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
+      if (u < 4 && ch[u])
+        wv[u & 3] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
     }
     // (3) the offset, overlapping the loads above
     const uint32_t sib =
@@ -856,9 +859,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
     prefix = group_prefix(uint64_t(blockIdx.x) * 4u * per_tile);
     if (!live) return;
     prefix += sib;
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (!ch[u]) continue;
+    auto put_octet = [&](int u, const uint4 &w) {
       const uint32_t o = uint32_t(u) * 64u + lane;
       const uint64_t elem = tbase + uint64_t(o) * 8;
       const uint32_t valid = octet_valid(elem, n);
@@ -870,8 +871,20 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         if (uint32_t(k) < (bl >> 6)) rank += uint32_t(__popcll(fw[k]));
       const uint64_t pos =
           (uint64_t(prefix + rank) << log2B) | ((o << 3) & (B - 1u));
-      if (pos + valid <= n) put_exc(pos, wv[u], valid);
+      if (pos + valid <= n) put_exc(pos, w, valid);
+    };
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (ch[u]) put_octet(u, wv[u]);
+    // (4) the other four
+#pragma unroll
+    for (int u = 4; u < 8; ++u) {
+      const uint64_t elem = tbase + (uint64_t(u) * 64u + lane) * 8;
+      if (ch[u]) wv[u & 3] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
     }
+#pragma unroll
+    for (int u = 4; u < 8; ++u)
+      if (ch[u]) put_octet(u, wv[u & 3]);
   } else {
     // 8 blocks of B > 512 values; the wave copies each changed block's
     // exponents 512 values at a time
