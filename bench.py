@@ -81,25 +81,38 @@ def describe(wl, B):
 
 
 class Setup:
-    """All device buffers of one workload, built before any timing."""
+    """All device buffers of one workload, built before any timing. With
+    raw=True every gather sends raw shards (tensors the selection rule
+    leaves uncompressed)."""
 
     def __init__(self, wl, B, dev):
         import torch
-        from paper_2609_04609_amd import ciera, synth
-        self.wl, self.B, self.dev = wl, B, dev
+        from paper_2609_04609_amd import synth
         R, n = wl.shards, wl.shard_elems
-        self.R, self.n = R, n
         t0 = time.time()
-        self.W = torch.empty(R * n, dtype=torch.int16, device=dev)
-        self.W2 = torch.empty(R * n, dtype=torch.int16, device=dev)
+        W = torch.empty(R * n, dtype=torch.int16, device=dev)
+        W2 = torch.empty(R * n, dtype=torch.int16, device=dev)
         for j in range(R):
             w, w2 = synth.shard_pair(wl, j, dev)
-            self.W[j * n:(j + 1) * n].copy_(w)
-            self.W2[j * n:(j + 1) * n].copy_(w2)
+            W[j * n:(j + 1) * n].copy_(w)
+            W2[j * n:(j + 1) * n].copy_(w2)
             del w, w2
         torch.cuda.synchronize()
         log(f"generated {2 * R * n * 2 / 1e9:.2f} GB of bf16 shards "
             f"in {time.time() - t0:.1f}s")
+        self._build(wl, W, W2, R, n, B, dev, False, t0)
+
+    @classmethod
+    def from_tensors(cls, W, W2, R, n, B, dev, raw=False):
+        S = cls.__new__(cls)
+        S._build(None, W, W2, R, n, B, dev, raw, time.time())
+        return S
+
+    def _build(self, wl, W, W2, R, n, B, dev, raw, t0):
+        import torch
+        from paper_2609_04609_amd import ciera
+        self.wl, self.B, self.dev, self.raw = wl, B, dev, raw
+        self.R, self.n, self.W, self.W2 = R, n, W, W2
         self.ws_enc = ciera.Workspace(n, 1, B, dev)
         self.ws_dec = ciera.Workspace(n, R, B, dev)
         self.cap = int(ciera.ciera_encoded_bound(n, B))
@@ -115,10 +128,12 @@ class Setup:
             ciera.update_cache_t(self.cache[j * n:(j + 1) * n], self.tmp, n,
                                  B, self.ws_enc)
         # A: W -> W' against exp(W);  B: W' -> W against exp(W')
-        self.gA, self.offA, self.totA = self._gather(self.W2, self.cache)
+        self.gA, self.offA, self.totA = self._gather(self.W2, self.cache,
+                                                     raw=raw)
         ciera.decode_gathered_t(self.gA, self.offA, n, B, self.out,
                                 self.cache, self.ws_dec)
-        self.gB, self.offB, self.totB = self._gather(self.W, self.cache)
+        self.gB, self.offB, self.totB = self._gather(self.W, self.cache,
+                                                     raw=raw)
         ciera.decode_gathered_t(self.gB, self.offB, n, B, self.out,
                                 self.cache, self.ws_dec)
         torch.cuda.synchronize()
@@ -158,6 +173,148 @@ class Setup:
                 raise RuntimeError("encode is not deterministic")
         off_t = torch.from_numpy(offs.view(np.int64)).to(self.dev)
         return g, off_t, totals
+
+
+def codec_steps(S, warmup, steps, stream):
+    """The codec step on a Setup (rank 0's encode, bringing its cache
+    forward, then the gathered decode; raw groups encode raw), alternating
+    W -> W' and back. Returns the mean encode and decode times and the wall
+    time per step (s); the last decode is checked bit for bit."""
+    import torch
+    from paper_2609_04609_amd import ciera
+    n, B = S.n, S.B
+
+    def one(s, e):
+        even = (s % 2) == 0
+        w_in = S.W2[:n] if even else S.W[:n]
+        g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
+        if e:
+            e[0].record(stream)
+        if S.raw:
+            ciera.encode_t(w_in, None, B, S.ws_enc, S.tmp, raw=True)
+        else:
+            ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
+                           update_cache=True)
+        if e:
+            e[1].record(stream)
+        ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
+        if e:
+            e[2].record(stream)
+
+    for s in range(warmup):
+        one(s, None)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        one(warmup + s, evs[s])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    expect = S.W2 if (warmup + steps - 1) % 2 == 0 else S.W
+    ok = bool(torch.equal(S.out, expect))
+    if not S.raw:
+        ok = ok and bool(torch.equal(S.cache[:n], S.send_cache))
+    if not ok or S.ws_enc.error() or S.ws_dec.error():
+        raise RuntimeError("codec steps are not exact")
+    t_enc = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / 1e3
+    t_dec = float(np.mean([e[1].elapsed_time(e[2]) for e in evs])) / 1e3
+    return t_enc, t_dec, wall
+
+
+def time_small_configs(B, dev, steps, stream):
+    """The tiny tensor and the single OLMoE expert (natural update, and 1%
+    of exponents forced), R shards each: the codec step as for the layer.
+    These sizes measure launch latency more than bandwidth."""
+    from paper_2609_04609_amd import synth
+    out = {}
+    for name in ("tiny", "olmoe_expert", "olmoe_expert_forced"):
+        wl = synth.WORKLOADS[name]
+        S = Setup(wl, B, dev)
+        t_enc, t_dec, wall = codec_steps(S, 10, steps, stream)
+        n, R = S.n, S.R
+        out[name] = {"workload": describe(wl, B),
+                     "us_per_step": round(wall * 1e6, 2),
+                     "encode_us": round(t_enc * 1e6, 2),
+                     "decode_us": round(t_dec * 1e6, 2),
+                     "bf16_gbps": round((2 * n + 2 * R * n) / wall / 1e9, 1),
+                     "wire_ratio": round(sum(S.totA) / (2.0 * R * n), 5)}
+        del S
+    return out
+
+
+def time_mixed_layer(B, dev, steps, stream):
+    """One layer of the mixed model step (attention q/k/v/o, router, two
+    layer norms and the 64-expert group, 16 shards each) at the steady
+    per-type change rates. The Section 3.2 rule decides per tensor on an
+    xGMI-class link (alpha 10 us, 150 GB/s per peer) from the block change
+    rate of this step's data, with a modelled decode time; the selected
+    tensors form one compressed group and the rest one raw group, and the
+    layer's codec step is both groups' steps. All 16 layers of the model
+    have this shape and these rates."""
+    import torch
+    from paper_2609_04609_amd import ciera, synth
+    R = synth.MIXED_SHARDS
+    shards, dec, ns = {}, {}, {}
+    for name, numel, kind in synth.MIXED_TENSORS:
+        n = numel // R
+        W = torch.empty(R * n, dtype=torch.int16, device=dev)
+        W2 = torch.empty_like(W)
+        for j in range(R):
+            w = synth.normal_bf16_bits(
+                n, 0.02, synth.seed_for("mixed", 0, name, j), dev)
+            W[j * n:(j + 1) * n] = w
+            W2[j * n:(j + 1) * n] = synth.forced_bernoulli_bits(
+                w, synth.STEADY_RATE[kind],
+                synth.seed_for("mixed", 0, name, "u", j))
+        e1 = (W.view(R, n).to(torch.int32) >> 7) & 0xFF
+        e2 = (W2.view(R, n).to(torch.int32) >> 7) & 0xFF
+        nb = -(-n // B)
+        d = torch.nn.functional.pad((e1 != e2).to(torch.int8),
+                                    (0, nb * B - n))
+        q = float(d.view(R, nb, B).amax(dim=2).float().mean())
+        t_dec_model = 5e-6 + R * (4 * n + q * n) / 5.5e12
+        dec[name], _ = ciera.ciera_should_compress(
+            n, B, q, R, 10e-6, 150e9, t_decmp_s=t_dec_model)
+        shards[name] = (W, W2, n)
+        ns[name] = n
+        del e1, e2, d
+    res = {"workload": ("mixed model step, one of 16 identical layers: "
+                        "q/k/v/o 2048x2048, router 2048x64, 2 layer norms "
+                        "of 2048, 64 experts x 3 matrices; R=16, steady "
+                        "per-type rates"),
+           "compressed": sorted(k for k, v in dec.items() if v),
+           "raw": sorted(k for k, v in dec.items() if not v)}
+    total_us, vals = 0.0, 0
+    for raw in (False, True):
+        names = [nm for nm, _, _ in synth.MIXED_TENSORS
+                 if bool(dec[nm]) != raw]
+        if not names:
+            continue
+        n_flat = sum(ns[nm] for nm in names)
+        Wf = torch.empty(R * n_flat, dtype=torch.int16, device=dev)
+        W2f = torch.empty_like(Wf)
+        for j in range(R):
+            off = j * n_flat
+            for nm in names:
+                W, W2, n = shards[nm]
+                Wf[off:off + n] = W[j * n:(j + 1) * n]
+                W2f[off:off + n] = W2[j * n:(j + 1) * n]
+                off += n
+        S = Setup.from_tensors(Wf, W2f, R, n_flat, B, dev, raw=raw)
+        t_enc, t_dec, wall = codec_steps(S, 5, steps, stream)
+        key = "raw_group" if raw else "compressed_group"
+        res[key] = {"values_per_shard": n_flat,
+                    "us_per_step": round(wall * 1e6, 2),
+                    "encode_us": round(t_enc * 1e6, 2),
+                    "decode_us": round(t_dec * 1e6, 2),
+                    "wire_ratio": round(sum(S.totA) / (2.0 * R * n_flat), 5)}
+        total_us += wall * 1e6
+        vals += R * n_flat
+        del S, Wf, W2f
+    res["us_per_layer"] = round(total_us, 2)
+    res["bf16_gbps"] = round(2 * vals / (total_us * 1e-6) / 1e9, 1)
+    return res
 
 
 def time_update_cache(S, steps, stream):
@@ -597,6 +754,10 @@ def run(args):
     overlap = (time_overlap(S, args.overlap_layers, 3, last_even)
                if args.overlap_layers > 0 and wl.name.startswith("olmoe_layer")
                else None)
+    small = (time_small_configs(B, dev, args.steps, stream)
+             if args.others and B >= 16 else None)
+    mixed = (time_mixed_layer(B, dev, min(args.steps, 20), stream)
+             if args.others and B >= 16 else None)
 
     t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
     t_dec = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
@@ -637,6 +798,8 @@ def run(args):
         "ans": ans,
         "overlap": overlap,
         "fp16": f16,
+        "small_configs": small,
+        "mixed_layer": mixed,
         "update_cache": {"us": round(t_upd * 1e6, 2),
                          "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
                          "alg_bytes": b_upd},
@@ -689,6 +852,9 @@ def main():
                     help="skip the fp16 measurement")
     ap.add_argument("--overlap-layers", type=int, default=4,
                     help="layer groups in the overlap measurement (0: skip)")
+    ap.add_argument("--no-others", dest="others", action="store_false",
+                    help="skip the tiny, single-expert and mixed-layer "
+                         "measurements")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")
