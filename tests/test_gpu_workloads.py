@@ -137,15 +137,15 @@ def test_olmoe_expert_matrices(lib, orc, name, B):
                 assert orc.header(G.shard_bytes(j))["E"] == k
 
 
-@pytest.mark.parametrize("B", [512, 1, 64])
-@pytest.mark.parametrize("name", ["olmoe_layer_c0.1", "olmoe_layer_c1",
-                                  "olmoe_layer_c5"])
+# every rate at B = 512 and B = 1; B = 64 at one rate
+@pytest.mark.parametrize("name,B", [
+    (name, B) for name in ("olmoe_layer_c0.1", "olmoe_layer_c1",
+                           "olmoe_layer_c5") for B in (512, 1)
+] + [("olmoe_layer_c1", 64)])
 def test_olmoe_layer_full(lib, orc, name, B):
     """The full 402,653,184-value OLMoE layer: every shard's encoding and the
     16-shard gathered decode, compared with the oracle byte for byte."""
     from paper_2609_04609_amd import synth
-    if B == 64 and name != "olmoe_layer_c1":
-        pytest.skip("B = 64 is covered at one rate")
     wl = synth.WORKLOADS[name]
     W, W2 = _pairs(wl)
     G = Group(lib, W, W2, wl.shards, wl.shard_elems, B)
