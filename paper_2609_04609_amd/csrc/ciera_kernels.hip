@@ -1056,7 +1056,21 @@ __global__ __launch_bounds__(kScanThreads) void tile_prefix_kernel(DecArgs a) {
     uint32_t cnt = 0;
     if (t < tiles) {
       const uint64_t b0 = uint64_t(t) << tb;  // the tile's first block
-      if (tb >= 5) {
+      if (tb >= 7) {
+        // 4 to 32 words: up to eight 16-byte vectors, all loaded before the
+        // sum (the section's word count is a multiple of 4)
+        const uint4 *v4 = reinterpret_cast<const uint4 *>(bmp32) + (b0 >> 7);
+        const uint64_t left = (words >> 2) - (b0 >> 7);
+        const uint32_t nv = 1u << (tb - 7);
+        uint4 x[8];
+#pragma unroll
+        for (uint32_t k = 0; k < 8; ++k)
+          x[k] = k < nv && k < left ? v4[k] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+        for (uint32_t k = 0; k < 8; ++k)
+          cnt += __popc(x[k].x) + __popc(x[k].y) + __popc(x[k].z) +
+                 __popc(x[k].w);
+      } else if (tb >= 5) {
         const uint64_t w0 = b0 >> 5, w1 = w0 + (uint64_t(1) << (tb - 5));
         for (uint64_t w = w0; w < w1 && w < words; ++w) cnt += __popc(bmp32[w]);
       } else if ((b0 >> 5) < words) {
