@@ -24,6 +24,19 @@ bool aligned(const void *p, uintptr_t a) {
   return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
 }
 
+// Bitmap bytes re-read per call past which a separate scan pays for its
+// launch (about 20 us of reads): the decode's prefix pass and the encode's
+// count scan.
+constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
+
+// The encode's exception pass: each 4-tile workgroup counts the bitmap in
+// front of it, half the bitmap on average.
+bool use_count_scan(uint64_t n, uint32_t l) {
+  if (l == 0) return false;
+  const uint64_t groups = (enc_tiles(n, l) + 3) / 4;
+  return groups * bitmap_bytes(n, l) / 2 > kPrefixPassBytes;
+}
+
 }  // namespace
 
 extern "C" {
@@ -71,7 +84,6 @@ bool dec_workspace_ok(uint64_t n, uint32_t nshards, uint64_t bytes) {
 // the tile re-reads half the shard's bitmap per tile on average, which grows
 // with tiles x bitmap; past about 20 us of such reads (128 MB) one prefix
 // pass over the bitmaps is cheaper than its extra launch.
-constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 // Large layers also walk their tiles in runs of 32 per XCD (measured on the
 // DeepSeek-style layer: 2-5% faster than in order; the OLMoE layer, which
 // counts in the tile, is fastest in order).
@@ -149,6 +161,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   a.hash_out = hash_out;
   a.hashed = hashed;
   a.f16 = f16;
+  a.scan_prefix = use_count_scan(n_elems, l);
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }

@@ -99,6 +99,9 @@ struct EncArgs {
   uint64_t *out_bytes;
   WsCtl *ctl;
   uint32_t *counts;  // num_tiles + 1 words
+  // B >= 16: pass 1 writes per-tile counts and a scan turns them into the
+  // exception pass's offsets (else each workgroup counts the bitmap)
+  bool scan_prefix;
   bool f16;  // fp16 values (B >= 16)
   // block-hash detector (B >= 16) in place of exact compare with `cache`
   bool hashed;

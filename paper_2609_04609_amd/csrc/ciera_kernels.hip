@@ -625,7 +625,7 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
     if (lane == 0 && tile < bm16) bmp_out[tile] = uint8_t(fbyte);
     count = __popc(fbyte);
   }
-  if (ELEMS && lane == 0) a.counts[tile] = count;
+  if ((ELEMS || a.scan_prefix) && lane == 0) a.counts[tile] = count;
 
   // the last tile zeroes the padding of the first two sections, before the
   // exception pass reads the bitmap back
@@ -854,11 +854,16 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         wv[u & 3] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
     }
     // (3) the offset, overlapping the loads above
-    const uint32_t sib =
-        wave_popc(uint64_t(blockIdx.x) * 4u * per_tile, byte0);
-    prefix = group_prefix(uint64_t(blockIdx.x) * 4u * per_tile);
-    if (!live) return;
-    prefix += sib;
+    if (a.scan_prefix) {
+      if (!live) return;
+      prefix = a.counts[tile];
+    } else {
+      const uint32_t sib =
+          wave_popc(uint64_t(blockIdx.x) * 4u * per_tile, byte0);
+      prefix = group_prefix(uint64_t(blockIdx.x) * 4u * per_tile);
+      if (!live) return;
+      prefix += sib;
+    }
     auto put_octet = [&](int u, const uint4 &w) {
       const uint32_t o = uint32_t(u) * 64u + lane;
       const uint64_t elem = tbase + uint64_t(o) * 8;
@@ -888,10 +893,15 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   } else {
     // 8 blocks of B > 512 values; the wave copies each changed block's
     // exponents 512 values at a time
-    const uint32_t sib = wave_popc(uint64_t(blockIdx.x) * 4u, tile);
-    prefix = group_prefix(uint64_t(blockIdx.x) * 4u);
-    if (!live) return;
-    prefix += sib;
+    if (a.scan_prefix) {
+      if (!live) return;
+      prefix = a.counts[tile];
+    } else {
+      const uint32_t sib = wave_popc(uint64_t(blockIdx.x) * 4u, tile);
+      prefix = group_prefix(uint64_t(blockIdx.x) * 4u);
+      if (!live) return;
+      prefix += sib;
+    }
     const uint32_t fbyte = tile < bm ? bmp[tile] : 0u;
     uint32_t rank = 0;
     for (uint32_t k = 0; k < 8; ++k) {
@@ -1570,7 +1580,7 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
       hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetExact>), grid,
                          block, 0, s, a);
   }
-  if (elems)
+  if (elems || a.scan_prefix)
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
   if (elems) {

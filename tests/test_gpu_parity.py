@@ -25,6 +25,50 @@ def gu():
     return gpu_util
 
 
+def test_encode_with_count_scan(gu, orc):
+    """A 25,165,832-value shard at B = 16: counting the bitmap in front of
+    every exception-pass workgroup would re-read about 151 MB, so pass 1
+    writes per-tile counts and a scan gives the offsets. Exact compare,
+    the block hash and fp16 all match the oracle byte for byte; the first
+    call after a small one reuses the workspace."""
+    from paper_2609_04609_amd import ciera, synth
+    n, B = 25_165_832, 16
+    ws = ciera.Workspace(n, 1, B)
+    w, w2 = gu.pair(n, 2525, c=0.002)
+    wh, w2h = gu.host_u16(w), gu.host_u16(w2)
+    cache_h = orc.split(wh)[0]
+    # a small call first: its counts and offsets must not leak into the next
+    out, total, _ = gu.gpu_encode(w2[:5000], gu.dev_u8(cache_h[:5000]), B, ws)
+    np.testing.assert_array_equal(gu.host_u8(out)[:total],
+                                  orc.encode(w2h[:5000], cache_h[:5000], B))
+    expect = orc.encode(w2h, cache_h, B)
+    out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
+    assert total == expect.size
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    # the block-hash detector gives the same bytes
+    nblk = -(-n // B)
+    h_in = torch.empty(2 * nblk, dtype=torch.int64, device="cuda")
+    h_out = torch.empty_like(h_in)
+    ciera.hash_blocks_t(w, B, h_in)
+    hb = torch.empty(int(ciera.ciera_encoded_bound(n, B)), dtype=torch.uint8,
+                     device="cuda")
+    nb = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ciera.encode_hashed_t(w2, h_in, h_out, B, ws, hb, out_bytes=nb)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u8(hb)[:int(nb.item())], expect)
+    # fp16 at the same size
+    f = synth.normal_f16_bits(n, 0.02, 2626, "cuda")
+    f2 = synth.forced_bernoulli_f16_bits(f, 0.002, 2627)
+    fc = orc.split_f16(gu.host_u16(f))[0]
+    fb = torch.empty(int(ciera.ciera_encoded_bound(n, B, ciera.FP16)),
+                     dtype=torch.uint8, device="cuda")
+    ciera.encode_t(f2, gu.dev_u8(fc), B, ws, fb, out_bytes=nb, fp16=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u8(fb)[:int(nb.item())],
+                                  orc.encode_f16(gu.host_u16(f2), fc, B))
+    assert ws.error() == 0
+
+
 @pytest.mark.parametrize("B", BLOCKS)
 def test_encode_matches_oracle(gu, orc, B):
     ws = None
