@@ -39,10 +39,10 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "e336e12e7759804ac2c05112db45b1eb27ccd92959d190784b8be873fcb8c9e6"
+_SRC_SHA = "063dd7af5ceae09c4ed771090620a41a94c0bc8e92824e9a47146b608975f30e"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780066445),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873322232),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780109006),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873559883),
 }
 
 

@@ -33,7 +33,9 @@ constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 // front of it, half the bitmap on average.
 bool use_count_scan(uint64_t n, uint32_t l) {
   if (l == 0) return false;
-  const uint64_t groups = (enc_tiles(n, l) + 3) / 4;
+  const uint64_t tiles = enc_tiles(n, l);
+  const uint64_t per_group = l >= 9 ? 4 * uint64_t(exc_tiles_per_wave(tiles)) : 4;
+  const uint64_t groups = (tiles + per_group - 1) / per_group;
   return groups * bitmap_bytes(n, l) / 2 > kPrefixPassBytes;
 }
 
@@ -162,6 +164,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   a.hashed = hashed;
   a.f16 = f16;
   a.scan_prefix = use_count_scan(n_elems, l);
+  a.exc_tiles_per_wave = exc_tiles_per_wave(tiles);
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }

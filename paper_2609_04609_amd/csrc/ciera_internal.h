@@ -78,6 +78,18 @@ static_assert((kDecTile & (kDecTile - 1)) == 0 && kDecTile >= 4096,
 // lane) when B <= 512, and 8 blocks (8B values, several chunks) when B > 512,
 // so that every tile owns whole bitmap bytes.
 constexpr uint64_t kEncChunk = 4096;
+// B >= 512: re-reads of W' that one wave of the exception pass keeps in
+// flight, and the waves it aims for
+constexpr uint32_t kExcBatch = 4;
+constexpr uint64_t kExcRowWaves = 16384;
+// 16-byte bitmap words per thread that a workgroup counting the flagged
+// blocks in front of it loads at once (the encode's row-wise exception pass,
+// the decode without a prefix pass)
+constexpr uint32_t kGroupLoads = 2;
+inline uint32_t exc_tiles_per_wave(uint64_t tiles) {
+  const uint64_t t = (tiles + kExcRowWaves - 1) / kExcRowWaves;
+  return uint32_t(t ? t : 1);
+}
 inline uint64_t enc_tile_elems(uint32_t log2B) {
   return log2B <= 9 ? kEncChunk : (uint64_t(8) << log2B);
 }
@@ -102,6 +114,8 @@ struct EncArgs {
   // B >= 16: pass 1 writes per-tile counts and a scan turns them into the
   // exception pass's offsets (else each workgroup counts the bitmap)
   bool scan_prefix;
+  // B >= 512: tiles per wave of the row-wise exception pass
+  uint32_t exc_tiles_per_wave;
   bool f16;  // fp16 values (B >= 16)
   // block-hash detector (B >= 16) in place of exact compare with `cache`
   bool hashed;

@@ -709,9 +709,71 @@ __global__ __launch_bounds__(kScanThreads) void scan_counts_kernel(
   if (tid == 0) c[count] = carry;
 }
 
-// Pass 2. The exceptions of the tile's changed blocks (B >= 16) or changed
-// values (B = 1), at the tile's offset in the list; the last tile writes the
-// header. W' is read again only where the bitmap says so.
+// The exponents of one octet at exception index pos: bf16 bytes at pos, fp16
+// five bit-plane bytes at 5 (pos / 8).
+template <bool VEC, bool F16>
+__device__ __forceinline__ void put_exc_octet(uint8_t *exc_out, uint64_t pos,
+                                              const uint4 &wv,
+                                              uint32_t valid) {
+  uint2 e, t0, t1;
+  if (F16) {
+    split4_f16(wv.x, wv.y, e.x, t0.x, t1.x);
+    split4_f16(wv.z, wv.w, e.y, t0.y, t1.y);
+    uint8_t *g = exc_out + 5 * (pos >> 3);
+#pragma unroll
+    for (uint32_t q = 0; q < 5; ++q) g[q] = uint8_t(plane_byte(e.x, e.y, q));
+  } else {
+    split4(wv.x, wv.y, e.x, t0.x);
+    split4(wv.z, wv.w, e.y, t0.y);
+    if (VEC && valid == 8)
+      st_nt8(exc_out + pos, e);
+    else
+      store_b8<VEC>(exc_out + pos, e, valid);
+  }
+}
+
+// The totals, known to the wave that holds the last tile: the header, the
+// exception section's zero padding and the encoded size. total_changed
+// counts changed blocks (B >= 16) or changed values (B = 1).
+template <bool ELEMS, bool F16>
+__device__ void exc_finish(const EncArgs &a, uint64_t total_changed,
+                           uint32_t lane) {
+  const uint64_t n = a.n;
+  const uint32_t log2B = a.log2B;
+  const uint32_t B = 1u << log2B;
+  const uint64_t S_sm = sm_bytes(n, F16);
+  const uint64_t n16 = pad16(S_sm);
+  const uint64_t bm = bitmap_bytes(n, log2B);
+  const uint64_t bm16 = pad16(bm);
+  const uint8_t *const bmp = a.out + kHeaderBytes + n16;
+  uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
+  uint64_t E = total_changed;
+  if (!ELEMS) {
+    E = total_changed << log2B;
+    const uint64_t nblk = blocks_of(n, log2B);
+    if (nblk) {
+      const uint64_t lb = nblk - 1;
+      const bool last_changed = (bmp[lb >> 3] >> (lb & 7u)) & 1u;
+      const uint64_t len_last = n - (lb << log2B);
+      if (last_changed) E -= (uint64_t(B) - len_last);
+    }
+  }
+  if (E > n) {  // only with a count array that was written by someone else
+    if (lane == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+    E = n;
+  }
+  const uint64_t S_exc = exc_bytes(E, F16);
+  const uint64_t P = S_sm + bm + S_exc;
+  const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(S_exc);
+  put_header(a.out, kModeCompressed, B, n, total_changed, E, P, total, lane,
+             F16 ? kDtypeFp16 : kDtypeBf16);
+  if (lane == 16 && a.out_bytes) *a.out_bytes = total;
+  for (uint64_t i = S_exc + lane; i < pad16(S_exc); i += 64) exc_out[i] = 0;
+}
+
+// Pass 2 for B = 1 and B = 16 ... 256. The exceptions of the tile's changed
+// blocks or values, at the tile's offset in the list; the last tile writes
+// the header. W' is read again only where the bitmap says so.
 //
 // Offsets at B >= 16: the bitmap is 1/(8B) of the shard, so a workgroup
 // counts the flagged blocks in front of its first tile straight from it (an
@@ -736,25 +798,6 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   const uint64_t bm16 = pad16(bm);
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
   uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
-  // the exponents of one octet of the list, at exception index pos: bf16
-  // bytes at pos, fp16 5 bit-plane bytes at 5 (pos / 8)
-  auto put_exc = [&](uint64_t pos, const uint4 &wv, uint32_t valid) {
-    uint2 e, t0, t1;
-    if (F16) {
-      split4_f16(wv.x, wv.y, e.x, t0.x, t1.x);
-      split4_f16(wv.z, wv.w, e.y, t0.y, t1.y);
-      uint8_t *g = exc_out + 5 * (pos >> 3);
-#pragma unroll
-      for (uint32_t q = 0; q < 5; ++q) g[q] = uint8_t(plane_byte(e.x, e.y, q));
-    } else {
-      split4(wv.x, wv.y, e.x, t0.x);
-      split4(wv.z, wv.w, e.y, t0.y);
-      if (VEC && valid == 8)
-        st_nt8(exc_out + pos, e);
-      else
-        store_b8<VEC>(exc_out + pos, e, valid);
-    }
-  };
   // bitmap bytes per tile (B >= 16)
   const uint64_t per_tile = log2B <= 9 ? (kEncChunk >> log2B) >> 3 : 1u;
 
@@ -818,7 +861,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         mm &= mm - 1u;
       }
     }
-  } else if (log2B <= 9) {
+  } else {
     // (1) the tile's own flags, as one to four 64-bit words, never reading
     // past the zero-padded bitmap (the exception section behind it is being
     // written by other tiles)
@@ -876,7 +919,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
         if (uint32_t(k) < (bl >> 6)) rank += uint32_t(__popcll(fw[k]));
       const uint64_t pos =
           (uint64_t(prefix + rank) << log2B) | ((o << 3) & (B - 1u));
-      if (pos + valid <= n) put_exc(pos, w, valid);
+      if (pos + valid <= n) put_exc_octet<VEC, F16>(exc_out, pos, w, valid);
     };
 #pragma unroll
     for (int u = 0; u < 4; ++u)
@@ -890,37 +933,9 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
 #pragma unroll
     for (int u = 4; u < 8; ++u)
       if (ch[u]) put_octet(u, wv[u & 3]);
-  } else {
-    // 8 blocks of B > 512 values; the wave copies each changed block's
-    // exponents 512 values at a time
-    if (a.scan_prefix) {
-      if (!live) return;
-      prefix = a.counts[tile];
-    } else {
-      const uint32_t sib = wave_popc(uint64_t(blockIdx.x) * 4u, tile);
-      prefix = group_prefix(uint64_t(blockIdx.x) * 4u);
-      if (!live) return;
-      prefix += sib;
-    }
-    const uint32_t fbyte = tile < bm ? bmp[tile] : 0u;
-    uint32_t rank = 0;
-    for (uint32_t k = 0; k < 8; ++k) {
-      if (!((fbyte >> k) & 1u)) continue;
-      const uint64_t bbase = tbase + (uint64_t(k) << log2B);
-      const uint64_t dst = uint64_t(prefix + rank) << log2B;
-      for (uint32_t c = 0; c < B; c += 512) {
-        const uint64_t elem = bbase + c + uint64_t(lane) * 8;
-        const uint32_t valid = octet_valid(elem, n);
-        if (!valid) continue;
-        const uint4 wv = load_w8<VEC>(a.w + elem, valid);
-        const uint64_t pos = dst + c + uint64_t(lane) * 8;
-        if (pos + valid <= n) put_exc(pos, wv, valid);
-      }
-      ++rank;
-    }
   }
 
-  // ---- the last tile knows the totals: header, exception padding, size ----
+  // ---- the last tile knows the totals ----
   const uint32_t last = a.num_tiles - 1;
   if (tile == last) {
     const uint64_t total_changed =
@@ -928,28 +943,141 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
               : uint64_t(prefix) +
                     wave_popc(uint64_t(last) * per_tile,
                               uint64_t(last) * per_tile + per_tile);
-    uint64_t E = total_changed;
-    if (!ELEMS) {
-      E = total_changed << log2B;
-      const uint64_t nblk = blocks_of(n, log2B);
-      if (nblk) {
-        const uint64_t lb = nblk - 1;
-        const bool last_changed = (bmp[lb >> 3] >> (lb & 7u)) & 1u;
-        const uint64_t len_last = n - (lb << log2B);
-        if (last_changed) E -= (uint64_t(B) - len_last);
+    exc_finish<ELEMS, F16>(a, total_changed, lane);
+  }
+}
+
+// Pass 2 for B >= 512. A row of 512 values lies inside one block, so it is
+// changed or unchanged as a whole, and the exceptions of the changed rows
+// follow one another in row order: the k-th changed row's exponents start at
+// 512 k in the list. A tile (8 blocks) is one bitmap byte. Each wave takes a
+// run of a.exc_tiles_per_wave tiles and copies its changed rows kExcBatch at
+// a time, so that that many re-reads of W' are in flight per wave; the first
+// batch is issued before the offset of the run (the changed blocks in front
+// of it) is counted, and the two overlap.
+template <bool VEC, bool F16>
+__global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
+  constexpr uint32_t D = kExcBatch;
+  __shared__ uint32_t s_red[4];
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t n = a.n;
+  const uint32_t rpb_log2 = a.log2B - 9;  // rows per block
+  const uint64_t S_sm = sm_bytes(n, F16);
+  const uint64_t n16 = pad16(S_sm);
+  const uint64_t bm = bitmap_bytes(n, a.log2B);
+  const uint8_t *const bmp = a.out + kHeaderBytes + n16;
+  uint8_t *const exc_out = a.out + kHeaderBytes + n16 + pad16(bm);
+  const uint64_t nt = a.num_tiles, tpw = a.exc_tiles_per_wave;
+  const uint64_t g0 = min(uint64_t(blockIdx.x) * 4u * tpw, nt);
+  const uint64_t t0 = min(g0 + wave * tpw, nt);
+  const uint64_t t1 = min(t0 + tpw, nt);
+  const uint64_t rows = (n + 511) >> 9;
+  const uint64_t r0 = min(t0 << (rpb_log2 + 3), rows);
+  const uint64_t r1 = min(t1 << (rpb_log2 + 3), rows);
+
+  // changed rows among [c, c + 64) of the run, as a wave-uniform mask
+  auto chunk_mask = [&](uint64_t c) -> uint64_t {
+    const uint64_t row = c + lane;
+    bool f = false;
+    if (row < r1) {
+      const uint64_t b = row >> rpb_log2;
+      f = (bmp[b >> 3] >> (b & 7u)) & 1u;
+    }
+    return __ballot(f);
+  };
+  uint64_t c = r0, m = r0 < r1 ? chunk_mask(r0) : 0ull;
+  uint32_t rr[D], cnt = 0;
+  uint4 wv[D];
+  // the next batch of changed rows of chunk c: positions and W' loads
+  auto take_batch = [&]() {
+    cnt = 0;
+#pragma unroll
+    for (uint32_t d = 0; d < D; ++d) {
+      if (m) {
+        rr[d] = uint32_t(__builtin_ctzll(m));
+        m &= m - 1ull;
+        cnt = d + 1;
       }
     }
-    if (E > n) {  // only with a count array that was written by someone else
-      if (lane == 0) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
-      E = n;
+#pragma unroll
+    for (uint32_t d = 0; d < D; ++d) {
+      if (d < cnt) {
+        const uint64_t elem = ((c + rr[d]) << 9) + uint64_t(lane) * 8;
+        const uint32_t valid = octet_valid(elem, n);
+        if (valid) wv[d] = reread_w8<VEC>(a.w + elem, valid);
+      }
     }
-    const uint64_t S_exc = exc_bytes(E, F16);
-    const uint64_t P = S_sm + bm + S_exc;
-    const uint64_t total = kHeaderBytes + n16 + bm16 + pad16(S_exc);
-    put_header(a.out, kModeCompressed, B, n, total_changed, E, P, total, lane,
-               F16 ? kDtypeFp16 : kDtypeBf16);
-    if (lane == 16 && a.out_bytes) *a.out_bytes = total;
-    for (uint64_t i = S_exc + lane; i < pad16(S_exc); i += 64) exc_out[i] = 0;
+  };
+  take_batch();
+
+  // the run's offset in changed blocks: the bitmap bytes in front of it.
+  // Every load is issued before the first count (clamped addresses, no
+  // branches), so the whole count costs one round trip per kGroupLoads
+  // words of 16 bytes per thread.
+  uint32_t prefix;
+  if (a.scan_prefix) {
+    prefix = a.counts[t0];
+  } else {
+    const uint64_t gb = min(g0, bm);  // the workgroup's bytes in front
+    const uint64_t sb = min(t0, bm);  // + the sibling runs in front
+    const uint64_t full16 = gb >> 4;
+    uint32_t cg = 0, cs = 0;
+    if (bm) {
+      const uint64_t ti = (full16 << 4) + threadIdx.x;  // < 16 tail bytes
+      const uint64_t si = gb + lane;
+      const uint32_t tb = bmp[min(ti, bm - 1)];
+      const uint32_t sv = bmp[min(si, bm - 1)];
+      const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
+      for (uint64_t i0 = 0; i0 < full16; i0 += kGroupLoads * kThreads) {
+        uint4 v[kGroupLoads];
+#pragma unroll
+        for (uint32_t j = 0; j < kGroupLoads; ++j) {
+          const uint64_t i = i0 + j * kThreads + threadIdx.x;
+          v[j] = b4[i < full16 ? i : full16 - 1];
+        }
+#pragma unroll
+        for (uint32_t j = 0; j < kGroupLoads; ++j) {
+          const uint64_t i = i0 + j * kThreads + threadIdx.x;
+          const uint32_t c = __popc(v[j].x) + __popc(v[j].y) +
+                             __popc(v[j].z) + __popc(v[j].w);
+          cg += i < full16 ? c : 0u;
+        }
+      }
+      cg += ti < gb ? uint32_t(__popc(tb)) : 0u;
+      cs = si < sb ? uint32_t(__popc(sv)) : 0u;
+      for (uint64_t i = si + 64; i < sb; i += 64)  // runs of > 21 tiles
+        cs += __popc(uint32_t(bmp[i]));
+    }
+    prefix = block_sum(cg, s_red) + wave_sum(cs);
+  }
+
+  uint64_t out_row = uint64_t(prefix) << rpb_log2;
+  for (;;) {
+#pragma unroll
+    for (uint32_t d = 0; d < D; ++d) {
+      if (d < cnt) {
+        const uint64_t elem = ((c + rr[d]) << 9) + uint64_t(lane) * 8;
+        const uint32_t valid = octet_valid(elem, n);
+        const uint64_t pos = ((out_row + d) << 9) + uint64_t(lane) * 8;
+        if (valid && pos + valid <= n)
+          put_exc_octet<VEC, F16>(exc_out, pos, wv[d], valid);
+      }
+    }
+    out_row += cnt;
+    while (!m) {
+      c += 64;
+      if (c >= r1) break;
+      m = chunk_mask(c);
+    }
+    if (c >= r1) break;
+    take_batch();
+  }
+
+  if (t0 < nt && t1 == nt) {
+    uint32_t own = 0;
+    for (uint64_t i = t0 + lane; i < min(t1, bm); i += 64)
+      own += __popc(uint32_t(bmp[i]));
+    exc_finish<false, F16>(a, uint64_t(prefix) + wave_sum(own), lane);
   }
 }
 
@@ -1116,6 +1244,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   constexpr uint32_t T = kThreads * 8 * OCT;
   // tile bitmap words (32 blocks each) covering at most T/16 blocks + 1 word
   constexpr uint32_t kBitWords = T / 16 / 32 + 2;
+  static_assert(kBitWords <= kThreads, "one bitmap word per thread");
   __shared__ uint32_t s_bits[kBitWords];
   __shared__ uint32_t s_pre[kBitWords];
   __shared__ uint32_t s_red[4];
@@ -1250,30 +1379,45 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
   const uint64_t fb = base >> log2B;             // first block of the tile
   const uint64_t lbk = (end - 1) >> log2B;       // last block of the tile
   const uint64_t w0 = fb >> 5;
-  const uint32_t nw = uint32_t((lbk >> 5) - w0 + 1);
-  for (uint32_t i = tid; i < nw; i += kThreads) {
-    uint32_t word = bmp32[w0 + i];
-    if (i == 0) word &= ~((1u << (fb & 31u)) - 1u);
-    s_bits[i] = word;
-  }
+  const uint32_t nw = uint32_t((lbk >> 5) - w0 + 1);  // <= 33 < kThreads
+  // one word per thread (clamped address, no branch), stored below, so that
+  // the count's loads are issued before anything waits for it
+  uint32_t word = bmp32[w0 + (tid < nw ? tid : nw - 1u)];
+  if (tid == 0) word &= ~((1u << (fb & 31u)) - 1u);
   // flagged blocks in front of the tile: from tile_prefix_kernel, or
-  // counted here straight from the bitmap
+  // counted here straight from the bitmap, every load issued before the
+  // first count
   uint32_t prefix;
   if (a.prefix_pass) {
     prefix = a.tile_excl[uint64_t(j) * dec_count_stride(ntiles) + tix];
+    if (tid < nw) s_bits[tid] = word;
     __syncthreads();  // s_bits, and the fp16 planes in s_hi
   } else {
-    uint32_t cnt = 0;
     const uint64_t full4 = w0 >> 2;  // whole 16-byte chunks before word w0
-    const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
-    for (uint64_t i = tid; i < full4; i += kThreads) {
-      const uint4 c = b4[i];
-      cnt += __popc(c.x) + __popc(c.y) + __popc(c.z) + __popc(c.w);
-    }
     const uint64_t wr = (full4 << 2) + tid;  // leftover words before w0
-    if (tid < 4 && wr < w0) cnt += __popc(bmp32[wr]);
+    const uint32_t wl = bmp32[wr < w0 ? wr : 0u];
+    const uint32_t wf = bmp32[w0];
+    const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
+    uint32_t cnt = 0;
+    for (uint64_t i0 = 0; i0 < full4; i0 += kGroupLoads * kThreads) {
+      uint4 v[kGroupLoads];
+#pragma unroll
+      for (uint32_t k = 0; k < kGroupLoads; ++k) {
+        const uint64_t i = i0 + k * kThreads + tid;
+        v[k] = b4[i < full4 ? i : full4 - 1];
+      }
+#pragma unroll
+      for (uint32_t k = 0; k < kGroupLoads; ++k) {
+        const uint64_t i = i0 + k * kThreads + tid;
+        const uint32_t c = __popc(v[k].x) + __popc(v[k].y) + __popc(v[k].z) +
+                           __popc(v[k].w);
+        cnt += i < full4 ? c : 0u;
+      }
+    }
+    if (tid < nw) s_bits[tid] = word;
+    cnt += (tid < 4 && wr < w0) ? uint32_t(__popc(wl)) : 0u;
     if (tid == 4 && (fb & 31u))
-      cnt += __popc(bmp32[w0] & ((1u << (fb & 31u)) - 1u));
+      cnt += __popc(wf & ((1u << (fb & 31u)) - 1u));
     prefix = block_sum(cnt, s_red);  // also orders s_bits and s_hi
   }
   if (tid == 0) {
@@ -1588,6 +1732,25 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
       hipLaunchKernelGGL((encode_exc_kernel<true, true>), grid, block, 0, s, a);
     else
       hipLaunchKernelGGL((encode_exc_kernel<false, true>), grid, block, 0, s, a);
+  } else if (a.log2B >= 9) {
+    const uint64_t waves = (a.num_tiles + a.exc_tiles_per_wave - 1) /
+                           a.exc_tiles_per_wave;
+    const dim3 rgrid(uint32_t((waves + 3) / 4));
+    if (a.f16) {
+      if (vec)
+        hipLaunchKernelGGL((encode_exc_rows_kernel<true, true>), rgrid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((encode_exc_rows_kernel<false, true>), rgrid, block,
+                           0, s, a);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((encode_exc_rows_kernel<true, false>), rgrid, block,
+                           0, s, a);
+      else
+        hipLaunchKernelGGL((encode_exc_rows_kernel<false, false>), rgrid,
+                           block, 0, s, a);
+    }
   } else if (a.f16) {
     if (vec)
       hipLaunchKernelGGL((encode_exc_kernel<true, false, true>), grid, block,
