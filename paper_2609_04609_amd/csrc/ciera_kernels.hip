@@ -709,6 +709,36 @@ __global__ __launch_bounds__(kScanThreads) void scan_counts_kernel(
   if (tid == 0) c[count] = carry;
 }
 
+// This thread's share of the flagged blocks in bitmap bytes [0, nbytes):
+// every load is issued before the first add (clamped addresses, no
+// branches), so a workgroup's count costs one round trip per kGroupLoads
+// 16-byte words per thread. Sum it over the workgroup with block_sum.
+__device__ __forceinline__ uint32_t popc_bytes_part(const uint8_t *bmp,
+                                                    uint64_t nbytes) {
+  if (!nbytes) return 0u;
+  const uint64_t full16 = nbytes >> 4;
+  const uint64_t ti = (full16 << 4) + threadIdx.x;  // < 16 tail bytes
+  const uint32_t tb = bmp[ti < nbytes ? ti : nbytes - 1];
+  const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
+  uint32_t c = 0;
+  for (uint64_t i0 = 0; i0 < full16; i0 += kGroupLoads * kThreads) {
+    uint4 v[kGroupLoads];
+#pragma unroll
+    for (uint32_t j = 0; j < kGroupLoads; ++j) {
+      const uint64_t i = i0 + j * kThreads + threadIdx.x;
+      v[j] = b4[i < full16 ? i : full16 - 1];
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < kGroupLoads; ++j) {
+      const uint64_t i = i0 + j * kThreads + threadIdx.x;
+      const uint32_t w = __popc(v[j].x) + __popc(v[j].y) + __popc(v[j].z) +
+                         __popc(v[j].w);
+      c += i < full16 ? w : 0u;
+    }
+  }
+  return c + (ti < nbytes ? uint32_t(__popc(tb)) : 0u);
+}
+
 // The exponents of one octet at exception index pos: bf16 bytes at pos, fp16
 // five bit-plane bytes at 5 (pos / 8).
 template <bool VEC, bool F16>
@@ -805,23 +835,16 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   // over the whole wave
   auto wave_popc = [&](uint64_t lo, uint64_t hi) -> uint32_t {
     if (hi > bm) hi = bm;
-    uint32_t c = 0;
-    for (uint64_t i = lo + lane; i < hi; i += 64) c += __popc(uint32_t(bmp[i]));
+    if (lo >= hi) return 0u;
+    const uint64_t i = lo + lane;
+    const uint32_t b = bmp[i < hi ? i : hi - 1];  // no branch around the load
+    uint32_t c = i < hi ? uint32_t(__popc(b)) : 0u;
+    for (uint64_t k = i + 64; k < hi; k += 64) c += __popc(uint32_t(bmp[k]));
     return wave_sum(c);
   };
   // flagged blocks in front of this workgroup's first tile (all threads)
   auto group_prefix = [&](uint64_t before) -> uint32_t {
-    if (before > bm) before = bm;
-    uint32_t cnt = 0;
-    const uint64_t full16 = before >> 4;
-    const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
-    for (uint64_t i = threadIdx.x; i < full16; i += kThreads) {
-      const uint4 v = b4[i];
-      cnt += __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
-    }
-    for (uint64_t i = (full16 << 4) + threadIdx.x; i < before; i += kThreads)
-      cnt += __popc(uint32_t(bmp[i]));
-    return block_sum(cnt, s_red);
+    return block_sum(popc_bytes_part(bmp, before < bm ? before : bm), s_red);
   };
 
   uint32_t prefix = 0;
@@ -1010,44 +1033,19 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   };
   take_batch();
 
-  // the run's offset in changed blocks: the bitmap bytes in front of it.
-  // Every load is issued before the first count (clamped addresses, no
-  // branches), so the whole count costs one round trip per kGroupLoads
-  // words of 16 bytes per thread.
+  // the run's offset in changed blocks: the bitmap bytes in front of it
   uint32_t prefix;
   if (a.scan_prefix) {
     prefix = a.counts[t0];
   } else {
     const uint64_t gb = min(g0, bm);  // the workgroup's bytes in front
     const uint64_t sb = min(t0, bm);  // + the sibling runs in front
-    const uint64_t full16 = gb >> 4;
-    uint32_t cg = 0, cs = 0;
-    if (bm) {
-      const uint64_t ti = (full16 << 4) + threadIdx.x;  // < 16 tail bytes
-      const uint64_t si = gb + lane;
-      const uint32_t tb = bmp[min(ti, bm - 1)];
-      const uint32_t sv = bmp[min(si, bm - 1)];
-      const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
-      for (uint64_t i0 = 0; i0 < full16; i0 += kGroupLoads * kThreads) {
-        uint4 v[kGroupLoads];
-#pragma unroll
-        for (uint32_t j = 0; j < kGroupLoads; ++j) {
-          const uint64_t i = i0 + j * kThreads + threadIdx.x;
-          v[j] = b4[i < full16 ? i : full16 - 1];
-        }
-#pragma unroll
-        for (uint32_t j = 0; j < kGroupLoads; ++j) {
-          const uint64_t i = i0 + j * kThreads + threadIdx.x;
-          const uint32_t c = __popc(v[j].x) + __popc(v[j].y) +
-                             __popc(v[j].z) + __popc(v[j].w);
-          cg += i < full16 ? c : 0u;
-        }
-      }
-      cg += ti < gb ? uint32_t(__popc(tb)) : 0u;
-      cs = si < sb ? uint32_t(__popc(sv)) : 0u;
-      for (uint64_t i = si + 64; i < sb; i += 64)  // runs of > 21 tiles
-        cs += __popc(uint32_t(bmp[i]));
-    }
+    const uint64_t si = gb + lane;
+    const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
+    const uint32_t cg = popc_bytes_part(bmp, gb);
+    uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
+    for (uint64_t i = si + 64; i < sb; i += 64)  // runs of > 21 tiles
+      cs += __popc(uint32_t(bmp[i]));
     prefix = block_sum(cg, s_red) + wave_sum(cs);
   }
 
