@@ -25,6 +25,56 @@ def gu():
     return gpu_util
 
 
+def test_encode_rows_with_count_scan(gu, orc):
+    """A 310,000,005-value shard at B = 512: the row-wise exception pass gives
+    each wave a run of 5 tiles, and its workgroups' counting would re-read
+    about 143 MB of bitmap, so the offsets come from pass 1's per-tile counts
+    and the scan. bf16 and fp16 match the oracle byte for byte; a small call
+    first must not leak its counts into the big one."""
+    from paper_2609_04609_amd import ciera, synth
+    n, B = 310_000_005, 512
+    ws = ciera.Workspace(n, 1, B)
+    w, w2 = gu.pair(n, 3131, c=0.0002)
+    wh, w2h = gu.host_u16(w), gu.host_u16(w2)
+    cache_h = orc.split(wh)[0]
+    out, total, _ = gu.gpu_encode(w2[:70_000], gu.dev_u8(cache_h[:70_000]), B,
+                                  ws)
+    np.testing.assert_array_equal(gu.host_u8(out)[:total],
+                                  orc.encode(w2h[:70_000], cache_h[:70_000], B))
+    expect = orc.encode(w2h, cache_h, B)
+    out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
+    assert total == expect.size
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    del w, w2, wh, w2h, cache_h, expect, out
+    torch.cuda.empty_cache()
+    f = synth.normal_f16_bits(n, 0.02, 3232, "cuda")
+    f2 = synth.forced_bernoulli_f16_bits(f, 0.0002, 3233)
+    fc = orc.split_f16(gu.host_u16(f))[0]
+    fb = torch.empty(int(ciera.ciera_encoded_bound(n, B, ciera.FP16)),
+                     dtype=torch.uint8, device="cuda")
+    nb = torch.zeros(1, dtype=torch.int64, device="cuda")
+    ciera.encode_t(f2, gu.dev_u8(fc), B, ws, fb, out_bytes=nb, fp16=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gu.host_u8(fb)[:int(nb.item())],
+                                  orc.encode_f16(gu.host_u16(f2), fc, B))
+    assert ws.error() == 0
+
+
+def test_encode_rows_several_chunks(gu, orc):
+    """A 600,000,003-value shard at B = 4096: each wave of the row-wise
+    exception pass takes two tiles, 128 rows of 512 values, so it walks its
+    run in two chunks of 64 rows. Matches the oracle byte for byte."""
+    n, B = 600_000_003, 4096
+    w, w2 = gu.pair(n, 3434, c=0.00002)
+    cache_h = orc.split(gu.host_u16(w))[0]
+    del w
+    out, total, ws = gu.gpu_encode(w2, gu.dev_u8(cache_h), B)
+    expect = orc.encode(gu.host_u16(w2), cache_h, B)
+    assert total == expect.size
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    assert ws.error() == 0
+
+
 def test_encode_with_count_scan(gu, orc):
     """A 25,165,832-value shard at B = 16: counting the bitmap in front of
     every exception-pass workgroup would re-read about 151 MB, so pass 1
