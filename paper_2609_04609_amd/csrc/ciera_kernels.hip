@@ -828,8 +828,8 @@ __global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
   const uint64_t bm16 = pad16(bm);
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
   uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
-  // bitmap bytes per tile (B >= 16)
-  const uint64_t per_tile = log2B <= 9 ? (kEncChunk >> log2B) >> 3 : 1u;
+  // bitmap bytes per tile (B = 16 ... 256, the B >= 16 paths below)
+  const uint64_t per_tile = (kEncChunk >> log2B) >> 3;
 
   // flagged blocks in bitmap bytes [lo, hi) (clipped to the bitmap), summed
   // over the whole wave
