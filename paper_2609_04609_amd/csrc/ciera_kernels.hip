@@ -1731,23 +1731,25 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     else
       hipLaunchKernelGGL((encode_exc_kernel<false, true>), grid, block, 0, s, a);
   } else if (a.log2B >= 9) {
-    const uint64_t waves = (a.num_tiles + a.exc_tiles_per_wave - 1) /
-                           a.exc_tiles_per_wave;
+    EncArgs r = a;
+    if (r.exc_tiles_per_wave == 0) r.exc_tiles_per_wave = 1;
+    const uint64_t waves = (uint64_t(r.num_tiles) + r.exc_tiles_per_wave - 1) /
+                           r.exc_tiles_per_wave;
     const dim3 rgrid(uint32_t((waves + 3) / 4));
-    if (a.f16) {
+    if (r.f16) {
       if (vec)
         hipLaunchKernelGGL((encode_exc_rows_kernel<true, true>), rgrid, block,
-                           0, s, a);
+                           0, s, r);
       else
         hipLaunchKernelGGL((encode_exc_rows_kernel<false, true>), rgrid, block,
-                           0, s, a);
+                           0, s, r);
     } else {
       if (vec)
         hipLaunchKernelGGL((encode_exc_rows_kernel<true, false>), rgrid, block,
-                           0, s, a);
+                           0, s, r);
       else
         hipLaunchKernelGGL((encode_exc_rows_kernel<false, false>), rgrid,
-                           block, 0, s, a);
+                           block, 0, s, r);
     }
   } else if (a.f16) {
     if (vec)
