@@ -39,10 +39,10 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "e1661a707528efd62e3bc34f70e92de1a17f020860942319ada0dd7afa5c386c"
+_SRC_SHA = "298ca6b6ad6dbadecd18c4a760eb30eb71a15e85ed5ad71a1cbf99cfe33ec658"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780094670),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873446093),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780097870),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873596746),
 }
 
 
