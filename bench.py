@@ -43,6 +43,10 @@ _SRC_SHA = "298ca6b6ad6dbadecd18c4a760eb30eb71a15e85ed5ad71a1cbf99cfe33ec658"
 MEASURED_TRAFFIC = {
     ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780097870),
     ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873596746),
+    # measured apart from the OLMoE figures, so it keeps its own source hash
+    ("dsv3_layer", 512, "bf16"): (
+        "298ca6b6ad6dbadecd18c4a760eb30eb71a15e85ed5ad71a1cbf99cfe33ec658",
+        48949533219),
 }
 
 
