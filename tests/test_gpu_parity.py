@@ -25,6 +25,53 @@ def gu():
     return gpu_util
 
 
+@pytest.mark.parametrize("B", [512, 1024, 2048, 4096])
+def test_encode_rows_random_sizes(gu, orc, B):
+    """The row-wise exception pass (B >= 512) on seeded random sizes and
+    change rates, bf16 and fp16, against the oracle byte for byte."""
+    from paper_2609_04609_amd import ciera, synth
+    rng = np.random.default_rng(B)
+    sizes = [int(x) for x in rng.integers(1, 2_000_000, 6)]
+    ws = ciera.Workspace(max(sizes), 1, B)
+    for i, n in enumerate(sizes):
+        c = float(rng.choice([0.0, 0.0005, 0.003, 0.05]))
+        w, w2 = gu.pair(n, 9000 + B + i, c=c)
+        cache_h = orc.split(gu.host_u16(w))[0]
+        out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
+        expect = orc.encode(gu.host_u16(w2), cache_h, B)
+        np.testing.assert_array_equal(gu.host_u8(out)[:total], expect,
+                                      err_msg=f"n={n} c={c}")
+        f = synth.normal_f16_bits(n, 0.02, 9100 + B + i, "cuda")
+        f2 = synth.forced_bernoulli_f16_bits(f, c, 9200 + B + i)
+        fc = orc.split_f16(gu.host_u16(f))[0]
+        fb = torch.empty(int(ciera.ciera_encoded_bound(n, B, ciera.FP16)),
+                         dtype=torch.uint8, device="cuda")
+        nb = torch.zeros(1, dtype=torch.int64, device="cuda")
+        ciera.encode_t(f2, gu.dev_u8(fc), B, ws, fb, out_bytes=nb, fp16=True)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(
+            gu.host_u8(fb)[:int(nb.item())],
+            orc.encode_f16(gu.host_u16(f2), fc, B), err_msg=f"fp16 n={n}")
+    assert ws.error() == 0
+
+
+@pytest.mark.parametrize("n", [16384 * 4096, 16384 * 4096 + 1,
+                               16384 * 4096 + 4097])
+def test_encode_rows_run_boundary(gu, orc, n):
+    """Shards around the size where the row-wise exception pass goes from
+    one tile per wave to two (16,384 tiles of 4096 values at B = 512): the
+    last run may hold a single, partial tile."""
+    B = 512
+    w, w2 = gu.pair(n, 9300 + n % 7, c=0.0005)
+    cache_h = orc.split(gu.host_u16(w))[0]
+    del w
+    out, total, ws = gu.gpu_encode(w2, gu.dev_u8(cache_h), B)
+    expect = orc.encode(gu.host_u16(w2), cache_h, B)
+    assert total == expect.size
+    np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    assert ws.error() == 0
+
+
 def test_encode_rows_with_count_scan(gu, orc):
     """A 310,000,005-value shard at B = 512: the row-wise exception pass gives
     each wave a run of 5 tiles, and its workgroups' counting would re-read
