@@ -39,14 +39,14 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "298ca6b6ad6dbadecd18c4a760eb30eb71a15e85ed5ad71a1cbf99cfe33ec658"
+_SRC_SHA = "0cb9ec2e61d6decf7993bcdb2d7453f284cc2d298fb601bda9fb771016b571ff"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780097870),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873596746),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780150349),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873466317),
     # measured apart from the OLMoE figures, so it keeps its own source hash
     ("dsv3_layer", 512, "bf16"): (
-        "298ca6b6ad6dbadecd18c4a760eb30eb71a15e85ed5ad71a1cbf99cfe33ec658",
-        48949533219),
+        "0cb9ec2e61d6decf7993bcdb2d7453f284cc2d298fb601bda9fb771016b571ff",
+        48950115670),
 }
 
 

@@ -34,7 +34,7 @@ constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 bool use_count_scan(uint64_t n, uint32_t l) {
   if (l == 0) return false;
   const uint64_t tiles = enc_tiles(n, l);
-  const uint64_t per_group = l >= 9 ? 4 * uint64_t(exc_tiles_per_wave(tiles)) : 4;
+  const uint64_t per_group = 4 * uint64_t(exc_tiles_per_wave(tiles));
   const uint64_t groups = (tiles + per_group - 1) / per_group;
   return groups * bitmap_bytes(n, l) / 2 > kPrefixPassBytes;
 }

@@ -10,12 +10,16 @@
 //   encode   (1) encode_pass_kernel: SplitExpMant, change detection, the
 //                sign+mantissa plane, the bitmap and a changed-block count
 //                per tile, streaming at copy speed;
-//            (2) encode_exc_kernel: the exponents of the changed blocks, in
-//                block order, read back from W' for those blocks only; the
-//                header. A workgroup finds its first exception by counting
-//                the bitmap bits in front of it (the bitmap is 1/(8B) of the
-//                shard and stays in L2). At B = 1 a scan_counts_kernel over
-//                the per-tile counts stands in for that count.
+//            (2) the exponents of the changed blocks, in block order, read
+//                back from W' for those blocks only, and the header:
+//                encode_exc_blocks_kernel (B = 16 ... 256, lanes over the
+//                changed blocks), encode_exc_rows_kernel (B >= 512, over the
+//                changed 512-value rows), encode_exc_elems_kernel (B = 1).
+//                A workgroup finds its first exception by counting the
+//                bitmap bits in front of it (the bitmap is 1/(8B) of the
+//                shard and stays in L2); at B = 1, and where that count
+//                would re-read too much, a scan_counts_kernel over pass 1's
+//                per-tile counts stands in for it.
 //            No workgroup ever waits on another: compacting the exception
 //            list costs one re-read of the changed blocks (2 bytes per
 //            changed value) instead of a cross-workgroup scan whose waits
@@ -801,173 +805,57 @@ __device__ void exc_finish(const EncArgs &a, uint64_t total_changed,
   for (uint64_t i = S_exc + lane; i < pad16(S_exc); i += 64) exc_out[i] = 0;
 }
 
-// Pass 2 for B = 1 and B = 16 ... 256. The exceptions of the tile's changed
-// blocks or values, at the tile's offset in the list; the last tile writes
+// Pass 2 for B = 1: the tile's changed values, at the tile's offset in the
+// list (from the scanned per-tile counts of pass 1); the last tile writes
 // the header. W' is read again only where the bitmap says so.
-//
-// Offsets at B >= 16: the bitmap is 1/(8B) of the shard, so a workgroup
-// counts the flagged blocks in front of its first tile straight from it (an
-// L2 read) and each wave adds the flags of the sibling tiles before it. The
-// re-read of W' depends only on the tile's own flags, so it is issued before
-// that count and the two overlap. At B = 1 the offsets come from the scanned
-// per-tile counts.
-template <bool VEC, bool ELEMS, bool F16 = false>
-__global__ __launch_bounds__(kThreads) void encode_exc_kernel(EncArgs a) {
-  __shared__ uint32_t s_red[4];
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
+    EncArgs a) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t tile = blockIdx.x * 4u + wave;
-  const bool live = tile < a.num_tiles;
+  if (tile >= a.num_tiles) return;
   const uint64_t n = a.n;
-  const uint32_t log2B = a.log2B;
-  const uint32_t B = 1u << log2B;
-  const uint64_t T = a.tile_elems;
-  const uint64_t tbase = uint64_t(tile) * T;
-  const uint64_t S_sm = sm_bytes(n, F16);
-  const uint64_t n16 = pad16(S_sm);
-  const uint64_t bm = bitmap_bytes(n, log2B);
-  const uint64_t bm16 = pad16(bm);
+  const uint64_t tbase = uint64_t(tile) * a.tile_elems;
+  const uint64_t n16 = pad16(sm_bytes(n, false));
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
-  uint8_t *const exc_out = a.out + kHeaderBytes + n16 + bm16;
-  // bitmap bytes per tile (B = 16 ... 256, the B >= 16 paths below)
-  const uint64_t per_tile = (kEncChunk >> log2B) >> 3;
-
-  // flagged blocks in bitmap bytes [lo, hi) (clipped to the bitmap), summed
-  // over the whole wave
-  auto wave_popc = [&](uint64_t lo, uint64_t hi) -> uint32_t {
-    if (hi > bm) hi = bm;
-    if (lo >= hi) return 0u;
-    const uint64_t i = lo + lane;
-    const uint32_t b = bmp[i < hi ? i : hi - 1];  // no branch around the load
-    uint32_t c = i < hi ? uint32_t(__popc(b)) : 0u;
-    for (uint64_t k = i + 64; k < hi; k += 64) c += __popc(uint32_t(bmp[k]));
-    return wave_sum(c);
-  };
-  // flagged blocks in front of this workgroup's first tile (all threads)
-  auto group_prefix = [&](uint64_t before) -> uint32_t {
-    return block_sum(popc_bytes_part(bmp, before < bm ? before : bm), s_red);
-  };
-
-  uint32_t prefix = 0;
-  if (ELEMS) {
-    if (!live) return;
-    prefix = a.counts[tile];
-    uint32_t mask[8], excl[8];
-    uint32_t run = 0;
+  uint8_t *const exc_out =
+      a.out + kHeaderBytes + n16 + pad16(bitmap_bytes(n, 0));
+  const uint32_t prefix = a.counts[tile];
+  uint32_t mask[8], excl[8];
+  uint32_t run = 0;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
-      const uint32_t valid = octet_valid(elem, n);
-      mask[u] = valid ? uint32_t(bmp[elem >> 3]) & ((1u << valid) - 1u) : 0u;
-      const uint32_t c = __popc(mask[u]);
-      const uint32_t incl = wave_incl_scan(c);
-      excl[u] = run + incl - c;
-      run += __shfl(incl, 63, 64);
-    }
-    uint4 wv[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
-      if (mask[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      uint32_t mm = mask[u];
-      if (!mm) continue;
-      uint2 e, sm;
-      split4(wv[u].x, wv[u].y, e.x, sm.x);
-      split4(wv[u].z, wv[u].w, e.y, sm.y);
-      uint64_t pos = uint64_t(prefix) + excl[u];
-      while (mm) {
-        const uint32_t i = __builtin_ctz(mm);
-        if (pos < n) exc_out[pos] = uint8_t(octet_byte(e, i));
-        ++pos;
-        mm &= mm - 1u;
-      }
-    }
-  } else {
-    // (1) the tile's own flags, as one to four 64-bit words, never reading
-    // past the zero-padded bitmap (the exception section behind it is being
-    // written by other tiles)
-    const uint32_t nbytes = uint32_t(per_tile);
-    const uint64_t byte0 = uint64_t(tile) * nbytes;
-    uint64_t fw[4] = {0ull, 0ull, 0ull, 0ull};
-    if (live) {
-      const uint64_t lim = bm16 > byte0 ? bm16 - byte0 : 0;
-      const uint32_t have = nbytes < lim ? nbytes : uint32_t(lim);
-      if (have == nbytes && nbytes >= 8) {
-        // byte0 is a multiple of nbytes, so 8-byte aligned
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          if (uint32_t(k) * 8u < nbytes)
-            fw[k] = *reinterpret_cast<const uint64_t *>(bmp + byte0 + 8u * k);
-      } else {
-        for (uint32_t i = 0; i < have; ++i)
-          fw[i >> 3] |= uint64_t(bmp[byte0 + i]) << (8u * (i & 7u));
-      }
-    }
-    // (2) W' of the changed octets, the first four now, overlapping the
-    // offset; holding all eight across it costs a wave per SIMD (88 VGPRs,
-    // and the OLMoE shard's 1536 workgroups no longer fit in one round)
-    bool ch[8];
-    uint4 wv[4];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t o = uint32_t(u) * 64u + lane;
-      const uint64_t elem = tbase + uint64_t(o) * 8;
-      const uint32_t bl = (o << 3) >> log2B;
-      ch[u] = live && elem < n && ((pick<4>(fw, bl >> 6) >> (bl & 63u)) & 1ull);
-      if (u < 4 && ch[u])
-        wv[u & 3] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
-    }
-    // (3) the offset, overlapping the loads above
-    if (a.scan_prefix) {
-      if (!live) return;
-      prefix = a.counts[tile];
-    } else {
-      const uint32_t sib =
-          wave_popc(uint64_t(blockIdx.x) * 4u * per_tile, byte0);
-      prefix = group_prefix(uint64_t(blockIdx.x) * 4u * per_tile);
-      if (!live) return;
-      prefix += sib;
-    }
-    auto put_octet = [&](int u, const uint4 &w) {
-      const uint32_t o = uint32_t(u) * 64u + lane;
-      const uint64_t elem = tbase + uint64_t(o) * 8;
-      const uint32_t valid = octet_valid(elem, n);
-      const uint32_t bl = (o << 3) >> log2B;
-      const uint64_t word = pick<4>(fw, bl >> 6);
-      uint32_t rank = uint32_t(__popcll(word & ((1ull << (bl & 63u)) - 1ull)));
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        if (uint32_t(k) < (bl >> 6)) rank += uint32_t(__popcll(fw[k]));
-      const uint64_t pos =
-          (uint64_t(prefix + rank) << log2B) | ((o << 3) & (B - 1u));
-      if (pos + valid <= n) put_exc_octet<VEC, F16>(exc_out, pos, w, valid);
-    };
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (ch[u]) put_octet(u, wv[u]);
-    // (4) the other four
-#pragma unroll
-    for (int u = 4; u < 8; ++u) {
-      const uint64_t elem = tbase + (uint64_t(u) * 64u + lane) * 8;
-      if (ch[u]) wv[u & 3] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
-    }
-#pragma unroll
-    for (int u = 4; u < 8; ++u)
-      if (ch[u]) put_octet(u, wv[u & 3]);
+  for (int u = 0; u < 8; ++u) {
+    const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
+    const uint32_t valid = octet_valid(elem, n);
+    mask[u] = valid ? uint32_t(bmp[elem >> 3]) & ((1u << valid) - 1u) : 0u;
+    const uint32_t c = __popc(mask[u]);
+    const uint32_t incl = wave_incl_scan(c);
+    excl[u] = run + incl - c;
+    run += __shfl(incl, 63, 64);
   }
-
-  // ---- the last tile knows the totals ----
-  const uint32_t last = a.num_tiles - 1;
-  if (tile == last) {
-    const uint64_t total_changed =
-        ELEMS ? uint64_t(a.counts[a.num_tiles])
-              : uint64_t(prefix) +
-                    wave_popc(uint64_t(last) * per_tile,
-                              uint64_t(last) * per_tile + per_tile);
-    exc_finish<ELEMS, F16>(a, total_changed, lane);
+  uint4 wv[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
+    if (mask[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
   }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    uint32_t mm = mask[u];
+    if (!mm) continue;
+    uint2 e, sm;
+    split4(wv[u].x, wv[u].y, e.x, sm.x);
+    split4(wv[u].z, wv[u].w, e.y, sm.y);
+    uint64_t pos = uint64_t(prefix) + excl[u];
+    while (mm) {
+      const uint32_t i = __builtin_ctz(mm);
+      if (pos < n) exc_out[pos] = uint8_t(octet_byte(e, i));
+      ++pos;
+      mm &= mm - 1u;
+    }
+  }
+  if (tile == a.num_tiles - 1)
+    exc_finish<true, false>(a, uint64_t(a.counts[a.num_tiles]), lane);
 }
 
 // Pass 2 for B >= 512. A row of 512 values lies inside one block, so it is
@@ -1074,6 +962,131 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   if (t0 < nt && t1 == nt) {
     uint32_t own = 0;
     for (uint64_t i = t0 + lane; i < min(t1, bm); i += 64)
+      own += __popc(uint32_t(bmp[i]));
+    exc_finish<false, F16>(a, uint64_t(prefix) + wave_sum(own), lane);
+  }
+}
+
+// Pass 2 for B = 16 ... 256, over the changed blocks only. A block is
+// B / 8 octets, so one wave instruction covers 512 / B blocks; the k-th
+// changed block's exponents start at B k in the list. Each wave takes a run
+// of a.exc_tiles_per_wave tiles (512 / B bitmap bytes each), lists the
+// changed blocks of each 64-block chunk of its run in LDS (ballot and mbcnt),
+// and copies them kExcBatch instructions at a time: the work follows the
+// changed blocks, not the shard. The first batch is issued before the
+// offset count of the run, and the two overlap.
+template <bool VEC, bool F16>
+__global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
+    EncArgs a) {
+  constexpr uint32_t D = kExcBatch;
+  __shared__ uint32_t s_red[4];
+  __shared__ uint32_t s_list[4][64];  // a wave's changed blocks of a chunk
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint64_t n = a.n;
+  const uint32_t log2B = a.log2B;
+  const uint32_t lpb_log2 = log2B - 3;  // lanes per block
+  const uint32_t bpr_log2 = 9 - log2B;  // blocks per instruction
+  const uint32_t slot = lane >> lpb_log2;
+  const uint64_t in_blk = uint64_t(lane & ((1u << lpb_log2) - 1u)) * 8u;
+  const uint64_t S_sm = sm_bytes(n, F16);
+  const uint64_t n16 = pad16(S_sm);
+  const uint64_t bm = bitmap_bytes(n, log2B);
+  const uint8_t *const bmp = a.out + kHeaderBytes + n16;
+  uint8_t *const exc_out = a.out + kHeaderBytes + n16 + pad16(bm);
+  const uint64_t nt = a.num_tiles, tpw = a.exc_tiles_per_wave;
+  const uint64_t bpt = (kEncChunk >> log2B) >> 3;  // bitmap bytes per tile
+  const uint64_t g0 = min(uint64_t(blockIdx.x) * 4u * tpw, nt);
+  const uint64_t t0 = min(g0 + wave * tpw, nt);
+  const uint64_t t1 = min(t0 + tpw, nt);
+  const uint64_t nblk = blocks_of(n, log2B);
+  const uint64_t b0 = min(t0 * bpt * 8u, nblk);
+  const uint64_t b1 = min(t1 * bpt * 8u, nblk);
+  uint32_t *const list = s_list[wave];
+
+  // the changed blocks among [c, c + 64) of the run, listed in order
+  uint64_t c = b0;
+  uint32_t nm = 0, r = 0;  // listed blocks of chunk c, and those taken
+  auto list_chunk = [&]() {
+    const uint64_t b = c + lane;
+    bool f = false;
+    if (b < b1) f = (bmp[b >> 3] >> (b & 7u)) & 1u;
+    const uint64_t m = __ballot(f);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();  // the last chunk's list was read
+    if (f)
+      list[__builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u))] =
+          uint32_t(b);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    nm = uint32_t(__popcll(m));
+    r = 0;
+  };
+  uint32_t kk[D], valid[D];
+  uint64_t elem[D];
+  uint4 wv[D];
+  uint32_t taken = 0;  // list entries this batch covers
+  // the next batch: D instructions of 512 / B listed blocks, W' loads issued
+  auto take_batch = [&]() {
+#pragma unroll
+    for (uint32_t d = 0; d < D; ++d) {
+      kk[d] = r + (d << bpr_log2) + slot;
+      valid[d] = 0;
+      if (kk[d] < nm) {
+        elem[d] = (uint64_t(list[kk[d]]) << log2B) + in_blk;
+        valid[d] = octet_valid(elem[d], n);
+        if (valid[d]) wv[d] = reread_w8<VEC>(a.w + elem[d], valid[d]);
+      }
+    }
+    taken = min(nm - r, D << bpr_log2);
+  };
+  if (b0 < b1) {
+    list_chunk();
+    take_batch();
+  }
+
+  // the run's offset in changed blocks: the bitmap bytes in front of it
+  uint32_t prefix;
+  if (a.scan_prefix) {
+    prefix = a.counts[t0];
+  } else {
+    const uint64_t gb = min(g0 * bpt, bm);  // the workgroup's bytes in front
+    const uint64_t sb = min(t0 * bpt, bm);  // + the sibling runs in front
+    const uint64_t si = gb + lane;
+    const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
+    const uint32_t cg = popc_bytes_part(bmp, gb);
+    uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
+    for (uint64_t i = si + 64; i < sb; i += 64)
+      cs += __popc(uint32_t(bmp[i]));
+    prefix = block_sum(cg, s_red) + wave_sum(cs);
+  }
+
+  uint64_t out_blk = prefix;  // list index of the batch's first block
+  while (b0 < b1) {
+#pragma unroll
+    for (uint32_t d = 0; d < D; ++d) {
+      if (valid[d]) {
+        const uint64_t pos = ((out_blk + kk[d] - r) << log2B) + in_blk;
+        if (pos + valid[d] <= n)
+          put_exc_octet<VEC, F16>(exc_out, pos, wv[d], valid[d]);
+      }
+    }
+    out_blk += taken;
+    r += taken;
+    while (r >= nm) {
+      c += 64;
+      if (c >= b1) break;
+      list_chunk();
+    }
+    if (c >= b1) break;
+    take_batch();
+  }
+
+  if (t0 < nt && t1 == nt) {
+    uint32_t own = 0;
+    for (uint64_t i = t0 * bpt + lane; i < min(t1 * bpt, bm); i += 64)
       own += __popc(uint32_t(bmp[i]));
     exc_finish<false, F16>(a, uint64_t(prefix) + wave_sum(own), lane);
   }
@@ -1727,15 +1740,36 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
                        a.counts, a.num_tiles, uint64_t(0));
   if (elems) {
     if (vec)
-      hipLaunchKernelGGL((encode_exc_kernel<true, true>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((encode_exc_elems_kernel<true>), grid, block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_exc_kernel<false, true>), grid, block, 0, s, a);
-  } else if (a.log2B >= 9) {
-    EncArgs r = a;
-    if (r.exc_tiles_per_wave == 0) r.exc_tiles_per_wave = 1;
-    const uint64_t waves = (uint64_t(r.num_tiles) + r.exc_tiles_per_wave - 1) /
-                           r.exc_tiles_per_wave;
-    const dim3 rgrid(uint32_t((waves + 3) / 4));
+      hipLaunchKernelGGL((encode_exc_elems_kernel<false>), grid, block, 0, s,
+                         a);
+    return hipGetLastError();
+  }
+  // B >= 16: runs of tiles per wave, over the changed blocks (B <= 256) or
+  // the changed 512-value rows (B >= 512)
+  EncArgs r = a;
+  if (r.exc_tiles_per_wave == 0) r.exc_tiles_per_wave = 1;
+  const uint64_t waves = (uint64_t(r.num_tiles) + r.exc_tiles_per_wave - 1) /
+                         r.exc_tiles_per_wave;
+  const dim3 rgrid(uint32_t((waves + 3) / 4));
+  if (r.log2B < 9) {
+    if (r.f16) {
+      if (vec)
+        hipLaunchKernelGGL((encode_exc_blocks_kernel<true, true>), rgrid,
+                           block, 0, s, r);
+      else
+        hipLaunchKernelGGL((encode_exc_blocks_kernel<false, true>), rgrid,
+                           block, 0, s, r);
+    } else {
+      if (vec)
+        hipLaunchKernelGGL((encode_exc_blocks_kernel<true, false>), rgrid,
+                           block, 0, s, r);
+      else
+        hipLaunchKernelGGL((encode_exc_blocks_kernel<false, false>), rgrid,
+                           block, 0, s, r);
+    }
+  } else {
     if (r.f16) {
       if (vec)
         hipLaunchKernelGGL((encode_exc_rows_kernel<true, true>), rgrid, block,
@@ -1751,20 +1785,6 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
         hipLaunchKernelGGL((encode_exc_rows_kernel<false, false>), rgrid,
                            block, 0, s, r);
     }
-  } else if (a.f16) {
-    if (vec)
-      hipLaunchKernelGGL((encode_exc_kernel<true, false, true>), grid, block,
-                         0, s, a);
-    else
-      hipLaunchKernelGGL((encode_exc_kernel<false, false, true>), grid, block,
-                         0, s, a);
-  } else {
-    if (vec)
-      hipLaunchKernelGGL((encode_exc_kernel<true, false>), grid, block, 0, s,
-                         a);
-    else
-      hipLaunchKernelGGL((encode_exc_kernel<false, false>), grid, block, 0, s,
-                         a);
   }
   return hipGetLastError();
 }
