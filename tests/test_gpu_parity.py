@@ -25,10 +25,11 @@ def gu():
     return gpu_util
 
 
-@pytest.mark.parametrize("B", [512, 1024, 2048, 4096])
+@pytest.mark.parametrize("B", [16, 32, 64, 128, 256, 512, 1024, 2048, 4096])
 def test_encode_rows_random_sizes(gu, orc, B):
-    """The row-wise exception pass (B >= 512) on seeded random sizes and
-    change rates, bf16 and fp16, against the oracle byte for byte."""
+    """The run-per-wave exception passes (over changed blocks for B <= 256,
+    over changed rows for B >= 512) on seeded random sizes and change rates,
+    bf16 and fp16, against the oracle byte for byte."""
     from paper_2609_04609_amd import ciera, synth
     rng = np.random.default_rng(B)
     sizes = [int(x) for x in rng.integers(1, 2_000_000, 6)]
@@ -55,13 +56,13 @@ def test_encode_rows_random_sizes(gu, orc, B):
     assert ws.error() == 0
 
 
+@pytest.mark.parametrize("B", [64, 512])
 @pytest.mark.parametrize("n", [16384 * 4096, 16384 * 4096 + 1,
                                16384 * 4096 + 4097])
-def test_encode_rows_run_boundary(gu, orc, n):
-    """Shards around the size where the row-wise exception pass goes from
-    one tile per wave to two (16,384 tiles of 4096 values at B = 512): the
-    last run may hold a single, partial tile."""
-    B = 512
+def test_encode_rows_run_boundary(gu, orc, n, B):
+    """Shards around the size where the exception pass goes from one tile
+    per wave to two (16,384 tiles of 4096 values): the last run may hold a
+    single, partial tile."""
     w, w2 = gu.pair(n, 9300 + n % 7, c=0.0005)
     cache_h = orc.split(gu.host_u16(w))[0]
     del w
