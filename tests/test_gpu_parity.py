@@ -222,7 +222,7 @@ def test_encode_edge_cases(gu, orc):
     assert ws.error() == 0
 
 
-@pytest.mark.parametrize("B", [1, 64])
+@pytest.mark.parametrize("B", [1, 64, 512, 4096])
 def test_encode_unaligned_pointers(gu, orc, B):
     """Inputs that are not 16-byte aligned take the element-wise path."""
     from paper_2609_04609_amd import ciera
