@@ -108,17 +108,25 @@ __device__ uint32_t block_argmax(uint64_t v, uint32_t idx, uint64_t *s_key) {
 
 // ================================================================ coding ==
 
+// The exponents of the changed blocks crowd into a few values, so the lanes
+// of one instruction adding into a single LDS histogram would mostly hit the
+// same counters. The workgroup keeps kHistCopies copies, thread t adding into
+// copy t mod kHistCopies; a copy is 257 words long, so one symbol's counters
+// in different copies fall in different LDS banks.
+constexpr int kHistCopies = 16;
+constexpr int kHistStride = 257;
 __global__ __launch_bounds__(kThreads) void ans_hist_kernel(AnsEncArgs a) {
-  __shared__ uint32_t s_h[kWaves][256];
+  __shared__ uint32_t s_h[kHistCopies * kHistStride];
   const uint8_t *enc = a.enc;
   const uint32_t mode = ld32(enc + 4) >> 16;
   const uint64_t E = ld64(enc + 32);
   if (mode != kModeCompressed || ld32(enc + 12) != kDtypeBf16 || E == 0 ||
       E > a.n)
     return;
-  const int tid = threadIdx.x, wave = tid >> 6;
-  for (int i = tid; i < kWaves * 256; i += kThreads) (&s_h[0][0])[i] = 0u;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < kHistCopies * kHistStride; i += kThreads) s_h[i] = 0u;
   __syncthreads();
+  uint32_t *const h = s_h + (tid & (kHistCopies - 1)) * kHistStride;
   const uint8_t *exc = enc + exc_offset(a.n, a.log2B);
   const uint64_t stride = uint64_t(gridDim.x) * kThreads * 16;
   for (uint64_t i = (uint64_t(blockIdx.x) * kThreads + tid) * 16; i < E;
@@ -130,15 +138,15 @@ __global__ __launch_bounds__(kThreads) void ans_hist_kernel(AnsEncArgs a) {
       for (int k = 0; k < 4; ++k)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
-          atomicAdd(&s_h[wave][(w[k] >> (8 * b)) & 255u], 1u);
+          atomicAdd(&h[(w[k] >> (8 * b)) & 255u], 1u);
     } else {
-      for (uint64_t k = i; k < E; ++k) atomicAdd(&s_h[wave][exc[k]], 1u);
+      for (uint64_t k = i; k < E; ++k) atomicAdd(&h[exc[k]], 1u);
     }
   }
   __syncthreads();
   uint32_t t = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) t += s_h[w][tid];
+  for (int c = 0; c < kHistCopies; ++c) t += s_h[c * kHistStride + tid];
   if (t) atomicAdd(&a.ans->hist[tid], t);
 }
 
