@@ -198,12 +198,26 @@ __global__ __launch_bounds__(kThreads) void ans_table_kernel(AnsEncArgs a) {
 // Persistent: a wave codes chunk c = (round * grid + workgroup) * 4 + wave;
 // every workgroup runs the same number of rounds so that its barriers match.
 __global__ __launch_bounds__(kThreads) void ans_encode_kernel(AnsEncArgs a) {
-  __shared__ uint32_t s_tab[256];  // f | cum << 13
+  // per symbol: the reciprocal m of f, and f | cum << 13 | sh2 << 26 |
+  // sh1 << 30
+  __shared__ uint2 s_tab[256];
   __shared__ __align__(16) uint8_t s_sym[kWaves][kAnsChunk];
   const uint32_t K = a.ans->K;
   if (K == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  s_tab[tid] = a.ans->freq[tid] | (a.ans->cum[tid] << 13);
+  {
+    // x / f without a divide (Granlund and Montgomery 1994, division by
+    // invariant integers, Fig. 4.1): with l = ceil(log2 f) and
+    // m = floor(2^32 (2^l - f) / f) + 1 < 2^32, t = mulhi(x, m) gives
+    // x / f = (t + ((x - t) >> min(l, 1))) >> max(l - 1, 0) for every
+    // 32-bit x. Absent symbols (f = 0) are never coded.
+    const uint32_t f = a.ans->freq[tid], cm = a.ans->cum[tid];
+    const uint32_t l = f > 1u ? 32u - uint32_t(__clz(f - 1u)) : 0u;
+    const uint32_t m =
+        f ? uint32_t(((((uint64_t(1) << l) - f) << 32) / f) + 1u) : 0u;
+    const uint32_t sh1 = l < 1u ? l : 1u, sh2 = l > 1u ? l - 1u : 0u;
+    s_tab[tid] = make_uint2(m, f | (cm << 13) | (sh2 << 26) | (sh1 << 30));
+  }
   const uint64_t E = ld64(a.enc + 32);
   const uint8_t *exc = a.enc + exc_offset(a.n, a.log2B);
   const uint32_t per_round = gridDim.x * kWaves;
@@ -231,8 +245,8 @@ __global__ __launch_bounds__(kThreads) void ans_encode_kernel(AnsEncArgs a) {
     for (int t = int((len + 63) / 64) - 1; t >= 0; --t) {
       const uint32_t i = uint32_t(t) * 64 + uint32_t(lane);
       const bool live = i < len;
-      const uint32_t e = s_tab[live ? s_sym[wave][i] : 0u];
-      const uint32_t f = e & 0x1FFFu, cm = e >> 13;
+      const uint2 e = s_tab[live ? s_sym[wave][i] : 0u];
+      const uint32_t f = e.y & 0x1FFFu, cm = (e.y >> 13) & 0xFFFu;
       const bool emit = live && uint64_t(x) >= (uint64_t(f) << 20);
       const uint64_t m = __ballot(emit);
       const uint32_t cnt = uint32_t(__popcll(m));
@@ -241,7 +255,12 @@ __global__ __launch_bounds__(kThreads) void ans_encode_kernel(AnsEncArgs a) {
         x >>= 16;
       }
       p -= cnt;
-      if (live) x = ((x / f) << kAnsScale) + (x % f) + cm;
+      if (live) {
+        const uint32_t t = __umulhi(x, e.x);
+        const uint32_t q =
+            (t + ((x - t) >> (e.y >> 30))) >> ((e.y >> 26) & 15u);
+        x = (q << kAnsScale) + (x - q * f) + cm;
+      }
     }
     a.states[uint64_t(c) * 64 + uint32_t(lane)] = x;
     if (lane == 0) a.counts[c] = kAnsChunk - p;
