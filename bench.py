@@ -763,8 +763,13 @@ def run(args):
     mixed = (time_mixed_layer(B, dev, min(args.steps, 20), stream)
              if args.others and B >= 16 else None)
 
-    t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
-    t_dec = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
+    enc_us = [e[0].elapsed_time(e[1]) * 1e3 for e in evs]
+    dec_us = [e[1].elapsed_time(e[2]) * 1e3 for e in evs]
+    t_enc = float(np.mean(enc_us)) / 1e6
+    t_dec = float(np.mean(dec_us)) / 1e6
+
+    def spread(v):
+        return [round(float(x), 2) for x in np.percentile(v, [10, 50, 90])]
     t_upd = time_update_cache(S, args.steps, stream)
     # exponents that changed in rank 0's shard: the fused cache update's bytes
     d0 = ((S.W[:n].to(torch.int32) ^ S.W2[:n].to(torch.int32)) >> 7) & 0xFF
@@ -794,6 +799,7 @@ def run(args):
         "config": {"workload": describe(wl, B), "name": wl.name,
                    "shards": R, "shard_elems": n, "block_elems": B},
         "encode": {"us": round(t_enc * 1e6, 2),
+                   "us_p10_p50_p90": spread(enc_us),
                    "bf16_gbps": round(2 * n / t_enc / 1e9, 1),
                    "hbm_gbps": round(b_enc / t_enc / 1e9, 1),
                    "hbm_frac": round(b_enc / t_enc / 1e9 / HBM_PEAK_GBPS, 4),
@@ -808,6 +814,7 @@ def run(args):
                          "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
                          "alg_bytes": b_upd},
         "decode": {"us": round(t_dec * 1e6, 2),
+                   "us_p10_p50_p90": spread(dec_us),
                    "bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
                    "hbm_gbps": round(b_dec / t_dec / 1e9, 1),
                    "hbm_frac": round(b_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
