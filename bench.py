@@ -39,14 +39,14 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
 # (scaled by a 1 GiB copy), for the kernel source with this sha256; see
 # profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "0cb9ec2e61d6decf7993bcdb2d7453f284cc2d298fb601bda9fb771016b571ff"
+_SRC_SHA = "494189aba3c4663f82e5f92dc1a890ca340e46551692eba66f31b9e6d7e13c70"
 MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780150349),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873466317),
+    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780160205),
+    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873777222),
     # measured apart from the OLMoE figures, so it keeps its own source hash
     ("dsv3_layer", 512, "bf16"): (
-        "0cb9ec2e61d6decf7993bcdb2d7453f284cc2d298fb601bda9fb771016b571ff",
-        48950115670),
+        "494189aba3c4663f82e5f92dc1a890ca340e46551692eba66f31b9e6d7e13c70",
+        48950711623),
 }
 
 

@@ -1650,8 +1650,11 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
     if (valid < 8) mask[u] &= (1u << valid) - 1u;
     cnt[u] = __popc(mask[u]);
     if (full) {
-      if (!UPDATE_ONLY) smv[u] = *reinterpret_cast<const uint2 *>(sm_in + elem);
-      ev[u] = *reinterpret_cast<const uint2 *>(cache + elem);
+      // streams this call touches once: non-temporal, as in decode_kernel
+      // (the cache update alone keeps plain loads there too)
+      if (!UPDATE_ONLY) smv[u] = ld_nt8(sm_in + elem);
+      ev[u] = UPDATE_ONLY ? *reinterpret_cast<const uint2 *>(cache + elem)
+                          : ld_nt8(cache + elem);
     } else {
       smv[u] = make_uint2(0u, 0u);
       ev[u] = make_uint2(0u, 0u);
@@ -1688,7 +1691,10 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
       uint4 wv;
       merge4(ev[u].x, smv[u].x, wv.x, wv.y);
       merge4(ev[u].y, smv[u].y, wv.z, wv.w);
-      store_w8<VEC>(out + elem, wv, valid);
+      if (full)
+        st_nt16(out + elem, wv);
+      else
+        store_w8<VEC>(out + elem, wv, valid);
     }
   }
   if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
