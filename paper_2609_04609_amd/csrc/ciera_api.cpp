@@ -29,8 +29,8 @@ bool aligned(const void *p, uintptr_t a) {
 // count scan.
 constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 
-// The encode's exception pass: each 4-tile workgroup counts the bitmap in
-// front of it, half the bitmap on average.
+// The encode's exception pass: each workgroup (four waves, each with a run
+// of tiles) counts the bitmap in front of it, half the bitmap on average.
 bool use_count_scan(uint64_t n, uint32_t l) {
   if (l == 0) return false;
   const uint64_t tiles = enc_tiles(n, l);

@@ -78,8 +78,9 @@ static_assert((kDecTile & (kDecTile - 1)) == 0 && kDecTile >= 4096,
 // lane) when B <= 512, and 8 blocks (8B values, several chunks) when B > 512,
 // so that every tile owns whole bitmap bytes.
 constexpr uint64_t kEncChunk = 4096;
-// B >= 512: re-reads of W' that one wave of the exception pass keeps in
-// flight, and the waves it aims for
+// B >= 16: the wave instructions of W' re-reads that one wave of the
+// exception pass keeps in flight, and the number of waves it aims for (each
+// wave takes a run of exc_tiles_per_wave tiles)
 constexpr uint32_t kExcBatch = 4;
 constexpr uint64_t kExcRowWaves = 16384;
 // 16-byte bitmap words per thread that a workgroup counting the flagged
@@ -114,7 +115,7 @@ struct EncArgs {
   // B >= 16: pass 1 writes per-tile counts and a scan turns them into the
   // exception pass's offsets (else each workgroup counts the bitmap)
   bool scan_prefix;
-  // B >= 512: tiles per wave of the row-wise exception pass
+  // B >= 16: tiles per wave of the exception pass
   uint32_t exc_tiles_per_wave;
   bool f16;  // fp16 values (B >= 16)
   // block-hash detector (B >= 16) in place of exact compare with `cache`
