@@ -215,10 +215,13 @@ def codec_steps(S, warmup, steps, stream):
         one(warmup + s, evs[s])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
-    expect = S.W2 if (warmup + steps - 1) % 2 == 0 else S.W
+    last_even = (warmup + steps - 1) % 2 == 0
+    expect = S.W2 if last_even else S.W
     ok = bool(torch.equal(S.out, expect))
     if not S.raw:
-        ok = ok and bool(torch.equal(S.cache[:n], S.send_cache))
+        g, t = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
+        ok = ok and bool(torch.equal(S.cache[:n], S.send_cache)) and \
+            bool(torch.equal(S.tmp[:t], g[:t]))
     if not ok or S.ws_enc.error() or S.ws_dec.error():
         raise RuntimeError("codec steps are not exact")
     t_enc = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / 1e3
@@ -739,11 +742,14 @@ def run(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    # the last step decoded the full layer: it must equal W' or W exactly
+    # the last step decoded the full layer: it must equal W' or W exactly,
+    # and its encode must have produced the bytes of rank 0's gathered slot
     last_even = ((base + args.steps - 1) % 2) == 0
     expect = S.W2 if last_even else S.W
+    g_last, t0_last = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
     ok = bool(torch.equal(S.out, expect)) and \
-        bool(torch.equal(S.cache[:n], S.send_cache))
+        bool(torch.equal(S.cache[:n], S.send_cache)) and \
+        bool(torch.equal(S.tmp[:t0_last], g_last[:t0_last]))
     errs = S.ws_enc.error() | S.ws_dec.error()
     if not ok or errs:
         raise RuntimeError(f"timed steps are not exact (err={errs})")

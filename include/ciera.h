@@ -69,11 +69,14 @@
  * `stream`, and return at once: they never allocate, free or synchronise. A
  * negative return means nothing was enqueued. Errors that only the device can
  * see (a shard whose header does not match the call, a shard offset that is
- * not 16-byte aligned, an exception index past the shard's list) set bits in
- * the error word at the start of the workspace; the shard concerned is skipped
- * (header errors) or its output is unspecified (inconsistent bitmap), and no
- * access leaves the shard's `total` bytes. The word is sticky: read it with
- * ciera_workspace_error after the stream has run.
+ * not 16-byte aligned, a shard that does not fit in the buffer length the
+ * caller gave, an exception index past the shard's list) set bits in the
+ * error word at the start of the workspace; the shard concerned is skipped
+ * (header, alignment and length errors) or its output is unspecified
+ * (inconsistent bitmap). The decoding calls read nothing outside the caller's
+ * [buffer, buffer + length): a shard's 64-byte header is read only when it
+ * lies inside, and its sections only when its `total` does too. The word is
+ * sticky: read it with ciera_workspace_error after the stream has run.
  *
  * The workspace is caller memory of at least ciera_workspace_bytes(); prepare
  * it once with ciera_workspace_init. Every call leaves it ready for the next.
@@ -103,7 +106,9 @@ enum ciera_status {
 /* Device error word bits (see ciera_workspace_error). */
 #define CIERA_DEVERR_FORMAT 0x1u   /* header magic/version/mode/n/B mismatch */
 #define CIERA_DEVERR_ALIGN 0x2u    /* a shard offset not 16-byte aligned */
-#define CIERA_DEVERR_BOUNDS 0x4u   /* bitmap flags more blocks than E holds */
+#define CIERA_DEVERR_BOUNDS 0x4u   /* a shard runs past the buffer length
+                                      given, or its bitmap flags more blocks
+                                      than E holds */
 #define CIERA_DEVERR_NOSPACE 0x8u  /* an rANS-coded shard met a workspace
                                       sized without CIERA_WS_ANS */
 
@@ -168,6 +173,9 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
 /* Receiver side of Algorithm 1 for the Allgather output: `nshards` encoded
  * shards of `shard_elems` values each, shard j starting at
  * gathered + shard_offsets[j] (device u64 array, offsets 16-byte aligned).
+ * gathered_bytes is the length of the gathered buffer: a shard whose header
+ * (offset + 64) or whose header's total (offset + total) reaches past it is
+ * skipped with CIERA_DEVERR_BOUNDS, before any other byte of it is read.
  * For every shard j it patches exp_cache[j*shard_elems ...] with the changed
  * blocks' exponents and writes the exact values to out[j*shard_elems ...]
  * (the Merge step); raw shards are copied and seed the cache. Compressed
@@ -177,7 +185,8 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
  * are decoded first into the workspace, which must then be sized with
  * CIERA_WS_ANS (else CIERA_DEVERR_NOSPACE). Decoding is idempotent: a
  * second call with the same gathered buffer gives the same out and cache. */
-int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
+int ciera_decode_gathered(const void *gathered, uint64_t gathered_bytes,
+                          const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
                           uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
@@ -199,8 +208,11 @@ int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
 /* The ExpCache patch of Algorithm 1 alone for one encoded shard: afterwards
  * exp_cache holds the exponents of the values that were encoded (changed
  * blocks are overwritten from the exception list; a raw shard sets every
- * byte). This is how a sender brings its own cache forward. */
+ * byte). This is how a sender brings its own cache forward. encoded_bytes is
+ * the length of the `encoded` buffer, checked on the device as for
+ * ciera_decode_gathered (CIERA_DEVERR_BOUNDS: nothing is read or written). */
 int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
+                       uint64_t encoded_bytes,
                        uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                        void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream);

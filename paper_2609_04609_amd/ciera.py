@@ -55,9 +55,9 @@ _SIGS = {
     "ciera_workspace_error": (_i32, [_vp, ctypes.POINTER(_u32), _i32, _vp]),
     "ciera_encode": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64, _vp, _vp,
                             _u64, _vp]),
-    "ciera_decode_gathered": (_i32, [_vp, _vp, _u32, _u64, _u32, _u32, _vp,
-                                     _vp, _vp, _u64, _vp]),
-    "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64,
+    "ciera_decode_gathered": (_i32, [_vp, _u64, _vp, _u32, _u64, _u32, _u32,
+                                     _vp, _vp, _vp, _u64, _vp]),
+    "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u64, _u32, _u32, _vp, _u64,
                                   _vp]),
     "ciera_ans_code": (_i32, [_vp, _u64, _u32, _vp, _vp, _u64, _vp]),
     "ciera_hash_blocks": (_i32, [_vp, _u64, _u32, _vp, _vp]),
@@ -126,21 +126,23 @@ def ciera_encode(w_new, exp_cache, n_elems, block_elems, flags, out,
                               workspace_bytes, stream)
 
 
-def ciera_decode_gathered(gathered, shard_offsets, nshards, shard_elems,
-                          block_elems, out, exp_cache, workspace,
+def ciera_decode_gathered(gathered, gathered_bytes, shard_offsets, nshards,
+                          shard_elems, block_elems, out, exp_cache, workspace,
                           workspace_bytes, stream, flags=0):
     """The C call of the same name; `flags` (0 or FP16) comes last here."""
-    return lib().ciera_decode_gathered(gathered, shard_offsets, nshards,
-                                       shard_elems, block_elems, flags, out,
-                                       exp_cache, workspace, workspace_bytes,
-                                       stream)
+    return lib().ciera_decode_gathered(gathered, gathered_bytes,
+                                       shard_offsets, nshards, shard_elems,
+                                       block_elems, flags, out, exp_cache,
+                                       workspace, workspace_bytes, stream)
 
 
-def ciera_update_cache(exp_cache, encoded, n_elems, block_elems, workspace,
-                       workspace_bytes, stream, flags=0):
+def ciera_update_cache(exp_cache, encoded, encoded_bytes, n_elems,
+                       block_elems, workspace, workspace_bytes, stream,
+                       flags=0):
     """The C call of the same name; `flags` (0 or FP16) comes last here."""
-    return lib().ciera_update_cache(exp_cache, encoded, n_elems, block_elems,
-                                    flags, workspace, workspace_bytes, stream)
+    return lib().ciera_update_cache(exp_cache, encoded, encoded_bytes,
+                                    n_elems, block_elems, flags, workspace,
+                                    workspace_bytes, stream)
 
 
 def ciera_ans_code(encoded, n_elems, block_elems, out_bytes, workspace,
@@ -254,16 +256,24 @@ def ans_code_t(encoded, n_elems, block_elems, ws, out_bytes=None):
     return _check("ciera_ans_code", rc)
 
 
+def _nbytes(t, nbytes):
+    return t.numel() * t.element_size() if nbytes is None else nbytes
+
+
 def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,
-                      ws, fp16=False):
-    rc = ciera_decode_gathered(_ptr(gathered), _ptr(offsets), offsets.numel(),
-                               shard_elems, block_elems, _ptr(out),
-                               _ptr(cache), ws.ptr, ws.nbytes, _stream(),
-                               FP16 if fp16 else 0)
+                      ws, fp16=False, nbytes=None):
+    """Decode the shards of a gathered uint8 tensor; its length bounds every
+    shard unless ``nbytes`` gives another."""
+    rc = ciera_decode_gathered(_ptr(gathered), _nbytes(gathered, nbytes),
+                               _ptr(offsets), offsets.numel(), shard_elems,
+                               block_elems, _ptr(out), _ptr(cache), ws.ptr,
+                               ws.nbytes, _stream(), FP16 if fp16 else 0)
     return _check("ciera_decode_gathered", rc)
 
 
-def update_cache_t(cache, encoded, n_elems, block_elems, ws, fp16=False):
-    rc = ciera_update_cache(_ptr(cache), _ptr(encoded), n_elems, block_elems,
+def update_cache_t(cache, encoded, n_elems, block_elems, ws, fp16=False,
+                   nbytes=None):
+    rc = ciera_update_cache(_ptr(cache), _ptr(encoded),
+                            _nbytes(encoded, nbytes), n_elems, block_elems,
                             ws.ptr, ws.nbytes, _stream(), FP16 if fp16 else 0)
     return _check("ciera_update_cache", rc)

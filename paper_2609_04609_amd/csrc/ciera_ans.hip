@@ -369,7 +369,8 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   uint32_t *const ring = s_ring[wave];
   const uint16_t *const ring16 = reinterpret_cast<const uint16_t *>(ring);
   const uint64_t off = a.offsets ? a.offsets[j] : 0ull;
-  if (off & 15ull) return;  // the decode kernel reports it
+  // the decode kernel reports a misplaced shard
+  if ((off & 15ull) || off > a.bytes || a.bytes - off < kHeaderBytes) return;
   const uint8_t *enc = a.gathered + off;
   const uint64_t n = a.n;
   const uint32_t vm = ld32(enc + 4);
@@ -382,7 +383,10 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   const uint64_t bm = bitmap_bytes(n, a.log2B);
   if (E > n || P < n + bm + kAnsFixed) return;
   const uint64_t C = P - n - bm;
-  if (ld64(enc + 48) != kHeaderBytes + pad16(n) + pad16(bm) + pad16(C)) return;
+  const uint64_t htotal = ld64(enc + 48);
+  if (htotal != kHeaderBytes + pad16(n) + pad16(bm) + pad16(C) ||
+      htotal > a.bytes - off)
+    return;
   const uint8_t *sec = enc + exc_offset(n, a.log2B);
   const uint32_t K = ld32(sec);
   const uint64_t want_k = (E + kAnsChunk - 1) / kAnsChunk;

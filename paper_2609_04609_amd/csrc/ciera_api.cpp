@@ -247,7 +247,8 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
                            workspace_bytes, stream, true, false);
 }
 
-int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
+int ciera_decode_gathered(const void *gathered, uint64_t gathered_bytes,
+                          const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
                           uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
@@ -266,6 +267,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
     return CIERA_ENOSPC;
   DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(gathered);
+  a.bytes = gathered_bytes;
   a.offsets = shard_offsets;
   a.n = shard_elems;
   a.log2B = uint32_t(l);
@@ -288,6 +290,7 @@ int ciera_decode_gathered(const void *gathered, const uint64_t *shard_offsets,
 }
 
 int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
+                       uint64_t encoded_bytes,
                        uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                        void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream) {
@@ -302,6 +305,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   if (!dec_workspace_ok(n_elems, 1, workspace_bytes)) return CIERA_ENOSPC;
   DecArgs a{};
   a.gathered = static_cast<const uint8_t *>(encoded);
+  a.bytes = encoded_bytes;
   a.offsets = nullptr;
   a.n = n_elems;
   a.log2B = uint32_t(l);

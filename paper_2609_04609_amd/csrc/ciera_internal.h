@@ -127,6 +127,7 @@ constexpr int kHashMinLog2B = 4;  // the block hash needs B >= 16
 
 struct DecArgs {
   const uint8_t *gathered;
+  uint64_t bytes;  // length of the gathered buffer: no shard reaches past it
   // decoded exception lists of rANS-coded shards, shard j at
   // ans_exc + j * ans_stride (nullptr: the workspace has no room for them)
   uint8_t *ans_exc;

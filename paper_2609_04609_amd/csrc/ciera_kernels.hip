@@ -743,28 +743,55 @@ __device__ __forceinline__ uint32_t popc_bytes_part(const uint8_t *bmp,
   return c + (ti < nbytes ? uint32_t(__popc(tb)) : 0u);
 }
 
-// The exponents of one octet at exception index pos: bf16 bytes at pos, fp16
-// five bit-plane bytes at 5 (pos / 8).
+// The exponents of one octet (e: one byte per value) at exception index pos:
+// bf16 bytes at pos, fp16 five bit-plane bytes at 5 (pos / 8).
 template <bool VEC, bool F16>
-__device__ __forceinline__ void put_exc_octet(uint8_t *exc_out, uint64_t pos,
-                                              const uint4 &wv,
-                                              uint32_t valid) {
-  uint2 e, t0, t1;
+__device__ __forceinline__ void put_exc_exps(uint8_t *exc_out, uint64_t pos,
+                                             uint2 e, uint32_t valid) {
   if (F16) {
-    split4_f16(wv.x, wv.y, e.x, t0.x, t1.x);
-    split4_f16(wv.z, wv.w, e.y, t0.y, t1.y);
     uint8_t *g = exc_out + 5 * (pos >> 3);
 #pragma unroll
     for (uint32_t q = 0; q < 5; ++q) g[q] = uint8_t(plane_byte(e.x, e.y, q));
+  } else if (VEC && valid == 8) {
+    st_nt8(exc_out + pos, e);
   } else {
-    split4(wv.x, wv.y, e.x, t0.x);
-    split4(wv.z, wv.w, e.y, t0.y);
-    if (VEC && valid == 8)
-      st_nt8(exc_out + pos, e);
-    else
-      store_b8<VEC>(exc_out + pos, e, valid);
+    store_b8<VEC>(exc_out + pos, e, valid);
   }
 }
+
+// Where the exception pass takes a changed octet's exponents from. Without
+// the fused cache update it splits W' again (16 bytes an octet). With it,
+// pass 1 has already written the new exponent of every changed value into
+// the cache, and every other value of a changed block was unchanged, so the
+// cache holds exp(W') for the whole block: 8 bytes an octet.
+template <bool VEC, bool F16, bool FROMC>
+struct ExcSrc {
+  using T = typename std::conditional<FROMC, uint2, uint4>::type;
+  __device__ static __forceinline__ T load(const EncArgs &a, uint64_t elem,
+                                           uint32_t valid) {
+    if constexpr (FROMC) {
+      if (VEC && valid == 8) return ld_nt8(a.cache_out + elem);
+      return load_b8<VEC>(a.cache_out + elem, valid);
+    } else {
+      return reread_w8<VEC>(a.w + elem, valid);
+    }
+  }
+  __device__ static __forceinline__ uint2 exps(const T &v) {
+    if constexpr (FROMC) {
+      return v;
+    } else {
+      uint2 e, t0, t1;
+      if (F16) {
+        split4_f16(v.x, v.y, e.x, t0.x, t1.x);
+        split4_f16(v.z, v.w, e.y, t0.y, t1.y);
+      } else {
+        split4(v.x, v.y, e.x, t0.x);
+        split4(v.z, v.w, e.y, t0.y);
+      }
+      return e;
+    }
+  }
+};
 
 // The totals, known to the wave that holds the last tile: the header, the
 // exception section's zero padding and the encoded size. total_changed
@@ -808,9 +835,10 @@ __device__ void exc_finish(const EncArgs &a, uint64_t total_changed,
 // Pass 2 for B = 1: the tile's changed values, at the tile's offset in the
 // list (from the scanned per-tile counts of pass 1); the last tile writes
 // the header. W' is read again only where the bitmap says so.
-template <bool VEC>
+template <bool VEC, bool FROMC>
 __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
     EncArgs a) {
+  using Src = ExcSrc<VEC, false, FROMC>;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t tile = blockIdx.x * 4u + wave;
   if (tile >= a.num_tiles) return;
@@ -833,19 +861,17 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
     excl[u] = run + incl - c;
     run += __shfl(incl, 63, 64);
   }
-  uint4 wv[8];
+  typename Src::T wv[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
-    if (mask[u]) wv[u] = reread_w8<VEC>(a.w + elem, octet_valid(elem, n));
+    if (mask[u]) wv[u] = Src::load(a, elem, octet_valid(elem, n));
   }
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     uint32_t mm = mask[u];
     if (!mm) continue;
-    uint2 e, sm;
-    split4(wv[u].x, wv[u].y, e.x, sm.x);
-    split4(wv[u].z, wv[u].w, e.y, sm.y);
+    const uint2 e = Src::exps(wv[u]);
     uint64_t pos = uint64_t(prefix) + excl[u];
     while (mm) {
       const uint32_t i = __builtin_ctz(mm);
@@ -866,8 +892,9 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
 // a time, so that that many re-reads of W' are in flight per wave; the first
 // batch is issued before the offset of the run (the changed blocks in front
 // of it) is counted, and the two overlap.
-template <bool VEC, bool F16>
+template <bool VEC, bool F16, bool FROMC>
 __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
+  using Src = ExcSrc<VEC, F16, FROMC>;
   constexpr uint32_t D = kExcBatch;
   __shared__ uint32_t s_red[4];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -898,7 +925,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   };
   uint64_t c = r0, m = r0 < r1 ? chunk_mask(r0) : 0ull;
   uint32_t rr[D], cnt = 0;
-  uint4 wv[D];
+  typename Src::T wv[D];
   // the next batch of changed rows of chunk c: positions and W' loads
   auto take_batch = [&]() {
     cnt = 0;
@@ -915,7 +942,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
       if (d < cnt) {
         const uint64_t elem = ((c + rr[d]) << 9) + uint64_t(lane) * 8;
         const uint32_t valid = octet_valid(elem, n);
-        if (valid) wv[d] = reread_w8<VEC>(a.w + elem, valid);
+        if (valid) wv[d] = Src::load(a, elem, valid);
       }
     }
   };
@@ -946,7 +973,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
         const uint32_t valid = octet_valid(elem, n);
         const uint64_t pos = ((out_row + d) << 9) + uint64_t(lane) * 8;
         if (valid && pos + valid <= n)
-          put_exc_octet<VEC, F16>(exc_out, pos, wv[d], valid);
+          put_exc_exps<VEC, F16>(exc_out, pos, Src::exps(wv[d]), valid);
       }
     }
     out_row += cnt;
@@ -975,9 +1002,10 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
 // and copies them kExcBatch instructions at a time: the work follows the
 // changed blocks, not the shard. The first batch is issued before the
 // offset count of the run, and the two overlap.
-template <bool VEC, bool F16>
+template <bool VEC, bool F16, bool FROMC>
 __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
     EncArgs a) {
+  using Src = ExcSrc<VEC, F16, FROMC>;
   constexpr uint32_t D = kExcBatch;
   __shared__ uint32_t s_red[4];
   __shared__ uint32_t s_list[4][64];  // a wave's changed blocks of a chunk
@@ -1026,7 +1054,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
   };
   uint32_t kk[D], valid[D];
   uint64_t elem[D];
-  uint4 wv[D];
+  typename Src::T wv[D];
   uint32_t taken = 0;  // list entries this batch covers
   // the next batch: D instructions of 512 / B listed blocks, W' loads issued
   auto take_batch = [&]() {
@@ -1037,7 +1065,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
       if (kk[d] < nm) {
         elem[d] = (uint64_t(list[kk[d]]) << log2B) + in_blk;
         valid[d] = octet_valid(elem[d], n);
-        if (valid[d]) wv[d] = reread_w8<VEC>(a.w + elem[d], valid[d]);
+        if (valid[d]) wv[d] = Src::load(a, elem[d], valid[d]);
       }
     }
     taken = min(nm - r, D << bpr_log2);
@@ -1070,7 +1098,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
       if (valid[d]) {
         const uint64_t pos = ((out_blk + kk[d] - r) << log2B) + in_blk;
         if (pos + valid[d] <= n)
-          put_exc_octet<VEC, F16>(exc_out, pos, wv[d], valid[d]);
+          put_exc_exps<VEC, F16>(exc_out, pos, Src::exps(wv[d]), valid[d]);
       }
     }
     out_blk += taken;
@@ -1125,7 +1153,9 @@ struct ShardView {
 };
 
 // Every workgroup validates the header of its shard (a 64-byte line that all
-// of the shard's tiles share in L2). Tile 0 reports what is wrong.
+// of the shard's tiles share in L2). Tile 0 reports what is wrong. The header
+// is read only when it lies inside the caller's buffer, and the shard is used
+// only when its total does too.
 __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
                                                 bool report) {
   ShardView v;
@@ -1137,6 +1167,10 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   v.E = 0;
   if (off & 15ull) {
     if (report) set_error(a.ctl, CIERA_DEVERR_ALIGN);
+    return v;
+  }
+  if (off > a.bytes || a.bytes - off < kHeaderBytes) {
+    if (report) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
     return v;
   }
   const uint32_t *h32 = reinterpret_cast<const uint32_t *>(v.enc);
@@ -1170,6 +1204,10 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   }
   if (!ok) {
     if (report) set_error(a.ctl, CIERA_DEVERR_FORMAT);
+    return v;
+  }
+  if (htotal > a.bytes - off) {
+    if (report) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
     return v;
   }
   v.ok = true;
@@ -1709,6 +1747,29 @@ __global__ void fill_zero_kernel(uint32_t *p, uint64_t words) {
 }  // namespace
 
 // ============================================================= launchers ==
+namespace {
+template <bool B>
+using bool_c = std::integral_constant<bool, B>;
+
+// Launch the exception-pass kernel that pick(vec, f16, from_cache) names,
+// with the three flags as template arguments (f16 is always false at B = 1).
+template <bool ELEMS, typename Pick>
+void launch_exc(dim3 grid, const EncArgs &a, bool vec, bool f16, bool fromc,
+                hipStream_t s, Pick pick) {
+  auto go = [&](auto v, auto f, auto c) {
+    hipLaunchKernelGGL(pick(v, f, c), grid, dim3(kThreads), 0, s, a);
+  };
+  auto with_c = [&](auto v, auto f) {
+    if (fromc) go(v, f, bool_c<true>{}); else go(v, f, bool_c<false>{});
+  };
+  auto with_f = [&](auto v) {
+    if (!ELEMS && f16) with_c(v, bool_c<!ELEMS>{});
+    else with_c(v, bool_c<false>{});
+  };
+  if (vec) with_f(bool_c<true>{}); else with_f(bool_c<false>{});
+}
+}  // namespace
+
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
   const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
   const bool elems = a.log2B == 0;
@@ -1744,12 +1805,12 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
   if (elems || a.scan_prefix)
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
+  // the exception pass reads the updated cache when pass 1 brought it forward
+  const bool fromc = a.cache_out != nullptr;
   if (elems) {
-    if (vec)
-      hipLaunchKernelGGL((encode_exc_elems_kernel<true>), grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL((encode_exc_elems_kernel<false>), grid, block, 0, s,
-                         a);
+    launch_exc<true>(grid, a, vec, false, fromc, s, [](auto v, auto, auto c) {
+      return encode_exc_elems_kernel<decltype(v)::value, decltype(c)::value>;
+    });
     return hipGetLastError();
   }
   // B >= 16: runs of tiles per wave, over the changed blocks (B <= 256) or
@@ -1759,39 +1820,20 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
   const uint64_t waves = (uint64_t(r.num_tiles) + r.exc_tiles_per_wave - 1) /
                          r.exc_tiles_per_wave;
   const dim3 rgrid(uint32_t((waves + 3) / 4));
-  if (r.log2B < 9) {
-    if (r.f16) {
-      if (vec)
-        hipLaunchKernelGGL((encode_exc_blocks_kernel<true, true>), rgrid,
-                           block, 0, s, r);
-      else
-        hipLaunchKernelGGL((encode_exc_blocks_kernel<false, true>), rgrid,
-                           block, 0, s, r);
-    } else {
-      if (vec)
-        hipLaunchKernelGGL((encode_exc_blocks_kernel<true, false>), rgrid,
-                           block, 0, s, r);
-      else
-        hipLaunchKernelGGL((encode_exc_blocks_kernel<false, false>), rgrid,
-                           block, 0, s, r);
-    }
-  } else {
-    if (r.f16) {
-      if (vec)
-        hipLaunchKernelGGL((encode_exc_rows_kernel<true, true>), rgrid, block,
-                           0, s, r);
-      else
-        hipLaunchKernelGGL((encode_exc_rows_kernel<false, true>), rgrid, block,
-                           0, s, r);
-    } else {
-      if (vec)
-        hipLaunchKernelGGL((encode_exc_rows_kernel<true, false>), rgrid, block,
-                           0, s, r);
-      else
-        hipLaunchKernelGGL((encode_exc_rows_kernel<false, false>), rgrid,
-                           block, 0, s, r);
-    }
-  }
+  if (r.log2B < 9)
+    launch_exc<false>(rgrid, r, vec, r.f16, fromc, s,
+                      [](auto v, auto f, auto c) {
+                        return encode_exc_blocks_kernel<decltype(v)::value,
+                                                        decltype(f)::value,
+                                                        decltype(c)::value>;
+                      });
+  else
+    launch_exc<false>(rgrid, r, vec, r.f16, fromc, s,
+                      [](auto v, auto f, auto c) {
+                        return encode_exc_rows_kernel<decltype(v)::value,
+                                                      decltype(f)::value,
+                                                      decltype(c)::value>;
+                      });
   return hipGetLastError();
 }
 

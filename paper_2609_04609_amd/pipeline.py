@@ -14,11 +14,17 @@ same dependency graph for L layer groups in two schedules:
                 receiver  decode_i after Allgather_i
                 compute   compute_i after decode_i
 
-The Allgather is a stand-in: a one-thread spin kernel (torch.cuda._sleep)
-lasting the alpha-beta time alpha + (R-1) x / bw of the encoded payload x,
-while the gathered buffer itself was filled at set-up. Compute_i is a bf16
-linear layer over the decoded weights. Encode, cache update and decode are
-the library's kernels through the C ABI; nothing here computes codec data.
+Every layer has its own gathered buffers. The other ranks' shards in them
+were placed at set-up; rank 0's slot is filled during the step: the sender
+stream first overwrites the slot with 0xFF bytes and then encodes rank 0's
+shard into it, and the receiver decodes the buffer. A decode that ran ahead
+of its encode would meet a bad header or stale bytes and leave wrong values,
+so the schedule's event waits carry the data, not only the timing. The
+Allgather itself is a stand-in: a one-thread spin kernel (torch.cuda._sleep)
+lasting the alpha-beta time alpha + (R-1) x / bw of the encoded payload x.
+Compute_i is a bf16 linear layer over the decoded weights. Encode, cache
+update and decode are the library's kernels through the C ABI; nothing here
+computes codec data.
 """
 from __future__ import annotations
 
@@ -60,7 +66,10 @@ class OverlapPipeline:
                        for _ in range(layers)]
         self.ws_dec = [ciera.Workspace(self.n, self.R, self.B, dev)
                        for _ in range(layers)]
-        self.enc_out = [torch.empty_like(S.tmp) for _ in range(layers)]
+        # per layer the A (W -> W') and B (W' -> W) gathered buffers; rank
+        # 0's slot [0, total_0) is rewritten by the sender every step
+        self.gath = [(S.gA.clone(), S.gB.clone()) for _ in range(layers)]
+        self.slot0 = (int(S.totA[0]), int(S.totB[0]))
         # compute stand-in: x [tokens, 4096] times the decoded layer viewed as
         # [R n / 4096, 4096] bf16 weights
         self.k = 4096
@@ -86,17 +95,38 @@ class OverlapPipeline:
         self.parity = 1 if caches_hold_w2 else 0
 
     def _inputs(self):
+        """(rank 0's new values, A or B side, offsets, link time) of the next
+        step."""
         S = self.S
         if self.parity == 0:
-            return S.W2[:self.n], S.gA, S.offA, self.link_us[0]
-        return S.W[:self.n], S.gB, S.offB, self.link_us[1]
+            return S.W2[:self.n], 0, S.offA, self.link_us[0]
+        return S.W[:self.n], 1, S.offB, self.link_us[1]
 
-    def _layer(self, i, w_in, g, off, link_us, st_send, st_link, st_recv,
+    def _poison(self, i, side):
+        """Overwrite rank 0's slot of layer i's gathered buffer with 0xFF
+        (stale bytes until the sender's encode lands), on the current
+        stream."""
+        g = self.gath[i][side]
+        g[:self.slot0[side]].fill_(0xFF)
+        return g
+
+    def _encode(self, i, w_in, side):
+        """Encode rank 0's shard into its slot, bringing the sender's cache
+        forward, on the current stream."""
+        g = self.gath[i][side]
+        ciera.encode_t(w_in, self.send[i], self.B, self.ws_enc[i], g,
+                       update_cache=True)
+        return g
+
+    def _send(self, i, w_in, side):
+        self._poison(i, side)
+        return self._encode(i, w_in, side)
+
+    def _layer(self, i, w_in, side, off, link_us, st_send, st_link, st_recv,
                st_comp, ev=None):
         n, B = self.n, self.B
         with torch.cuda.stream(st_send):
-            ciera.encode_t(w_in, self.send[i], B, self.ws_enc[i],
-                           self.enc_out[i], update_cache=True)
+            g = self._send(i, w_in, side)
             if ev is not None:
                 ev["enc"][i].record(st_send)
         with torch.cuda.stream(st_link):
@@ -121,7 +151,7 @@ class OverlapPipeline:
     def step(self, overlapped):
         """One iteration over all L layers; returns the wall time in us
         (HIP events on the caller's stream, which every stream joins)."""
-        w_in, g, off, link_us = self._inputs()
+        w_in, side, off, link_us = self._inputs()
         main = torch.cuda.current_stream()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
@@ -132,42 +162,56 @@ class OverlapPipeline:
             ev = {k: [torch.cuda.Event() for _ in range(self.L)]
                   for k in ("enc", "link", "dec")}
             for i in range(self.L):
-                self._layer(i, w_in, g, off, link_us, *self.streams, ev)
+                self._layer(i, w_in, side, off, link_us, *self.streams, ev)
             for st in self.streams:
                 done = torch.cuda.Event()
                 done.record(st)
                 main.wait_event(done)
         else:
             for i in range(self.L):
-                self._layer(i, w_in, g, off, link_us, main, main, main, main)
+                self._layer(i, w_in, side, off, link_us, main, main, main,
+                            main)
         t1.record(main)
         torch.cuda.synchronize()
         self.parity ^= 1
         return t0.elapsed_time(t1) * 1e3
 
+    def last_gathered(self, i):
+        """Layer i's gathered buffer and offsets of the last step."""
+        side = self.parity ^ 1
+        return self.gath[i][side], (self.S.offA, self.S.offB)[side]
+
     def check(self):
-        """Every layer's output and caches equal the last decoded side."""
+        """Every layer's output and caches equal the last decoded side, rank
+        0's slot holds the bytes of the set-up's encoding of the same shard
+        against the same cache, and no device error was raised."""
         S = self.S
-        expect = S.W2 if self.parity == 1 else S.W
+        side = self.parity ^ 1
+        expect = S.W2 if side == 0 else S.W
+        ref = (S.gA, S.gB)[side][:self.slot0[side]]
         for i in range(self.L):
             if not torch.equal(self.outs[i], expect):
                 return False
             if not torch.equal(self.caches[i][:self.n], self.send[i]):
+                return False
+            if not torch.equal(self.gath[i][side][:self.slot0[side]], ref):
+                return False
+            if self.ws_enc[i].error() or self.ws_dec[i].error():
                 return False
         return True
 
     def component_us(self, reps=5):
         """Stand-alone times of one layer's pieces (events, one stream)."""
         main = torch.cuda.current_stream()
-        w_in, g, off, link_us = self._inputs()
+        w_in, side, off, link_us = self._inputs()
         out = {}
         names = ["encode", "link", "decode", "compute"]
         acc = {k: [] for k in names}
         for _ in range(reps):
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            self._poison(0, side)
             ev[0].record(main)
-            ciera.encode_t(w_in, self.send[0], self.B, self.ws_enc[0],
-                           self.enc_out[0], update_cache=True)
+            g = self._encode(0, w_in, side)
             ev[1].record(main)
             torch.cuda._sleep(int(link_us / self.us_per_cycle))
             ev[2].record(main)
@@ -188,12 +232,12 @@ class OverlapPipeline:
         return out
 
     def _replay_back(self, i):
-        """Bring layer i's caches back by decoding the reverse buffer."""
+        """Bring layer i's caches back by encoding and decoding the reverse
+        side."""
         S = self.S
-        w_back, g, off = ((S.W[:self.n], S.gB, S.offB) if self.parity == 0
-                          else (S.W2[:self.n], S.gA, S.offA))
-        ciera.encode_t(w_back, self.send[i], self.B, self.ws_enc[i],
-                       self.enc_out[i], update_cache=True)
+        w_back, side, off = ((S.W[:self.n], 1, S.offB) if self.parity == 0
+                             else (S.W2[:self.n], 0, S.offA))
+        g = self._send(i, w_back, side)
         ciera.decode_gathered_t(g, off, self.n, self.B, self.outs[i],
                                 self.caches[i], self.ws_dec[i])
         torch.cuda.synchronize()

@@ -51,3 +51,26 @@ def gather(encs):
     stand-in for the Allgather output."""
     offs = np.cumsum([0] + [e.size for e in encs[:-1]]).astype(np.uint64)
     return np.concatenate(encs), offs
+
+
+def check_fused_update(orc, w2, cache_h, B, expect, ws, fp16=False, msg=""):
+    """Encode W' with the fused cache update (CIERA_ENC_UPDATE_CACHE) on a
+    device copy of cache_h: the bytes must equal `expect` (the oracle's
+    encoding) and the cache afterwards the oracle's update of cache_h from
+    those bytes, the exponents of W'."""
+    n = w2.numel()
+    flags = ciera.FP16 if fp16 else 0
+    cache = dev_u8(cache_h)
+    cap = int(ciera.ciera_encoded_bound(n, B, flags))
+    out = torch.full((cap,), 0xA5, dtype=torch.uint8, device=DEV)
+    nbytes = torch.zeros(1, dtype=torch.int64, device=DEV)
+    ciera.encode_t(w2, cache, B, ws, out, out_bytes=nbytes, fp16=fp16,
+                   update_cache=True)
+    torch.cuda.synchronize()
+    total = int(nbytes.item())
+    assert total == expect.size, msg
+    np.testing.assert_array_equal(host_u8(out[:total]), expect, err_msg=msg)
+    c_o = np.array(cache_h, dtype=np.uint8, copy=True)
+    (orc.update_cache_f16 if fp16 else orc.update_cache)(c_o, expect, n)
+    np.testing.assert_array_equal(host_u8(cache), c_o, err_msg=msg)
+

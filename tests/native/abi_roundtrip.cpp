@@ -111,8 +111,8 @@ int main() {
                            d_tot + j, d_ws, wsb, s));
   // the receivers' decode of all R shards, twice
   for (int rep = 0; rep < 2; ++rep)
-    CIERA_OK_(ciera_decode_gathered(d_gath, d_offs, R, n, B, 0, d_out, d_recv,
-                                    d_ws, wsb, s));
+    CIERA_OK_(ciera_decode_gathered(d_gath, slot * R, d_offs, R, n, B, 0,
+                                    d_out, d_recv, d_ws, wsb, s));
   uint32_t err = 0;
   CIERA_OK_(ciera_workspace_error(d_ws, &err, 1, s));
   if (err != 0) {

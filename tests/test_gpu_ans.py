@@ -141,6 +141,16 @@ def test_ans_error_paths(gu, orc):
     torch.cuda.synchronize()
     assert ws_small.error() == ciera.DEVERR_NOSPACE
     assert torch.all(out == 7)
+    # a buffer length 16 bytes short of the shard's total (the allocation is
+    # the whole shard, so a missing check would still read mapped memory):
+    # skipped by the rANS pass and the decode alike, output untouched
+    cache_d = gu.dev_u8(cache_h)
+    ciera.decode_gathered_t(gu.dev_u8(enc), offs_t, n, B, out, cache_d, ws,
+                            nbytes=enc.size - 16)
+    torch.cuda.synchronize()
+    assert ws.error() == ciera.DEVERR_BOUNDS
+    assert torch.all(out == 7)
+    np.testing.assert_array_equal(gu.host_u8(cache_d), cache_h)
     a16 = lambda x: -(-x // 16) * 16
     sec = 64 + a16(n) + a16(-(-(-(-n // B)) // 8))
     # a frequency changed: the table no longer sums to 4096

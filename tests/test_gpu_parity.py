@@ -42,6 +42,8 @@ def test_encode_rows_random_sizes(gu, orc, B):
         expect = orc.encode(gu.host_u16(w2), cache_h, B)
         np.testing.assert_array_equal(gu.host_u8(out)[:total], expect,
                                       err_msg=f"n={n} c={c}")
+        gu.check_fused_update(orc, w2, cache_h, B, expect, ws,
+                              msg=f"fused n={n} c={c}")
         f = synth.normal_f16_bits(n, 0.02, 9100 + B + i, "cuda")
         f2 = synth.forced_bernoulli_f16_bits(f, c, 9200 + B + i)
         fc = orc.split_f16(gu.host_u16(f))[0]
@@ -50,9 +52,11 @@ def test_encode_rows_random_sizes(gu, orc, B):
         nb = torch.zeros(1, dtype=torch.int64, device="cuda")
         ciera.encode_t(f2, gu.dev_u8(fc), B, ws, fb, out_bytes=nb, fp16=True)
         torch.cuda.synchronize()
+        expect16 = orc.encode_f16(gu.host_u16(f2), fc, B)
         np.testing.assert_array_equal(
-            gu.host_u8(fb)[:int(nb.item())],
-            orc.encode_f16(gu.host_u16(f2), fc, B), err_msg=f"fp16 n={n}")
+            gu.host_u8(fb)[:int(nb.item())], expect16, err_msg=f"fp16 n={n}")
+        gu.check_fused_update(orc, f2, fc, B, expect16, ws, fp16=True,
+                              msg=f"fused fp16 n={n}")
     assert ws.error() == 0
 
 
@@ -93,7 +97,9 @@ def test_encode_rows_with_count_scan(gu, orc):
     out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
     assert total == expect.size
     np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
-    del w, w2, wh, w2h, cache_h, expect, out
+    del out
+    gu.check_fused_update(orc, w2, cache_h, B, expect, ws, msg="fused")
+    del w, w2, wh, w2h, cache_h, expect
     torch.cuda.empty_cache()
     f = synth.normal_f16_bits(n, 0.02, 3232, "cuda")
     f2 = synth.forced_bernoulli_f16_bits(f, 0.0002, 3233)
@@ -120,6 +126,8 @@ def test_encode_rows_several_chunks(gu, orc):
     expect = orc.encode(gu.host_u16(w2), cache_h, B)
     assert total == expect.size
     np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    del out
+    gu.check_fused_update(orc, w2, cache_h, B, expect, ws, msg="fused")
     assert ws.error() == 0
 
 
@@ -143,6 +151,7 @@ def test_encode_with_count_scan(gu, orc):
     out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
     assert total == expect.size
     np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    gu.check_fused_update(orc, w2, cache_h, B, expect, ws, msg="fused")
     # the block-hash detector gives the same bytes
     nblk = -(-n // B)
     h_in = torch.empty(2 * nblk, dtype=torch.int64, device="cuda")
@@ -162,8 +171,10 @@ def test_encode_with_count_scan(gu, orc):
                      dtype=torch.uint8, device="cuda")
     ciera.encode_t(f2, gu.dev_u8(fc), B, ws, fb, out_bytes=nb, fp16=True)
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(gu.host_u8(fb)[:int(nb.item())],
-                                  orc.encode_f16(gu.host_u16(f2), fc, B))
+    expect16 = orc.encode_f16(gu.host_u16(f2), fc, B)
+    np.testing.assert_array_equal(gu.host_u8(fb)[:int(nb.item())], expect16)
+    gu.check_fused_update(orc, f2, fc, B, expect16, ws, fp16=True,
+                          msg="fused fp16")
     assert ws.error() == 0
 
 
@@ -184,6 +195,8 @@ def test_encode_matches_oracle(gu, orc, B):
         np.testing.assert_array_equal(got[:total], expect, err_msg=f"n={n} B={B}")
         # nothing written past the encoded size
         assert np.all(got[total:] == 0xA5)
+        gu.check_fused_update(orc, w2, cache_h, B, expect, ws,
+                              msg=f"fused n={n} B={B}")
         assert ws.error() == 0
 
 
@@ -334,6 +347,19 @@ def test_decode_with_prefix_pass(gu, orc, n_s):
     np.testing.assert_array_equal(gu.host_u16(out), expect)
     np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
     assert ws.error() == 0
+    # the prefix pass too skips a shard that runs past the given length
+    out.fill_(7)
+    cache = gu.dev_u8(cache0)
+    ciera.decode_gathered_t(gu.dev_u8(gathered),
+                            torch.from_numpy(offs.view(np.int64)).to("cuda"),
+                            n_s, B, out, cache, ws,
+                            nbytes=gathered.size - 16)
+    torch.cuda.synchronize()
+    assert ws.error() == ciera.DEVERR_BOUNDS
+    last = (R - 1) * n_s
+    np.testing.assert_array_equal(gu.host_u16(out[:last]), expect[:last])
+    assert bool(torch.all(out[last:] == 7))
+    np.testing.assert_array_equal(gu.host_u8(cache[last:]), cache0[last:])
     del gathered, cache0, values, out, cache
     n1 = 4 * n_s
     g1, o1, c1, _ = _decode_case(gu, orc, 1, n1, B, [False], 99 + n_s % 8)
@@ -406,6 +432,72 @@ def test_decode_unaligned_and_bad_shards(gu, orc, B):
     assert ws.error() & ciera.DEVERR_FORMAT
 
 
+@pytest.mark.parametrize("B", [1, 64, 512])
+def test_decode_respects_buffer_length(gu, orc, B):
+    """The decoding calls read nothing past the length the caller gives.
+    A valid copy of shard 2 sits in the allocation just past that length, so
+    a missing check would read mapped memory and decode it: the test sees
+    that as an untouched shard that changed. Each case: shard 2 is skipped
+    with CIERA_DEVERR_BOUNDS (its values and cache untouched) and the other
+    shards decode as the oracle does."""
+    from paper_2609_04609_amd import ciera
+    R, n_s = 3, 5003
+    gathered, offs, cache0, values = _decode_case(gu, orc, R, n_s, B,
+                                                  [False, True, False], 777)
+    cache_o = cache0.copy()
+    expect = orc.decode_gathered(gathered, offs, n_s, cache_o)
+    L = gathered.size  # a multiple of 16
+    enc2 = gathered[int(offs[2]):]
+    big = gu.dev_u8(np.concatenate([gathered, enc2]))
+    ws = ciera.Workspace(n_s, R, B)
+    moved = offs.copy()
+    moved[2] = L  # the copy past the buffer's end
+    cases = [
+        ("offset at the end", moved, L),
+        ("header inside, total outside", moved, L + 64),
+        ("total runs 16 bytes past", offs, L - 16),
+    ]
+    for name, o_h, nbytes in cases:
+        o = torch.from_numpy(o_h.view(np.int64)).to("cuda")
+        out = torch.full((R * n_s,), 7, dtype=torch.int16, device="cuda")
+        cache = gu.dev_u8(cache0)
+        ciera.decode_gathered_t(big, o, n_s, B, out, cache, ws, nbytes=nbytes)
+        torch.cuda.synchronize()
+        assert ws.error() == ciera.DEVERR_BOUNDS, name
+        got, gc = gu.host_u16(out), gu.host_u8(cache)
+        np.testing.assert_array_equal(got[:2 * n_s], expect[:2 * n_s],
+                                      err_msg=name)
+        np.testing.assert_array_equal(gc[:2 * n_s], cache_o[:2 * n_s],
+                                      err_msg=name)
+        assert np.all(got[2 * n_s:] == 7), name
+        np.testing.assert_array_equal(gc[2 * n_s:], cache0[2 * n_s:],
+                                      err_msg=name)
+    # the exact length: everything decodes, no error
+    o = torch.from_numpy(moved.view(np.int64)).to("cuda")
+    out = torch.empty(R * n_s, dtype=torch.int16, device="cuda")
+    cache = gu.dev_u8(cache0)
+    ciera.decode_gathered_t(big, o, n_s, B, out, cache, ws,
+                            nbytes=L + enc2.size)
+    torch.cuda.synchronize()
+    assert ws.error() == 0
+    np.testing.assert_array_equal(gu.host_u16(out), expect)
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o)
+    # the stand-alone cache update with a short length leaves the cache alone
+    one = gu.dev_u8(enc2)
+    c2 = cache0[2 * n_s:]
+    for nbytes in (enc2.size - 16, 63, 0):
+        cache = gu.dev_u8(c2)
+        ciera.update_cache_t(cache, one, n_s, B, ws, nbytes=nbytes)
+        torch.cuda.synchronize()
+        assert ws.error() == ciera.DEVERR_BOUNDS, nbytes
+        np.testing.assert_array_equal(gu.host_u8(cache), c2)
+    cache = gu.dev_u8(c2)
+    ciera.update_cache_t(cache, one, n_s, B, ws)
+    torch.cuda.synchronize()
+    assert ws.error() == 0
+    np.testing.assert_array_equal(gu.host_u8(cache), cache_o[2 * n_s:])
+
+
 @pytest.mark.parametrize("B", [1, 512])
 def test_round_trip_chain_on_gpu(gu, orc, B):
     """T iterations of encode -> gather -> decode entirely on the GPU: every
@@ -448,7 +540,8 @@ def test_round_trip_chain_on_gpu(gu, orc, B):
     assert ws_e.error() == 0 and ws_d.error() == 0
 
 
-@pytest.mark.parametrize("B", [1, 16, 512, 4096])
+@pytest.mark.parametrize("B", [1, 16, 32, 64, 128, 256, 512, 1024, 2048,
+                               4096])
 def test_encode_with_cache_update(gu, orc, B):
     """CIERA_ENC_UPDATE_CACHE: the same bytes as the pure encode, and the
     cache afterwards equals the oracle's update of it from those bytes (the

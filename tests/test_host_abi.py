@@ -108,11 +108,13 @@ def test_host_argument_checks(cl):
     # fp16 needs B >= 16 (encode, decode, cache update, bound)
     assert cl.ciera_encode(fake, fake, 1000, 1, cl.FP16, fake, 1 << 20, 0,
                            fake, ws_bytes, 0) == cl.EUNSUPPORTED
-    assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 1, fake, fake, fake,
-                                    ws_bytes, 0, cl.FP16) == cl.EUNSUPPORTED
-    assert cl.ciera_update_cache(fake, fake, 1000, 1, fake, ws_bytes, 0,
+    MB = 1 << 20  # buffer length of the decoding calls
+    assert cl.ciera_decode_gathered(fake, MB, fake, 4, 1000, 1, fake, fake,
+                                    fake, ws_bytes, 0,
+                                    cl.FP16) == cl.EUNSUPPORTED
+    assert cl.ciera_update_cache(fake, fake, MB, 1000, 1, fake, ws_bytes, 0,
                                  cl.FP16) == cl.EUNSUPPORTED
-    assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 512, fake, fake,
+    assert cl.ciera_decode_gathered(fake, MB, fake, 4, 1000, 512, fake, fake,
                                     fake, ws_bytes, 0, 0x80000000) == cl.EINVAL
     assert cl.ciera_encoded_bound(1000, 1, cl.FP16) == 0
     assert cl.ciera_encoded_bound(1000, 512, 0x80000000) == 0
@@ -127,15 +129,15 @@ def test_host_argument_checks(cl):
     assert cl.ciera_encode(fake, fake, 1000, 512, 0, fake, bound, 0, fake,
                            256, 0) == cl.ENOSPC
     # decode: zero shards, null offsets, unaligned gathered buffer
-    assert cl.ciera_decode_gathered(fake, fake, 0, 1000, 512, fake, fake, fake,
-                                    ws_bytes, 0) == cl.EINVAL
-    assert cl.ciera_decode_gathered(fake, 0, 4, 1000, 512, fake, fake, fake,
-                                    ws_bytes, 0) == cl.EINVAL
-    assert cl.ciera_decode_gathered(fake + 4, fake, 4, 1000, 512, fake, fake,
+    assert cl.ciera_decode_gathered(fake, MB, fake, 0, 1000, 512, fake, fake,
                                     fake, ws_bytes, 0) == cl.EINVAL
-    assert cl.ciera_decode_gathered(fake, fake, 4, 1000, 3, fake, fake, fake,
-                                    ws_bytes, 0) == cl.EUNSUPPORTED
-    assert cl.ciera_update_cache(0, fake, 1000, 512, fake, ws_bytes,
+    assert cl.ciera_decode_gathered(fake, MB, 0, 4, 1000, 512, fake, fake,
+                                    fake, ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_decode_gathered(fake + 4, MB, fake, 4, 1000, 512, fake,
+                                    fake, fake, ws_bytes, 0) == cl.EINVAL
+    assert cl.ciera_decode_gathered(fake, MB, fake, 4, 1000, 3, fake, fake,
+                                    fake, ws_bytes, 0) == cl.EUNSUPPORTED
+    assert cl.ciera_update_cache(0, fake, MB, 1000, 512, fake, ws_bytes,
                                  0) == cl.EINVAL
     assert cl.ciera_workspace_init(0, 1024, 0) == cl.EINVAL
     # block hash: B = 1 and unsupported B, null / misaligned hash arrays
