@@ -192,6 +192,34 @@ int ciera_decode_gathered(const void *gathered, uint64_t gathered_bytes,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream);
 
+/* ciera_decode_gathered for callers that cannot allocate device memory or
+ * bring a workspace: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation. Same arguments, work and results as
+ * ciera_decode_gathered, except:
+ *   - no workspace: the decode's per-tile offsets live in a library-owned
+ *     device array of CIERA_NOALLOC_SCRATCH_BYTES (4 MiB) per GPU, held
+ *     until the process ends. It must hold 16 ceil((ceil(shard_elems /
+ *     16384) + 1) / 4) bytes per shard (128 shards of up to about 134M
+ *     values), else CIERA_ENOSPC with nothing enqueued;
+ *   - `err` (device u32, 4-byte aligned) receives this call's device error
+ *     bits (CIERA_DEVERR_*): the call zeroes it first, on `stream`;
+ *   - rANS-coded shards (mode 2) are not decoded: they set
+ *     CIERA_DEVERR_NOSPACE and are skipped.
+ * Nothing is allocated or freed, and there is no memset node: the call
+ * enqueues a fill kernel and the decode kernels. Every call on one GPU shares
+ * that GPU's array, so calls that overlap in time on one GPU (other streams,
+ * other threads) race and give unspecified results; serialise them. Call it
+ * with the stream's device current: the array's address is looked up for the
+ * current device on its first call there. */
+#define CIERA_NOALLOC_SCRATCH_BYTES (4u << 20)
+int ciera_decode_gathered_noalloc(const void *gathered,
+                                  uint64_t gathered_bytes,
+                                  const uint64_t *shard_offsets,
+                                  uint32_t nshards, uint64_t shard_elems,
+                                  uint32_t block_elems, uint32_t flags,
+                                  uint16_t *out, uint8_t *exp_cache,
+                                  uint32_t *err, hipStream_t stream);
+
 /* Entropy coding of the exception section (Section 3.1: the changed
  * exponents travel ANS-coded), in place on an encoded shard of n values at
  * block size B >= 16: when the rANS-coded section (format above) is smaller

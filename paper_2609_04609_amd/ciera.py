@@ -59,6 +59,9 @@ _SIGS = {
                                      _vp, _vp, _vp, _u64, _vp]),
     "ciera_update_cache": (_i32, [_vp, _vp, _u64, _u64, _u32, _u32, _vp, _u64,
                                   _vp]),
+    "ciera_decode_gathered_noalloc": (_i32, [_vp, _u64, _vp, _u32, _u64,
+                                             _u32, _u32, _vp, _vp, _vp,
+                                             _vp]),
     "ciera_ans_code": (_i32, [_vp, _u64, _u32, _vp, _vp, _u64, _vp]),
     "ciera_hash_blocks": (_i32, [_vp, _u64, _u32, _vp, _vp]),
     "ciera_encode_hashed": (_i32, [_vp, _vp, _vp, _u64, _u32, _vp, _u64, _vp,
@@ -134,6 +137,15 @@ def ciera_decode_gathered(gathered, gathered_bytes, shard_offsets, nshards,
                                        shard_offsets, nshards, shard_elems,
                                        block_elems, flags, out, exp_cache,
                                        workspace, workspace_bytes, stream)
+
+
+def ciera_decode_gathered_noalloc(gathered, gathered_bytes, shard_offsets,
+                                  nshards, shard_elems, block_elems, out,
+                                  exp_cache, err, stream, flags=0):
+    """The C call of the same name; `flags` (0 or FP16) comes last here."""
+    return lib().ciera_decode_gathered_noalloc(
+        gathered, gathered_bytes, shard_offsets, nshards, shard_elems,
+        block_elems, flags, out, exp_cache, err, stream)
 
 
 def ciera_update_cache(exp_cache, encoded, encoded_bytes, n_elems,
@@ -269,6 +281,17 @@ def decode_gathered_t(gathered, offsets, shard_elems, block_elems, out, cache,
                                block_elems, _ptr(out), _ptr(cache), ws.ptr,
                                ws.nbytes, _stream(), FP16 if fp16 else 0)
     return _check("ciera_decode_gathered", rc)
+
+
+def decode_gathered_noalloc_t(gathered, offsets, shard_elems, block_elems,
+                              out, cache, err, fp16=False, nbytes=None):
+    """decode_gathered_t without a workspace; ``err`` is a one-element int32
+    device tensor that receives the call's device error bits."""
+    rc = ciera_decode_gathered_noalloc(
+        _ptr(gathered), _nbytes(gathered, nbytes), _ptr(offsets),
+        offsets.numel(), shard_elems, block_elems, _ptr(out), _ptr(cache),
+        _ptr(err), _stream(), FP16 if fp16 else 0)
+    return _check("ciera_decode_gathered_noalloc", rc)
 
 
 def update_cache_t(cache, encoded, n_elems, block_elems, ws, fp16=False,

@@ -31,9 +31,12 @@ namespace {
 
 constexpr int kWaves = kThreads / 64;
 
-__device__ __forceinline__ void set_err(WsCtl *ctl, uint32_t bits) {
-  __hip_atomic_fetch_or(&ctl->err, bits, __ATOMIC_RELAXED,
+__device__ __forceinline__ void set_err(uint32_t *err, uint32_t bits) {
+  __hip_atomic_fetch_or(err, bits, __ATOMIC_RELAXED,
                         __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void set_err(WsCtl *ctl, uint32_t bits) {
+  set_err(&ctl->err, bits);
 }
 
 __device__ __forceinline__ uint32_t ld32(const uint8_t *p) {
@@ -398,7 +401,7 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   s_cum[tid] = cum;
   ok = ok && total == kAnsM;
   if (!ok) {
-    if (blockIdx.x == 0 && tid == 0) set_err(a.ctl, CIERA_DEVERR_FORMAT);
+    if (blockIdx.x == 0 && tid == 0) set_err(a.err, CIERA_DEVERR_FORMAT);
     return;
   }
   __syncthreads();
@@ -421,7 +424,7 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
     const uint32_t end = ends[c];
     if (!(start <= end && end <= avail && ((start | end) & 3u) == 0 &&
           end - start >= 256u && end - start <= kAnsStreamMax)) {
-      if (lane == 0) set_err(a.ctl, CIERA_DEVERR_FORMAT);
+      if (lane == 0) set_err(a.err, CIERA_DEVERR_FORMAT);
       continue;
     }
     const uint8_t *st = streams + start;
@@ -487,7 +490,7 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
     else if (rd < nwords &&
              reinterpret_cast<const uint16_t *>(wsrc)[rd] != 0)
       bad = true;
-    if (__ballot(bad) != 0ull && lane == 0) set_err(a.ctl, CIERA_DEVERR_FORMAT);
+    if (__ballot(bad) != 0ull && lane == 0) set_err(a.err, CIERA_DEVERR_FORMAT);
   }
 }
 

@@ -3,10 +3,19 @@
 // include/ciera.h.
 #include <stdint.h>
 
-#include <hip/hip_runtime_api.h>
+#include <mutex>
+
+#include <hip/hip_runtime.h>
 
 #include "ciera.h"
 #include "ciera_internal.h"
+
+// Scratch of ciera_decode_gathered_noalloc: the per-tile offsets of the
+// decode, in a file-scope device array instead of a workspace. Every GPU the
+// library runs on holds its own copy until the process ends. In host code
+// this name is a stand-in, not a device address: kernels get the address
+// that hipGetSymbolAddress returns for the current device (noalloc_scratch).
+static __device__ __align__(256) uint8_t scratch[CIERA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -22,6 +31,29 @@ int log2_block(uint32_t B) {
 
 bool aligned(const void *p, uintptr_t a) {
   return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+// The device address of `scratch` on the current device. hipGetSymbolAddress
+// runs once per device, with that device current, on its first call there;
+// later calls reuse the address.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+hipError_t noalloc_scratch(void **p) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *q = nullptr;
+    e = hipGetSymbolAddress(&q, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = q;
+  }
+  *p = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 // Bitmap bytes re-read per call past which a separate scan pays for its
@@ -247,44 +279,66 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
                            workspace_bytes, stream, true, false);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Host checks shared by both gathered decodes, and the DecArgs they fill
+// (everything but the error word, the tile offsets and the rANS lists).
+int decode_args(const void *gathered, uint64_t gathered_bytes,
+                const uint64_t *shard_offsets, uint32_t nshards,
+                uint64_t shard_elems, uint32_t block_elems, uint32_t flags,
+                uint16_t *out, uint8_t *exp_cache, DecArgs *a, bool *vec) {
+  const int l = log2_block(block_elems);
+  if (l < 0) return CIERA_EUNSUPPORTED;
+  if (flags & ~CIERA_FP16) return CIERA_EINVAL;
+  const bool f16 = flags & CIERA_FP16;
+  if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
+  if (!gathered || !shard_offsets || !out || !exp_cache) return CIERA_EINVAL;
+  if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
+  if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
+  if (!aligned(gathered, 16)) return CIERA_EINVAL;
+  *a = DecArgs{};
+  a->gathered = static_cast<const uint8_t *>(gathered);
+  a->bytes = gathered_bytes;
+  a->offsets = shard_offsets;
+  a->n = shard_elems;
+  a->log2B = uint32_t(l);
+  a->nshards = nshards;
+  a->out = out;
+  a->cache = exp_cache;
+  a->ans_stride = pad16(shard_elems);
+  a->f16 = f16;
+  a->prefix_pass = use_prefix_pass(shard_elems, nshards, l);
+  a->xcd_run_log2 = a->prefix_pass ? kXcdRunLog2 : 0u;
+  *vec = (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
+  return CIERA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int ciera_decode_gathered(const void *gathered, uint64_t gathered_bytes,
                           const uint64_t *shard_offsets,
                           uint32_t nshards, uint64_t shard_elems,
                           uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream) {
-  const int l = log2_block(block_elems);
-  if (l < 0) return CIERA_EUNSUPPORTED;
-  if (flags & ~CIERA_FP16) return CIERA_EINVAL;
-  const bool f16 = flags & CIERA_FP16;
-  if (f16 && l < kF16MinLog2B) return CIERA_EUNSUPPORTED;
-  if (!gathered || !shard_offsets || !out || !exp_cache || !workspace)
-    return CIERA_EINVAL;
-  if (nshards == 0 || nshards > 65535) return CIERA_EINVAL;
-  if (shard_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
-  if (!aligned(gathered, 16) || !aligned(workspace, 16)) return CIERA_EINVAL;
+  DecArgs a;
+  bool vec = false;
+  const int rc = decode_args(gathered, gathered_bytes, shard_offsets, nshards,
+                             shard_elems, block_elems, flags, out, exp_cache,
+                             &a, &vec);
+  if (rc != CIERA_OK) return rc;
+  if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
   if (!dec_workspace_ok(shard_elems, nshards, workspace_bytes))
     return CIERA_ENOSPC;
-  DecArgs a{};
-  a.gathered = static_cast<const uint8_t *>(gathered);
-  a.bytes = gathered_bytes;
-  a.offsets = shard_offsets;
-  a.n = shard_elems;
-  a.log2B = uint32_t(l);
-  a.nshards = nshards;
-  a.out = out;
-  a.cache = exp_cache;
-  a.ctl = static_cast<WsCtl *>(workspace);
+  a.err = &static_cast<WsCtl *>(workspace)->err;
   a.tile_excl = tile_excl_of(workspace);
-  a.ans_exc = f16 ? nullptr
-                  : ans_lists_of(workspace, workspace_bytes, shard_elems,
-                                 nshards, l);
-  a.ans_stride = pad16(shard_elems);
-  a.f16 = f16;
-  a.prefix_pass = use_prefix_pass(shard_elems, nshards, l);
-  a.xcd_run_log2 = a.prefix_pass ? kXcdRunLog2 : 0u;
-  const bool vec =
-      (shard_elems % 8 == 0) && aligned(out, 16) && aligned(exp_cache, 8);
+  a.ans_exc = a.f16 ? nullptr
+                    : ans_lists_of(workspace, workspace_bytes, shard_elems,
+                                   nshards, int(a.log2B));
   if (launch_ans_decode(a, stream) != hipSuccess) return CIERA_EHIP;
   return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
@@ -312,7 +366,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
   a.nshards = 1;
   a.out = nullptr;
   a.cache = exp_cache;
-  a.ctl = static_cast<WsCtl *>(workspace);
+  a.err = &static_cast<WsCtl *>(workspace)->err;
   a.tile_excl = tile_excl_of(workspace);
   a.ans_exc =
       f16 ? nullptr : ans_lists_of(workspace, workspace_bytes, n_elems, 1, l);
@@ -353,6 +407,36 @@ int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
   p += 256 * kmax;
   a.words = reinterpret_cast<uint16_t *>(p);
   return launch_ans_code(a, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
+}
+
+
+int ciera_decode_gathered_noalloc(const void *gathered,
+                                  uint64_t gathered_bytes,
+                                  const uint64_t *shard_offsets,
+                                  uint32_t nshards, uint64_t shard_elems,
+                                  uint32_t block_elems, uint32_t flags,
+                                  uint16_t *out, uint8_t *exp_cache,
+                                  uint32_t *err, hipStream_t stream) {
+  DecArgs a;
+  bool vec = false;
+  const int rc = decode_args(gathered, gathered_bytes, shard_offsets, nshards,
+                             shard_elems, block_elems, flags, out, exp_cache,
+                             &a, &vec);
+  if (rc != CIERA_OK) return rc;
+  if (!err || !aligned(err, 4)) return CIERA_EINVAL;
+  // the tile offsets of every shard must fit in the scratch
+  if (uint64_t(nshards) * dec_count_stride(dec_tiles(shard_elems)) * 4 >
+      uint64_t(CIERA_NOALLOC_SCRATCH_BYTES))
+    return CIERA_ENOSPC;
+  void *sp = nullptr;
+  if (noalloc_scratch(&sp) != hipSuccess) return CIERA_EHIP;
+  // the caller's word receives this call's errors only
+  if (launch_fill_zero(err, sizeof(uint32_t), stream) != hipSuccess)
+    return CIERA_EHIP;
+  a.err = err;
+  a.tile_excl = static_cast<uint32_t *>(sp);
+  a.ans_exc = nullptr;  // no room for decoded rANS lists: NOSPACE
+  return launch_decode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }
 
 }  // extern "C"

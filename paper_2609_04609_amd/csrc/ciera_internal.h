@@ -139,7 +139,7 @@ struct DecArgs {
   uint32_t nshards;
   uint16_t *out;            // nullptr for the cache-update-only pass
   uint8_t *cache;
-  WsCtl *ctl;
+  uint32_t *err;            // sticky device error bits (CIERA_DEVERR_*)
   // per shard and decode tile: the flagged blocks (B >= 16) or changed values
   // (B = 1) in front of the tile, dec_count_stride(tiles) words per shard
   uint32_t *tile_excl;

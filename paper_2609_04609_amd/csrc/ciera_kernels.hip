@@ -251,9 +251,12 @@ __device__ __forceinline__ void set_octet_byte(uint2 &v, uint32_t i,
     v.y = (v.y & ~(0xFFu << sh)) | (b << sh);
 }
 
-__device__ __forceinline__ void set_error(WsCtl *ctl, uint32_t bits) {
-  __hip_atomic_fetch_or(&ctl->err, bits, __ATOMIC_RELAXED,
+__device__ __forceinline__ void set_error(uint32_t *err, uint32_t bits) {
+  __hip_atomic_fetch_or(err, bits, __ATOMIC_RELAXED,
                         __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void set_error(WsCtl *ctl, uint32_t bits) {
+  set_error(&ctl->err, bits);
 }
 
 __device__ __forceinline__ void put_header(uint8_t *out, uint32_t mode,
@@ -1166,11 +1169,11 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
   v.mode = 0;
   v.E = 0;
   if (off & 15ull) {
-    if (report) set_error(a.ctl, CIERA_DEVERR_ALIGN);
+    if (report) set_error(a.err, CIERA_DEVERR_ALIGN);
     return v;
   }
   if (off > a.bytes || a.bytes - off < kHeaderBytes) {
-    if (report) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+    if (report) set_error(a.err, CIERA_DEVERR_BOUNDS);
     return v;
   }
   const uint32_t *h32 = reinterpret_cast<const uint32_t *>(v.enc);
@@ -1194,7 +1197,7 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
          htotal == kHeaderBytes + pad16(hn) + pad16(bm) +
                        pad16(hP - hn - bm);
     if (ok && a.ans_exc == nullptr) {
-      if (report) set_error(a.ctl, CIERA_DEVERR_NOSPACE);
+      if (report) set_error(a.err, CIERA_DEVERR_NOSPACE);
       return v;
     }
   } else if (ok && mode == kModeRaw) {
@@ -1203,11 +1206,11 @@ __device__ __forceinline__ ShardView read_shard(const DecArgs &a, uint32_t j,
     ok = false;
   }
   if (!ok) {
-    if (report) set_error(a.ctl, CIERA_DEVERR_FORMAT);
+    if (report) set_error(a.err, CIERA_DEVERR_FORMAT);
     return v;
   }
   if (htotal > a.bytes - off) {
-    if (report) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+    if (report) set_error(a.err, CIERA_DEVERR_BOUNDS);
     return v;
   }
   v.ok = true;
@@ -1567,7 +1570,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
       }
     }
   }
-  if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+  if (bad) set_error(a.err, CIERA_DEVERR_BOUNDS);
 }
 
 // ============================================== element exceptions (B = 1) ==
@@ -1735,7 +1738,7 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
         store_w8<VEC>(out + elem, wv, valid);
     }
   }
-  if (bad) set_error(a.ctl, CIERA_DEVERR_BOUNDS);
+  if (bad) set_error(a.err, CIERA_DEVERR_BOUNDS);
 }
 
 __global__ void fill_zero_kernel(uint32_t *p, uint64_t words) {

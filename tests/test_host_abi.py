@@ -139,6 +139,25 @@ def test_host_argument_checks(cl):
                                     fake, ws_bytes, 0) == cl.EUNSUPPORTED
     assert cl.ciera_update_cache(0, fake, MB, 1000, 512, fake, ws_bytes,
                                  0) == cl.EINVAL
+    # the decode without a workspace: a null or misaligned error word, and
+    # tile offsets that would not fit its 4 MiB scratch (16 bytes per 4
+    # decode tiles of 16384 values, counting one more tile per shard) are
+    # refused before any HIP call
+    nd = cl.ciera_decode_gathered_noalloc
+    assert nd(fake, MB, fake, 4, 1000, 512, fake, fake, 0, 0) == cl.EINVAL
+    assert nd(fake, MB, fake, 4, 1000, 512, fake, fake, fake + 2,
+              0) == cl.EINVAL
+    assert nd(fake, MB, fake, 4, 1000, 3, fake, fake, fake,
+              0) == cl.EUNSUPPORTED
+    assert nd(fake, MB, fake, 0, 1000, 512, fake, fake, fake,
+              0) == cl.EINVAL
+    # 256 shards of 4095 tiles fill the scratch exactly; one value more per
+    # shard needs a 4096th tile and 4 more words per shard
+    assert 256 * 4096 * 4 == 4 << 20
+    assert nd(fake, MB, fake, 256, 4095 * 16384 + 1, 512, fake, fake, fake,
+              0) == cl.ENOSPC
+    assert nd(fake, MB, fake, 16, (1 << 32) - 1, 1, fake, fake, fake,
+              0) == cl.ENOSPC
     assert cl.ciera_workspace_init(0, 1024, 0) == cl.EINVAL
     # block hash: B = 1 and unsupported B, null / misaligned hash arrays
     assert cl.ciera_hash_blocks(fake, 1000, 1, fake, 0) == cl.EUNSUPPORTED
