@@ -112,12 +112,15 @@ __device__ __forceinline__ uint2 unplane(const uint8_t *g) {
 
 // ---------------------------------------------------- streaming accesses --
 // Bytes that a call reads or writes once (the sign|mantissa plane, the
-// exception list, the decoded values, the cache bytes a pass compares) go
-// through non-temporal loads and stores (the nt bit), so that they do not
-// push out what is read again: the bitmap words every decode tile counts in
-// front of it, and the W' lines the exception pass of the encode re-reads
-// (pass 1 loads W' normally for that reason). Measured on the codec step of
-// the OLMoE layer: decode 316 -> 279 us, encode 39 -> 32 us.
+// exception list, the decoded values and the merge's cache patches, W' or
+// the cache bytes pass 1 compares, whichever the exception pass does not
+// read again) go through non-temporal loads and stores (the nt bit), so
+// that they neither push out what is read again (the bitmap words every
+// decode tile counts in front of it, what the exception pass re-reads) nor
+// leave dirty lines in the Infinity Cache for the next kernel to write back.
+// Plain stores of the merge's cache patches, for one, left up to 256 MB of
+// them behind a DeepSeek-style decode: the encode after it took 131 instead
+// of 84 us.
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -328,7 +331,12 @@ __device__ __forceinline__ uint64_t sm64_mix(uint64_t z) {
 enum : int { kDetExact = 0, kDetHash = 1, kDetHashOnly = 2 };
 
 // Pass 1. Everything but the exception list.
-template <bool VEC, bool ELEMS, int DET, bool F16 = false>
+// NTW (the fused cache update): the exception pass takes the changed
+// exponents from the cache brought forward here, so W' is read once and its
+// loads are non-temporal, while the cache bytes are loaded plainly for the
+// exception pass to find again. Without it the exception pass re-reads W'
+// and the cache is read once: the other way round.
+template <bool VEC, bool ELEMS, int DET, bool F16 = false, bool NTW = false>
 __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   constexpr bool HASH = DET != kDetExact;
   constexpr bool OUT = DET != kDetHashOnly;
@@ -494,12 +502,15 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
       uint2 cv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u)
-        wv[u] = *reinterpret_cast<const uint4 *>(
-            a.w + cbase + (uint64_t(u) * 64 + lane) * 8);
+        wv[u] = NTW ? ld_nt16(a.w + cbase + (uint64_t(u) * 64 + lane) * 8)
+                    : *reinterpret_cast<const uint4 *>(
+                          a.w + cbase + (uint64_t(u) * 64 + lane) * 8);
       if (!HASH) {
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-          cv[u] = ld_nt8(a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
+          cv[u] = NTW ? *reinterpret_cast<const uint2 *>(
+                            a.cache + cbase + (uint64_t(u) * 64 + lane) * 8)
+                      : ld_nt8(a.cache + cbase + (uint64_t(u) * 64 + lane) * 8);
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -1515,7 +1526,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
 #pragma unroll
     for (int u = 0; u < OCT; ++u) {
       const uint64_t elem = base + (uint64_t(wave * OCT + u) * 64u + lane) * 8u;
-      if (ch[u]) *reinterpret_cast<uint2 *>(cache + elem) = ev[u];
+      if (ch[u]) {
+        if (UPDATE_ONLY)
+          *reinterpret_cast<uint2 *>(cache + elem) = ev[u];
+        else  // the merge's patches: non-temporal, like its other streams
+          st_nt8(cache + elem, ev[u]);
+      }
       if (!UPDATE_ONLY) {
         uint4 wv;
         if (F16) {
@@ -1726,7 +1742,10 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
         set_octet_byte(ev[u], i, exc[pos++]);
         m &= m - 1u;
       }
-      store_b8<VEC>(cache + elem, ev[u], valid);
+      if (!UPDATE_ONLY && full)
+        st_nt8(cache + elem, ev[u]);
+      else
+        store_b8<VEC>(cache + elem, ev[u], valid);
     }
     if (!UPDATE_ONLY) {
       uint4 wv;
@@ -1776,20 +1795,24 @@ void launch_exc(dim3 grid, const EncArgs &a, bool vec, bool f16, bool fromc,
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
   const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
   const bool elems = a.log2B == 0;
+  // with the fused cache update the exception pass reads the cache, not W'
+  const bool fromc = a.cache_out != nullptr;
+  auto exact = [&](auto v, auto e, auto f) {
+    constexpr bool V = decltype(v)::value, E = decltype(e)::value,
+                   F = decltype(f)::value;
+    if (fromc)
+      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, true>), grid,
+                         block, 0, s, a);
+    else
+      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, false>),
+                         grid, block, 0, s, a);
+  };
   if (elems) {
-    if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, true, kDetExact>), grid,
-                         block, 0, s, a);
-    else
-      hipLaunchKernelGGL((encode_pass_kernel<false, true, kDetExact>), grid,
-                         block, 0, s, a);
+    if (vec) exact(bool_c<true>{}, bool_c<true>{}, bool_c<false>{});
+    else exact(bool_c<false>{}, bool_c<true>{}, bool_c<false>{});
   } else if (a.f16) {
-    if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetExact, true>),
-                         grid, block, 0, s, a);
-    else
-      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetExact, true>),
-                         grid, block, 0, s, a);
+    if (vec) exact(bool_c<true>{}, bool_c<false>{}, bool_c<true>{});
+    else exact(bool_c<false>{}, bool_c<false>{}, bool_c<true>{});
   } else if (a.hashed) {
     if (vec)
       hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHash>), grid,
@@ -1798,18 +1821,12 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
       hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHash>), grid,
                          block, 0, s, a);
   } else {
-    if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetExact>), grid,
-                         block, 0, s, a);
-    else
-      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetExact>), grid,
-                         block, 0, s, a);
+    if (vec) exact(bool_c<true>{}, bool_c<false>{}, bool_c<false>{});
+    else exact(bool_c<false>{}, bool_c<false>{}, bool_c<false>{});
   }
   if (elems || a.scan_prefix)
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
-  // the exception pass reads the updated cache when pass 1 brought it forward
-  const bool fromc = a.cache_out != nullptr;
   if (elems) {
     launch_exc<true>(grid, a, vec, false, fromc, s, [](auto v, auto, auto c) {
       return encode_exc_elems_kernel<decltype(v)::value, decltype(c)::value>;

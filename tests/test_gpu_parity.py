@@ -373,6 +373,68 @@ def test_decode_with_prefix_pass(gu, orc, n_s):
     assert ws1.error() == 0
 
 
+@pytest.mark.parametrize("B,fp16", [(64, False), (512, True), (1, False)])
+def test_decode_caches_past_1gib(gu, orc, B, fp16):
+    """17 shards of 67,108,864 values: 1.14 GB of caches, past the size
+    where the merge writes its cache patches with non-temporal stores. Every
+    shard is encoded by the oracle and its decoded values and updated cache
+    are compared with the oracle's, shard by shard on the host."""
+    import concurrent.futures as cf
+    import os
+    from paper_2609_04609_amd import ciera, synth
+    R, n = 17, 1 << 26
+    enc_o = orc.encode_f16 if fp16 else orc.encode
+    split = orc.split_f16 if fp16 else orc.split
+    dec_o = orc.decode_f16 if fp16 else orc.decode
+
+    def shard(j):
+        if fp16:
+            w = synth.normal_f16_bits(n, 0.02, 4100 + j, "cuda")
+            w2 = synth.forced_bernoulli_f16_bits(w, 0.001, 4200 + j)
+        else:
+            w, w2 = gu.pair(n, 4100 + 2 * j, c=0.001)
+        return gu.host_u16(w), gu.host_u16(w2)
+
+    def encode(j):
+        wh, w2h = shard(j)
+        c = split(wh)[0]
+        return enc_o(w2h, c, B), c, w2h
+
+    workers = max(1, min(8, os.cpu_count() or 1))
+    with cf.ThreadPoolExecutor(workers) as ex:
+        parts = list(ex.map(encode, range(R)))
+    encs = [p[0] for p in parts]
+    gathered, offs = gu.gather(encs)
+    cache = torch.empty(R * n, dtype=torch.uint8, device="cuda")
+    for j, (_, c, _) in enumerate(parts):
+        cache[j * n:(j + 1) * n].copy_(torch.from_numpy(c))
+    out = torch.empty(R * n, dtype=torch.int16, device="cuda")
+    ws = ciera.Workspace(n, R, B)
+    ciera.decode_gathered_t(gu.dev_u8(gathered),
+                            torch.from_numpy(offs.view(np.int64)).cuda(), n,
+                            B, out, cache, ws, fp16=fp16)
+    torch.cuda.synchronize()
+    assert ws.error() == 0
+    del gathered
+
+    def check(j):
+        enc, c, w2h = parts[j]
+        c_o = c.copy()
+        out_o = dec_o(enc, n, c_o)
+        sl = slice(j * n, (j + 1) * n)
+        if not np.array_equal(out_o, w2h):
+            return f"shard {j}: oracle round trip"
+        if not np.array_equal(gu.host_u16(out[sl]), out_o):
+            return f"shard {j}: values"
+        if not np.array_equal(gu.host_u8(cache[sl]), c_o):
+            return f"shard {j}: cache"
+        return None
+
+    with cf.ThreadPoolExecutor(workers) as ex:
+        errs = [e for e in ex.map(check, range(R)) if e]
+    assert not errs, errs
+
+
 @pytest.mark.parametrize("B", [1, 16, 512, 4096])
 def test_update_cache_matches_oracle(gu, orc, B):
     from paper_2609_04609_amd import ciera
