@@ -8,14 +8,22 @@ ranks sees it:
   3. ciera_decode_gathered over all R encoded shards placed back to back in
      one HBM buffer (the one-GPU stand-in for the Allgather output), which
      patches the R receiver caches and rebuilds every bf16 value.
-The stand-alone cache update (ciera_update_cache) is timed beside the step.
 Steps alternate between the update W -> W' and its reverse W' -> W, so every
 step changes the same set of exponents against caches that really hold the
 previous iteration's exponents, and the work per step is constant.
 
-Inputs are resident in HBM before timing starts. Per-kernel times come from
-HIP events recorded on the stream the kernels run on. The CPU oracle is timed
-on the host cores as a reported baseline (same input bytes).
+The headline workload is the DeepSeek-V3-style MoE layer (256 experts, 128
+shards of 88,080,384 values, 0.5% clustered exponent changes, B = 512), the
+largest configuration that fits one GPU. Beside it: the OLMoE layer (16
+shards of 25,165,824 values) at B = 512 and at B = 1, its fp16, block-hash,
+rANS and overlap variants, the small configurations and one layer of the
+mixed model step.
+
+Inputs are resident in HBM before timing starts. Phase times come from HIP
+events recorded on the stream the kernels run on: one before the encode and
+one between encode and decode, the decode ending at the next step's first
+event. The CPU oracle is timed on the host cores as a reported baseline, on
+the same bytes, streamed shard by shard.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--block B]
 """
@@ -36,28 +44,23 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, 8 TB/s
 COPY_CAL_BYTES = 1 << 30
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
                           "ciera_kernels.hip")
-# HBM bytes per decode launch measured with rocprofv3 FETCH_SIZE / WRITE_SIZE
-# (scaled by a 1 GiB copy), for the kernel source with this sha256; see
-# profiles/hbm_traffic_*.md. Reported only while the source is unchanged.
-_SRC_SHA = "494189aba3c4663f82e5f92dc1a890ca340e46551692eba66f31b9e6d7e13c70"
-MEASURED_TRAFFIC = {
-    ("olmoe_layer_c0.1", 512, "bf16"): (_SRC_SHA, 1780160205),
-    ("olmoe_layer_c0.1", 512, "fp16"): (_SRC_SHA, 1873777222),
-    # measured apart from the OLMoE figures, so it keeps its own source hash
-    ("dsv3_layer", 512, "bf16"): (
-        "494189aba3c4663f82e5f92dc1a890ca340e46551692eba66f31b9e6d7e13c70",
-        48950711623),
-}
+# HBM bytes per call measured with rocprofv3 FETCH_SIZE + WRITE_SIZE (each
+# scaled by what the counters read for a 1 GiB copy) for the kernel source
+# with this sha256; see profiles/hbm_traffic_*.md. Reported only while the
+# source is unchanged.
+MEASURED_TRAFFIC = {}
 
 
 def measured_traffic(name, B, dtype="bf16"):
+    """{"decode": bytes, "encode": bytes} of the current kernel source, or
+    None when no counter run covers it."""
     import hashlib
     rec = MEASURED_TRAFFIC.get((name, B, dtype))
     if rec is None:
         return None
     with open(KERNEL_SRC, "rb") as f:
         digest = hashlib.sha256(f.read()).hexdigest()
-    return rec[1] if digest == rec[0] else None
+    return rec if digest == rec["sha"] else None
 
 
 METRIC = ("encode & N-shard decode GB/s (bf16 weights), % HBM peak, "
@@ -179,54 +182,68 @@ class Setup:
         return g, off_t, totals
 
 
-def codec_steps(S, warmup, steps, stream):
+def timed_steps(S, warmup, steps, stream, decide=None, start=0):
     """The codec step on a Setup (rank 0's encode, bringing its cache
     forward, then the gathered decode; raw groups encode raw), alternating
-    W -> W' and back. Returns the mean encode and decode times and the wall
-    time per step (s); the last decode is checked bit for bit."""
+    W -> W' and back: step s goes W -> W' when s is even, so a sequence of
+    calls continues with start = the steps already run. `decide(s)` runs on
+    the host before step s (the Section 3.2 decision). Two events per step:
+    before the encode and
+    between encode and decode; the decode ends at the next step's first
+    event (or a last one). Returns per-step encode and decode times (us) and
+    the wall time per step (s). The last step's encoded bytes, decoded
+    values and caches are checked bit for bit."""
     import torch
     from paper_2609_04609_amd import ciera
     n, B = S.n, S.B
 
-    def one(s, e):
+    def one(s, e0, e1):
         even = (s % 2) == 0
         w_in = S.W2[:n] if even else S.W[:n]
         g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
-        if e:
-            e[0].record(stream)
+        if decide is not None:
+            decide(s)
+        if e0 is not None:
+            e0.record(stream)
         if S.raw:
             ciera.encode_t(w_in, None, B, S.ws_enc, S.tmp, raw=True)
         else:
             ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
                            update_cache=True)
-        if e:
-            e[1].record(stream)
+        if e1 is not None:
+            e1.record(stream)
         ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
-        if e:
-            e[2].record(stream)
 
     for s in range(warmup):
-        one(s, None)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
-           for _ in range(steps)]
+        one(start + s, None, None)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
-        one(warmup + s, evs[s])
+        one(start + warmup + s, ev[2 * s], ev[2 * s + 1])
+    ev[2 * steps].record(stream)
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
-    last_even = (warmup + steps - 1) % 2 == 0
+    last_even = (start + warmup + steps - 1) % 2 == 0
     expect = S.W2 if last_even else S.W
     ok = bool(torch.equal(S.out, expect))
     if not S.raw:
         g, t = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
         ok = ok and bool(torch.equal(S.cache[:n], S.send_cache)) and \
             bool(torch.equal(S.tmp[:t], g[:t]))
-    if not ok or S.ws_enc.error() or S.ws_dec.error():
-        raise RuntimeError("codec steps are not exact")
-    t_enc = float(np.mean([e[0].elapsed_time(e[1]) for e in evs])) / 1e3
-    t_dec = float(np.mean([e[1].elapsed_time(e[2]) for e in evs])) / 1e3
-    return t_enc, t_dec, wall
+    errs = S.ws_enc.error() | S.ws_dec.error()
+    if not ok or errs:
+        raise RuntimeError(f"codec steps are not exact (err={errs})")
+    enc = [ev[2 * k].elapsed_time(ev[2 * k + 1]) * 1e3 for k in range(steps)]
+    dec = [ev[2 * k + 1].elapsed_time(ev[2 * k + 2]) * 1e3
+           for k in range(steps)]
+    return enc, dec, wall
+
+
+def codec_steps(S, warmup, steps, stream):
+    """Mean encode and decode times and the wall time per step (s)."""
+    enc, dec, wall = timed_steps(S, warmup, steps, stream)
+    return float(np.mean(enc)) / 1e6, float(np.mean(dec)) / 1e6, wall
 
 
 def time_small_configs(B, dev, steps, stream):
@@ -583,7 +600,8 @@ def time_f16(wl, B, dev, steps, stream):
             "decode_hbm_gbps": round(alg_dec / t_dec / 1e9, 1),
             "decode_hbm_frac": round(alg_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
             "decode_alg_bytes": alg_dec,
-            "decode_traffic": measured_traffic(wl.name, B, "fp16"),
+            "decode_traffic": (measured_traffic(wl.name, B, "fp16") or
+                               {}).get("decode"),
             "exceptions_local": E0}
 
 
@@ -623,67 +641,183 @@ def time_overlap(S, layers, steps, cache_is_w2):
     return out
 
 
-def cpu_baseline(setup, min_s=10.0, max_s=30.0):
-    """The oracle on the host cores, on the same bytes as the GPU step:
-    encode of rank 0's shard (one thread), then decode of the R gathered
-    shards (one thread per shard, up to the host's 16-core share). The step is
-    repeated until at least min_s of wall time has been spent; for workloads
-    whose single step would exceed max_s, a subset of the shards is decoded
-    and the decode time is scaled to all R."""
+def cpu_baseline(S, budget_s=20.0):
+    """The oracle on the host cores, on the same bytes as the GPU step,
+    streamed shard by shard (each shard's inputs copied from the device and
+    its receiver cache split from W just before use): the encode of rank 0's
+    shard on one thread; the decode of gathered shards on one thread, shard
+    after shard, for about a third of the budget; and the decode of every
+    one of the R shards with one shard per thread on up to 16 cores (the
+    host's share on the GPU machine), in rounds of one shard per thread. The step
+    rate is encode + that all-core decode of all R shards."""
     import concurrent.futures as cf
     from oracle import oracle
     oracle.build(force=False)
-    n, R, B = setup.n, setup.R, setup.B
-    offs = setup.offA.cpu().numpy().view(np.uint64)
-    tot = setup.totA
+    n, R, B = S.n, S.R, S.B
+    offs = S.offA.cpu().numpy().view(np.uint64)
+    tot = S.totA
 
     def shard_inputs(j):
-        w = setup.W[j * n:(j + 1) * n].cpu().numpy().view(np.uint16)
-        enc = setup.gA[int(offs[j]):int(offs[j]) + tot[j]].cpu().numpy()
+        w = S.W[j * n:(j + 1) * n].cpu().numpy().view(np.uint16)
+        enc = S.gA[int(offs[j]):int(offs[j]) + tot[j]].cpu().numpy()
         return oracle.split(w)[0], enc
 
     cache0, enc0 = shard_inputs(0)
-    w2 = setup.W2[:n].cpu().numpy().view(np.uint16)
+    w2 = S.W2[:n].cpu().numpy().view(np.uint16)
+    t0 = time.perf_counter()
     enc = oracle.encode(w2, cache0, B)
+    t_enc = time.perf_counter() - t0
     if not np.array_equal(enc, enc0):
         raise RuntimeError("oracle and GPU encodings of shard 0 differ")
-    t0 = time.perf_counter()
-    out0 = oracle.decode(enc0, n, cache0.copy())
-    t_one = time.perf_counter() - t0
+    del enc
+    # one thread, shard after shard
+    t_1, k1 = 0.0, 0
+    while k1 == 0 or (t_1 < budget_s / 3 and k1 < R):
+        c, e = (cache0.copy(), enc0) if k1 == 0 else shard_inputs(k1)
+        t0 = time.perf_counter()
+        out = oracle.decode(e, n, c)
+        t_1 += time.perf_counter() - t0
+        if k1 == 0 and not np.array_equal(out, w2):
+            raise RuntimeError("oracle decode of shard 0 is not exact")
+        k1 += 1
+    del out, w2
     threads = max(1, min(16, os.cpu_count() or 1, R))
-    # shards decoded per step: all of them, unless one step would be too long
-    k = R
-    if t_one * R / threads > max_s / 2:
-        k = max(threads, int(max_s / 2 / t_one) * threads)
-        k = min(R, k)
-    inputs = [shard_inputs(j) for j in range(k)]
-
-    def dec(j):
-        c, e = inputs[j]
-        return oracle.decode(e, n, c.copy())
-
-    steps, t_enc, t_dec = 0, 0.0, 0.0
+    t_all, k_all = 0.0, 0
     with cf.ThreadPoolExecutor(threads) as ex:
-        while steps == 0 or (t_enc + t_dec < min_s and steps < 1000):
+        while k_all < R and (k_all == 0 or t_all < budget_s):
+            js = list(range(k_all, min(R, k_all + threads)))
+            inputs = list(ex.map(shard_inputs, js))
             t0 = time.perf_counter()
-            oracle.encode(w2, cache0, B)
-            t1 = time.perf_counter()
-            outs = list(ex.map(dec, range(k)))
-            t2 = time.perf_counter()
-            t_enc += t1 - t0
-            t_dec += t2 - t1
-            steps += 1
-    if not np.array_equal(outs[0], out0):
-        raise RuntimeError("oracle decode is not deterministic")
-    t_step = (t_enc + t_dec * (R / k)) / steps
-    gbps = (2 * n + 2 * R * n) / t_step / 1e9
-    return {"value": round(gbps, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle",
-            "sample": (f"{steps} steps of: encode of rank 0's shard "
-                       f"({n:,} values, 1 thread) + decode of {k} of {R} "
-                       f"gathered shards ({threads} threads); "
-                       f"{t_enc + t_dec:.1f} s in total, decode scaled to "
-                       f"{R} shards")}
+            list(ex.map(lambda ce: oracle.decode(ce[1], n, ce[0]), inputs))
+            t_all += time.perf_counter() - t0
+            k_all += len(js)
+            del inputs
+    t_step = t_enc + t_all * R / k_all
+    return {"value": round((2 * n + 2 * R * n) / t_step / 1e9, 4),
+            "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "encode_1thread_gbps": round(2 * n / t_enc / 1e9, 4),
+            "decode_1thread_gbps": round(2 * n * k1 / t_1 / 1e9, 4),
+            "decode_allcores_gbps": round(2 * n * k_all / t_all / 1e9, 4),
+            "sample": (f"encode of rank 0's shard ({n:,} values, 1 thread, "
+                       f"{t_enc:.2f} s); decode of {k1} shard(s) on 1 thread "
+                       f"({t_1:.1f} s); decode of {k_all} of {R} shards, one "
+                       f"per thread on {threads} threads ({t_all:.1f} s)"
+                       + ("" if k_all == R else
+                          f", scaled to all {R}") +
+                       "; shards streamed from the GPU set-up one at a "
+                       "time")}
+
+
+def copy_ceiling(dev, stream, nbytes=2 << 30, reps=10):
+    """A plain device copy of nbytes (torch copy_ of uint8 tensors), event
+    timed: read + write bytes per second (GB/s)."""
+    import torch
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    evs = [(torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        dst.copy_(src)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t = float(np.median([a.elapsed_time(b) for a, b in evs])) / 1e3
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / t / 1e9
+
+
+def spread(v):
+    return [round(float(x), 2) for x in np.percentile(v, [10, 50, 90])]
+
+
+def measure_layer(S, args, stream, decide_link_bps=8e9):
+    """The timed codec steps of one Setup and their figures: per-phase times,
+    algorithmic bytes and HBM fractions (decode and encode rooflines), the
+    stand-alone cache update, the wire ratio and the Section 3.2 decision
+    taken every step on an inter-node link (the paper's ~8 GB/s bus, alpha
+    10 us) with the decode time measured in warm-up."""
+    import torch
+    from paper_2609_04609_amd import ciera
+    wl, B, R, n = S.wl, S.B, S.R, S.n
+    q = S.changed_blocks / max(1, -(-n // B))
+    decision = {"t_decmp_s": 0.0}
+
+    def decide(s):
+        decision["dec"], decision["gain"] = ciera.ciera_should_compress(
+            n, B, q, R, 10e-6, decide_link_bps,
+            t_decmp_s=decision["t_decmp_s"])
+
+    if args.warmup:
+        _, dec_w, _ = timed_steps(S, 0, args.warmup, stream, decide)
+        decision["t_decmp_s"] = float(np.mean(dec_w)) / 1e6
+    enc_us, dec_us, wall = timed_steps(S, 0, args.steps, stream, decide,
+                                       start=args.warmup)
+    t_enc = float(np.mean(enc_us)) / 1e6
+    t_dec = float(np.mean(dec_us)) / 1e6
+    t_upd = time_update_cache(S, args.steps, stream)
+    # exponents that changed in rank 0's shard: the fused cache update's bytes
+    d0 = ((S.W[:n].to(torch.int32) ^ S.W2[:n].to(torch.int32)) >> 7) & 0xFF
+    changed_vals = int((d0 != 0).sum().item())
+    del d0
+    E_A = []
+    for j in range(R):
+        h = S.gA[int(S.offA[j]):int(S.offA[j]) + 64].cpu().numpy()
+        E_A.append(int(h[32:40].view(np.uint64)[0]))
+    b_enc, b_dec, b_upd = algorithmic_bytes(n, R, B, E_A, None)
+    b_enc += changed_vals
+    tr = measured_traffic(wl.name, B)
+    dec_gbps = b_dec / t_dec / 1e9
+    enc_gbps = b_enc / t_enc / 1e9
+    return {
+        "workload": describe(wl, B),
+        "ms_per_step": round(wall * 1e3, 4),
+        "bf16_gbps": round((2 * n + 2 * R * n) / wall / 1e9, 2),
+        "encode": {"us": round(t_enc * 1e6, 2),
+                   "us_p10_p50_p90": spread(enc_us),
+                   "bf16_gbps": round(2 * n / t_enc / 1e9, 1),
+                   "hbm_gbps": round(enc_gbps, 1),
+                   "hbm_frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
+                   "alg_bytes": b_enc},
+        "decode": {"us": round(t_dec * 1e6, 2),
+                   "us_p10_p50_p90": spread(dec_us),
+                   "bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
+                   "hbm_gbps": round(dec_gbps, 1),
+                   "hbm_frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
+                   "alg_bytes": b_dec},
+        "update_cache": {"us": round(t_upd * 1e6, 2),
+                         "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
+                         "alg_bytes": b_upd},
+        "roofline": {"bound": "hbm",
+                     "kernel": ("tile_prefix_kernel + decode_kernel "
+                                "(ciera_decode_gathered)" if B > 1 else
+                                "count_tile_bits + scan_counts + "
+                                "decode_elems_kernel (ciera_decode_gathered)"),
+                     "achieved": round(dec_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": tr["decode"] if tr else None},
+        "roofline_encode": {"bound": "hbm",
+                            "kernel": ("encode_pass_kernel + exception pass "
+                                       "(ciera_encode with the fused cache "
+                                       "update)"),
+                            "achieved": round(enc_gbps, 1),
+                            "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                            "frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
+                            "traffic": tr["encode"] if tr else None},
+        "wire_ratio": round(sum(S.totA) / (2.0 * R * n), 5),
+        "q_blocks": round(q, 5),
+        "exceptions_local": E_A[0],
+        "should_compress": {"decision": int(decision["dec"]),
+                            "gain_s": decision["gain"],
+                            "link": "alpha 10us, 8 GB/s per rank pair"},
+        "verified": ("every step's encode bytes equal rank 0's gathered "
+                     "slot; the last decoded layer equals W' (or W) bit for "
+                     "bit and the sender cache equals the receivers'"),
+        "_cache_is_w2": (args.warmup + args.steps - 1) % 2 == 0,
+    }
 
 
 def run(args):
@@ -695,153 +829,84 @@ def run(args):
         build.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
     wl = synth.WORKLOADS[args.workload]
     B = args.block
     S = Setup(wl, B, dev)
     R, n = S.R, S.n
-    stream = torch.cuda.current_stream()
-
-    # Section 3.2 decision inputs: the measured block change rate of this
-    # group, an inter-node Allgather link (the paper's ~8 GB/s bus), and the
-    # decode time measured in warm-up
-    q = S.changed_blocks / max(1, -(-n // B))
-    decision = {"t_decmp_s": 0.0}
-
-    def step(s, evs):
-        even = (s % 2) == 0
-        w_in = S.W2[:n] if even else S.W[:n]
-        g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
-        decision["dec"], decision["gain"] = ciera.ciera_should_compress(
-            n, B, q, R, 10e-6, 8e9, t_decmp_s=decision["t_decmp_s"])
-        evs[0].record(stream)
-        ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
-                       update_cache=True)
-        evs[1].record(stream)
-        ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
-        evs[2].record(stream)
-
-    def events():
-        return [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-
-    warm = [events() for _ in range(args.warmup)]
-    for s in range(args.warmup):
-        step(s, warm[s])
-    torch.cuda.synchronize()
-    if args.warmup:
-        decision["t_decmp_s"] = np.mean(
-            [e[1].elapsed_time(e[2]) for e in warm]) / 1e3
-    # keep the parity of W vs W' aligned with the caches: an odd number of
-    # warm-up steps leaves the caches at exp(W'), so start the timed loop on
-    # the matching side
-    base = args.warmup
-    evs = [events() for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(base + s, evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-
-    # the last step decoded the full layer: it must equal W' or W exactly,
-    # and its encode must have produced the bytes of rank 0's gathered slot
-    last_even = ((base + args.steps - 1) % 2) == 0
-    expect = S.W2 if last_even else S.W
-    g_last, t0_last = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
-    ok = bool(torch.equal(S.out, expect)) and \
-        bool(torch.equal(S.cache[:n], S.send_cache)) and \
-        bool(torch.equal(S.tmp[:t0_last], g_last[:t0_last]))
-    errs = S.ws_enc.error() | S.ws_dec.error()
-    if not ok or errs:
-        raise RuntimeError(f"timed steps are not exact (err={errs})")
-
-    hashed = (time_encode_hashed(S, args.steps, stream, last_even)
-              if B >= 16 else None)
-    ans = (time_ans(S, args.steps, stream, last_even)
-           if B >= 16 and args.ans else None)
-    f16 = (time_f16(wl, B, dev, args.steps, stream)
-           if args.fp16 and B >= 16 and wl.name.startswith("olmoe_layer")
-           else None)
-    overlap = (time_overlap(S, args.overlap_layers, 3, last_even)
-               if args.overlap_layers > 0 and wl.name.startswith("olmoe_layer")
-               else None)
-    small = (time_small_configs(B, dev, args.steps, stream)
-             if args.others and B >= 16 else None)
-    mixed = (time_mixed_layer(B, dev, min(args.steps, 20), stream)
-             if args.others and B >= 16 else None)
-
-    enc_us = [e[0].elapsed_time(e[1]) * 1e3 for e in evs]
-    dec_us = [e[1].elapsed_time(e[2]) * 1e3 for e in evs]
-    t_enc = float(np.mean(enc_us)) / 1e6
-    t_dec = float(np.mean(dec_us)) / 1e6
-
-    def spread(v):
-        return [round(float(x), 2) for x in np.percentile(v, [10, 50, 90])]
-    t_upd = time_update_cache(S, args.steps, stream)
-    # exponents that changed in rank 0's shard: the fused cache update's bytes
-    d0 = ((S.W[:n].to(torch.int32) ^ S.W2[:n].to(torch.int32)) >> 7) & 0xFF
-    changed_vals = int((d0 != 0).sum().item())
-    E_A = []
-    for j in range(R):
-        h = S.gA[int(S.offA[j]):int(S.offA[j]) + 64].cpu().numpy()
-        E_A.append(int(h[32:40].view(np.uint64)[0]))
-    b_enc, b_dec, b_upd = algorithmic_bytes(n, R, B, E_A, None)
-    b_enc += changed_vals
-    wire = sum(S.totA) / (2.0 * R * n)
-    ms = wall / args.steps * 1e3
-    value = (2 * n + 2 * R * n) / (wall / args.steps) / 1e9
+    rec = measure_layer(S, args, stream)
+    rec.pop("_cache_is_w2")
+    copy_gbps = copy_ceiling(dev, stream)
+    ms = rec["ms_per_step"]
     res = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": rec["bf16_gbps"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
         "data": "synthetic",
-        "config": {"workload": describe(wl, B), "name": wl.name,
+        "config": {"workload": rec["workload"], "name": wl.name,
                    "shards": R, "shard_elems": n, "block_elems": B},
-        "encode": {"us": round(t_enc * 1e6, 2),
-                   "us_p10_p50_p90": spread(enc_us),
-                   "bf16_gbps": round(2 * n / t_enc / 1e9, 1),
-                   "hbm_gbps": round(b_enc / t_enc / 1e9, 1),
-                   "hbm_frac": round(b_enc / t_enc / 1e9 / HBM_PEAK_GBPS, 4),
-                   "alg_bytes": b_enc},
-        "encode_hashed": hashed,
-        "ans": ans,
-        "overlap": overlap,
-        "fp16": f16,
-        "small_configs": small,
-        "mixed_layer": mixed,
-        "update_cache": {"us": round(t_upd * 1e6, 2),
-                         "hbm_gbps": round(b_upd / t_upd / 1e9, 1),
-                         "alg_bytes": b_upd},
-        "decode": {"us": round(t_dec * 1e6, 2),
-                   "us_p10_p50_p90": spread(dec_us),
-                   "bf16_gbps": round(2 * R * n / t_dec / 1e9, 1),
-                   "hbm_gbps": round(b_dec / t_dec / 1e9, 1),
-                   "hbm_frac": round(b_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
-                   "alg_bytes": b_dec},
-        "wire_ratio": round(wire, 5),
-        "q_blocks": round(q, 5),
-        "exceptions_local": E_A[0],
-        "should_compress": {"decision": int(decision["dec"]),
-                            "gain_s": decision["gain"],
-                            "link": "alpha 10us, 8 GB/s per rank pair"},
-        "roofline": {"bound": "hbm",
-                     "kernel": "decode_kernel (ciera_decode_gathered)",
-                     "achieved": round(b_dec / t_dec / 1e9, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(b_dec / t_dec / 1e9 / HBM_PEAK_GBPS, 4),
-                     "traffic": measured_traffic(wl.name, B)},
-        "verified": "last decoded layer equals W' (or W) bit for bit",
+        "roofline": rec["roofline"],
+        "roofline_encode": rec["roofline_encode"],
+        "encode": rec["encode"],
+        "decode": rec["decode"],
+        "update_cache": rec["update_cache"],
+        "wire_ratio": rec["wire_ratio"],
+        "q_blocks": rec["q_blocks"],
+        "exceptions_local": rec["exceptions_local"],
+        "should_compress": rec["should_compress"],
+        "copy_ceiling": {
+            "gbps": round(copy_gbps, 1),
+            "frac_of_peak": round(copy_gbps / HBM_PEAK_GBPS, 4),
+            "decode_frac_of_copy": round(
+                rec["decode"]["hbm_gbps"] / copy_gbps, 4),
+            "encode_frac_of_copy": round(
+                rec["encode"]["hbm_gbps"] / copy_gbps, 4),
+            "note": "a plain 2 GiB device copy (torch copy_), read + write "
+                    "bytes per second"},
+        "verified": rec["verified"],
     }
     if args.cpu_baseline:
         log("timing the CPU oracle")
         res["cpu_baseline"] = cpu_baseline(S)
+    del S
+    torch.cuda.empty_cache()
+
+    if args.others:
+        # the OLMoE layer: the same record at B = 512 and at B = 1, then its
+        # block-hash, rANS, fp16 and overlap variants
+        olmoe = synth.WORKLOADS["olmoe_layer_c0.1"]
+        So = Setup(olmoe, 512, dev)
+        ro = measure_layer(So, args, stream)
+        w2_side = ro.pop("_cache_is_w2")
+        ro["encode_hashed"] = time_encode_hashed(So, args.steps, stream,
+                                                 w2_side)
+        ro["ans"] = (time_ans(So, args.steps, stream, w2_side)
+                     if args.ans else None)
+        ro["overlap"] = (time_overlap(So, args.overlap_layers, 3, w2_side)
+                         if args.overlap_layers > 0 else None)
+        res["olmoe_layer"] = ro
+        del So
+        torch.cuda.empty_cache()
+        So1 = Setup(olmoe, 1, dev)
+        r1 = measure_layer(So1, args, stream)
+        r1.pop("_cache_is_w2")
+        res["olmoe_layer_b1"] = r1
+        del So1
+        torch.cuda.empty_cache()
+        res["fp16"] = (time_f16(olmoe, 512, dev, args.steps, stream)
+                       if args.fp16 else None)
+        res["small_configs"] = time_small_configs(512, dev, args.steps,
+                                                  stream)
+        res["mixed_layer"] = time_mixed_layer(512, dev,
+                                              min(args.steps, 20), stream)
     if args.copy_calibration:
         # a plain device copy of a known size, for scaling the HBM byte
         # counters of a rocprofv3 --pmc run of this same command
@@ -859,7 +924,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="olmoe_layer_c0.1")
+    ap.add_argument("--workload", default="dsv3_layer")
     ap.add_argument("--block", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline",
                     action="store_false")
@@ -870,8 +935,8 @@ def main():
     ap.add_argument("--overlap-layers", type=int, default=4,
                     help="layer groups in the overlap measurement (0: skip)")
     ap.add_argument("--no-others", dest="others", action="store_false",
-                    help="skip the tiny, single-expert and mixed-layer "
-                         "measurements")
+                    help="time the headline workload only (no OLMoE layer "
+                         "records, small configurations or mixed layer)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")
