@@ -20,10 +20,11 @@ rANS and overlap variants, the small configurations and one layer of the
 mixed model step.
 
 Inputs are resident in HBM before timing starts. Phase times come from HIP
-events recorded on the stream the kernels run on: one before the encode and
-one between encode and decode, the decode ending at the next step's first
-event. The CPU oracle is timed on the host cores as a reported baseline, on
-the same bytes, streamed shard by shard.
+events on the stream the kernels run on, stamped by the library's kernels
+themselves (ciera_time_next_call: the start of a call's first kernel, the
+end of its last), so that the timed steps run back to back with no marker
+packet between encode and decode. The CPU oracle is timed on the host cores
+as a reported baseline, on the same bytes, streamed shard by shard.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--block B]
 """
@@ -65,6 +66,81 @@ def measured_traffic(name, B, dtype="bf16"):
 
 METRIC = ("encode & N-shard decode GB/s (bf16 weights), % HBM peak, "
           "wire-bytes ratio")
+
+
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence:
+    recording it makes no system-scope release, so it neither writes back
+    nor invalidates the L2 between the kernels it brackets (a default event
+    does both, which costs the stream about 5 us per event on MI355X and
+    moves the write-back of one kernel's dirty lines into the gap). The
+    timestamps are read after a device synchronisation. With fenced=True it
+    is a default (fenced) timing event instead, for comparison."""
+    _hip = None
+    fenced = False
+
+    def __init__(self):
+        import ctypes
+        if TimingEvent._hip is None:
+            lib = ctypes.CDLL("libamdhip64.so.7")  # the runtime torch loaded
+            lib.hipEventCreateWithFlags.argtypes = [
+                ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventElapsedTime.argtypes = [
+                ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            TimingEvent._hip = lib
+        self._h = ctypes.c_void_p()
+        flags = 0 if TimingEvent.fenced else 0x20000000
+        if TimingEvent._hip.hipEventCreateWithFlags(ctypes.byref(self._h),
+                                                    flags) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self, stream):
+        if self._hip.hipEventRecord(self._h, stream.cuda_stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end):
+        """Milliseconds from this event to `end` (both recorded and done)."""
+        import ctypes
+        ms = ctypes.c_float()
+        if self._hip.hipEventElapsedTime(ctypes.byref(ms), self._h,
+                                         end._h) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._hip is not None:
+            self._hip.hipEventDestroy(self._h)
+
+
+# Phase times: by default the library's own kernels stamp the events
+# (ciera_time_next_call: the first kernel of a call its start, the last its
+# end), so no marker packet sits between the timed calls; with marker
+# timing, events are recorded on the stream around each call instead.
+KERNEL_STAMPS = True
+
+
+class Span:
+    """The time one library call's kernels take on their stream."""
+
+    def __init__(self):
+        self.a, self.b = TimingEvent(), TimingEvent()
+
+    def arm(self, stream):
+        if KERNEL_STAMPS:
+            from paper_2609_04609_amd import ciera
+            ciera.ciera_time_next_call(self.a._h, self.b._h)
+        else:
+            self.a.record(stream)
+
+    def close(self, stream):
+        if not KERNEL_STAMPS:
+            self.b.record(stream)
+
+    def us(self):
+        return self.a.elapsed_time(self.b) * 1e3
 
 
 def log(msg):
@@ -187,41 +263,41 @@ def timed_steps(S, warmup, steps, stream, decide=None, start=0):
     forward, then the gathered decode; raw groups encode raw), alternating
     W -> W' and back: step s goes W -> W' when s is even, so a sequence of
     calls continues with start = the steps already run. `decide(s)` runs on
-    the host before step s (the Section 3.2 decision). Two events per step:
-    before the encode and
-    between encode and decode; the decode ends at the next step's first
-    event (or a last one). Returns per-step encode and decode times (us) and
-    the wall time per step (s). The last step's encoded bytes, decoded
-    values and caches are checked bit for bit."""
+    the host before step s (the Section 3.2 decision). Each call is timed
+    by a Span. Returns per-step encode and decode times (us) and the wall
+    time per step (s). The last step's encoded bytes, decoded values and
+    caches are checked bit for bit."""
     import torch
     from paper_2609_04609_amd import ciera
     n, B = S.n, S.B
 
-    def one(s, e0, e1):
+    def one(s, se, sd):
         even = (s % 2) == 0
         w_in = S.W2[:n] if even else S.W[:n]
         g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
         if decide is not None:
             decide(s)
-        if e0 is not None:
-            e0.record(stream)
+        if se is not None:
+            se.arm(stream)
         if S.raw:
             ciera.encode_t(w_in, None, B, S.ws_enc, S.tmp, raw=True)
         else:
             ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
                            update_cache=True)
-        if e1 is not None:
-            e1.record(stream)
+        if se is not None:
+            se.close(stream)
+            sd.arm(stream)
         ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
+        if sd is not None:
+            sd.close(stream)
 
     for s in range(warmup):
         one(start + s, None, None)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps + 1)]
+    spans = [(Span(), Span()) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
-        one(start + warmup + s, ev[2 * s], ev[2 * s + 1])
-    ev[2 * steps].record(stream)
+        one(start + warmup + s, *spans[s])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     last_even = (start + warmup + steps - 1) % 2 == 0
@@ -234,9 +310,8 @@ def timed_steps(S, warmup, steps, stream, decide=None, start=0):
     errs = S.ws_enc.error() | S.ws_dec.error()
     if not ok or errs:
         raise RuntimeError(f"codec steps are not exact (err={errs})")
-    enc = [ev[2 * k].elapsed_time(ev[2 * k + 1]) * 1e3 for k in range(steps)]
-    dec = [ev[2 * k + 1].elapsed_time(ev[2 * k + 2]) * 1e3
-           for k in range(steps)]
+    enc = [se.us() for se, _ in spans]
+    dec = [sd.us() for _, sd in spans]
     return enc, dec, wall
 
 
@@ -351,14 +426,13 @@ def time_update_cache(S, steps, stream):
     enc = S.gA[:int(S.totA[0])]
     for _ in range(3):
         ciera.update_cache_t(c, enc, n, B, S.ws_enc)
-    evs = [(torch.cuda.Event(enable_timing=True),
-            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in evs:
-        a.record(stream)
+    spans = [Span() for _ in range(steps)]
+    for sp in spans:
+        sp.arm(stream)
         ciera.update_cache_t(c, enc, n, B, S.ws_enc)
-        b.record(stream)
+        sp.close(stream)
     torch.cuda.synchronize()
-    return float(np.mean([a.elapsed_time(b) for a, b in evs])) / 1e3
+    return float(np.mean([sp.us() for sp in spans])) / 1e6
 
 
 def algorithmic_bytes(n, R, B, E_list, changed_list):
@@ -412,15 +486,14 @@ def time_encode_hashed(S, steps, stream, cache_is_w2):
     for i in range(4):
         ciera.encode_hashed_t(pairs[i % 2][0], pairs[i % 2][1], hout, B,
                               S.ws_enc, out)
-    evs = [(torch.cuda.Event(enable_timing=True),
-            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    spans = [Span() for _ in range(steps)]
     for i in range(steps):
-        evs[i][0].record(stream)
+        spans[i].arm(stream)
         ciera.encode_hashed_t(pairs[i % 2][0], pairs[i % 2][1], hout, B,
                               S.ws_enc, out)
-        evs[i][1].record(stream)
+        spans[i].close(stream)
     torch.cuda.synchronize()
-    t = np.mean([a.elapsed_time(b) for a, b in evs]) / 1e3
+    t = np.mean([sp.us() for sp in spans]) / 1e6
     bm = -(-nb // 8)
     alg = 2 * n + 16 * nb + n + bm + S.E0 + 64 + 16 * nb
     return {"us": round(t * 1e6, 2), "bf16_gbps": round(2 * n / t / 1e9, 1),
@@ -465,27 +538,24 @@ def time_ans(S, steps, stream, cache_is_w2):
     # coding time: encode (fresh mode-0 bytes) then code, events between
     w_in = S.W[:n] if cache_is_w2 else S.W2[:n]
     out = torch.empty_like(S.tmp)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
-           for _ in range(steps)]
+    spans = [Span() for _ in range(steps)]
     for i in range(steps + 3):
-        e = evs[i - 3] if i >= 3 else None
-        if e: e[0].record(stream)
+        sp = spans[i - 3] if i >= 3 else None
         ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, out)
-        if e: e[1].record(stream)
+        if sp: sp.arm(stream)
         ciera.ans_code_t(out, n, B, ws1)
-        if e: e[2].record(stream)
+        if sp: sp.close(stream)
     torch.cuda.synchronize()
-    t_code = np.mean([e[1].elapsed_time(e[2]) for e in evs]) / 1e3
+    t_code = np.mean([sp.us() for sp in spans]) / 1e6
     # decode of the coded buffers, starting on the side the caches are at
     pairs = [(gB, oB, S.W), (gA, oA, S.W2)] if cache_is_w2 else \
         [(gA, oA, S.W2), (gB, oB, S.W)]
-    dev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
-           for _ in range(steps)]
+    dspans = [Span() for _ in range(steps)]
     for i in range(steps):
         g, o, _ = pairs[i % 2]
-        dev[i][0].record(stream)
+        dspans[i].arm(stream)
         ciera.decode_gathered_t(g, o, n, B, S.out, S.cache, wsR)
-        dev[i][1].record(stream)
+        dspans[i].close(stream)
     torch.cuda.synchronize()
     expect = pairs[(steps - 1) % 2][2]
     if not torch.equal(S.out, expect) or wsR.error() != 0:
@@ -495,7 +565,7 @@ def time_ans(S, steps, stream, cache_is_w2):
         g, o, _ = pairs[1]
         ciera.decode_gathered_t(g, o, n, B, S.out, S.cache, wsR)
         torch.cuda.synchronize()
-    t_dec = np.mean([a.elapsed_time(b) for a, b in dev]) / 1e3
+    t_dec = np.mean([sp.us() for sp in dspans]) / 1e6
     E0 = S.E0
     q_eff = (C0 if C0 is not None else E0) / n
     dec, gain = ciera.ciera_should_compress(n, B, q_eff, R, 10e-6, 8e9,
@@ -562,24 +632,23 @@ def time_f16(wl, B, dev, steps, stream):
     hA = gA[:64].cpu().numpy()
     E0 = int(hA[32:40].view(np.uint64)[0])
     pairs = [(W2, gA, oA), (W, gB, oB)]
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)]
-           for _ in range(steps)]
+    spans = [(Span(), Span()) for _ in range(steps)]
     for i in range(steps + 2):
         w_in, g, o = pairs[i % 2]
-        e = evs[i - 2] if i >= 2 else None
-        if e: e[0].record(stream)
+        se, sd = spans[i - 2] if i >= 2 else (None, None)
+        if se: se.arm(stream)
         ciera.encode_t(w_in[:n], send, B, ws_e, tmp, fp16=True)
-        if e: e[1].record(stream)
+        if se: se.close(stream)
         ciera.update_cache_t(send, tmp, n, B, ws_e, fp16=True)
-        if e: e[2].record(stream)
+        if sd: sd.arm(stream)
         ciera.decode_gathered_t(g, o, n, B, out, cache, ws_d, fp16=True)
-        if e: e[3].record(stream)
+        if sd: sd.close(stream)
     torch.cuda.synchronize()
     last = (steps + 1) % 2
     if not torch.equal(out, pairs[last][0]) or ws_d.error() or ws_e.error():
         raise RuntimeError("fp16 steps are not exact")
-    t_enc = np.mean([e[0].elapsed_time(e[1]) for e in evs]) / 1e3
-    t_dec = np.mean([e[2].elapsed_time(e[3]) for e in evs]) / 1e3
+    t_enc = np.mean([se.us() for se, _ in spans]) / 1e6
+    t_dec = np.mean([sd.us() for _, sd in spans]) / 1e6
     nbk = -(-n // B)
     bm = -(-nbk // 8)
     S_sm = n + 3 * (-(-n // 8))
@@ -716,8 +785,8 @@ def copy_ceiling(dev, stream, nbytes=2 << 30, reps=10):
     dst = torch.empty_like(src)
     for _ in range(3):
         dst.copy_(src)
-    evs = [(torch.cuda.Event(enable_timing=True),
-            torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    evs = [(TimingEvent(),
+            TimingEvent()) for _ in range(reps)]
     for a, b in evs:
         a.record(stream)
         dst.copy_(src)
@@ -872,6 +941,12 @@ def run(args):
             "note": "a plain 2 GiB device copy (torch copy_), read + write "
                     "bytes per second"},
         "verified": rec["verified"],
+        "timing": ("HIP events stamped by the first and last kernel of each "
+                   "library call (hipExtLaunchKernel), on the kernels' stream"
+                   if KERNEL_STAMPS else
+                   "HIP events recorded on the kernels' stream around each "
+                   "call (" + ("fenced" if TimingEvent.fenced else
+                              "hipEventDisableSystemFence") + ")"),
     }
     if args.cpu_baseline:
         log("timing the CPU oracle")
@@ -940,7 +1015,18 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")
+    ap.add_argument("--marker-events", action="store_true",
+                    help="time the library calls with events recorded on "
+                         "the stream around them instead of events stamped "
+                         "by their kernels")
+    ap.add_argument("--fenced-events", action="store_true",
+                    help="with --marker-events: default HIP events (a "
+                         "system-scope release at every event) instead of "
+                         "fence-free ones")
     args = ap.parse_args()
+    global KERNEL_STAMPS
+    KERNEL_STAMPS = not args.marker_events
+    TimingEvent.fenced = args.fenced_events
     if args.gpus != 1:
         print("bench.py measures one GPU: the codec is rank-local and the "
               "Allgather is stood in for by one HBM buffer, so --gpus must "

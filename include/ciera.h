@@ -67,7 +67,9 @@
  * All buffers are device memory unless marked (host); the caller owns every
  * buffer. GPU calls validate their arguments on the host, enqueue on
  * `stream`, and return at once: they never allocate, free or synchronise. A
- * negative return means nothing was enqueued. Errors that only the device can
+ * negative return means nothing was enqueued; CIERA_EHIP reports the call's
+ * own launches only (a HIP error left pending on the calling thread by
+ * earlier work is cleared when a GPU call starts). Errors that only the device can
  * see (a shard whose header does not match the call, a shard offset that is
  * not 16-byte aligned, a shard that does not fit in the buffer length the
  * caller gave, an exception index past the shard's list) set bits in the
@@ -148,6 +150,17 @@ int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
  * Synchronises `stream` (the only call that does). */
 int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
                           hipStream_t stream);
+
+/* Measurement aid (not part of the method). The next GPU call of this
+ * library made from the calling host thread launches its first kernel with
+ * `start` and every kernel with `stop` as hipExtLaunchKernel events, so that
+ * hipEventElapsedTime(start, stop) is the span from the start of the call's
+ * first kernel to the end of its last, with no marker packet between calls
+ * (an event recorded between two calls idles the stream for a few us).
+ * Either event may be NULL. The request ends when that call returns, also
+ * when the call fails or enqueues nothing (its events then stay
+ * unrecorded). Events: created by the caller, on the call's device. */
+int ciera_time_next_call(hipEvent_t start, hipEvent_t stop);
 
 /* Sender side of Algorithm 1 for one shard (Section 3.1). flags: any of
  * CIERA_ENC_RAW, CIERA_FP16, CIERA_ENC_UPDATE_CACHE (not with RAW).

@@ -17,9 +17,26 @@
 // that hipGetSymbolAddress returns for the current device (noalloc_scratch).
 static __device__ __align__(256) uint8_t scratch[CIERA_NOALLOC_SCRATCH_BYTES];
 
+namespace ciera {
+LaunchTiming &launch_timing() {
+  static thread_local LaunchTiming t;
+  return t;
+}
+}  // namespace ciera
+
 namespace {
 
 using namespace ciera;
+
+// The scope of one GPU call. On entry it clears a HIP error that earlier
+// work left pending on this thread, so that the hipGetLastError after the
+// call's launches reports the call's own failures only; on return it ends a
+// timing request (ciera_time_next_call).
+struct CallScope {
+  CallScope() { (void)hipGetLastError(); }
+  CallScope(const CallScope &) = delete;
+  ~CallScope() { launch_timing() = LaunchTiming{}; }
+};
 
 // B = 1 or a power of two in [16, 4096]; returns log2(B) or -1.
 int log2_block(uint32_t B) {
@@ -65,6 +82,9 @@ constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 // of tiles) counts the bitmap in front of it, half the bitmap on average.
 bool use_count_scan(uint64_t n, uint32_t l) {
   if (l == 0) return false;
+#ifdef CIERA_FORCE_COUNT_SCAN
+  return true;
+#endif
   const uint64_t tiles = enc_tiles(n, l);
   const uint64_t per_group = 4 * uint64_t(exc_tiles_per_wave(tiles));
   const uint64_t groups = (tiles + per_group - 1) / per_group;
@@ -142,18 +162,27 @@ uint8_t *ans_lists_of(void *workspace, uint64_t bytes, uint64_t n,
 }
 }  // namespace
 
+int ciera_time_next_call(hipEvent_t start, hipEvent_t stop) {
+  LaunchTiming &t = launch_timing();
+  t.start = start;
+  t.stop = stop;
+  return CIERA_OK;
+}
+
 int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
                          hipStream_t stream) {
+  CallScope scope;
   if (!workspace || workspace_bytes < kWsCtlBytes || !aligned(workspace, 16))
     return CIERA_EINVAL;
-  return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream) ==
-                 hipSuccess
+  return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream,
+                          true) == hipSuccess
              ? CIERA_OK
              : CIERA_EHIP;
 }
 
 int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
                           hipStream_t stream) {
+  CallScope scope;
   if (!workspace || !err) return CIERA_EINVAL;
   if (hipMemcpyAsync(err, workspace, sizeof(uint32_t), hipMemcpyDeviceToHost,
                      stream) != hipSuccess)
@@ -208,6 +237,7 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
                  void *out, uint64_t out_capacity, uint64_t *out_bytes,
                  void *workspace, uint64_t workspace_bytes,
                  hipStream_t stream) {
+  CallScope scope;
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
   if (flags & ~(CIERA_ENC_RAW | CIERA_FP16 | CIERA_ENC_UPDATE_CACHE))
@@ -242,6 +272,7 @@ int ciera_encode(const uint16_t *w_new, const uint8_t *exp_cache,
 int ciera_hash_blocks(const uint16_t *w, uint64_t n_elems,
                       uint32_t block_elems, uint64_t *hash_cache,
                       hipStream_t stream) {
+  CallScope scope;
   const int l = log2_block(block_elems);
   if (l < 0 || l < kHashMinLog2B) return CIERA_EUNSUPPORTED;
   if (n_elems >= (uint64_t(1) << 32)) return CIERA_EINVAL;
@@ -265,6 +296,7 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
                         uint64_t out_capacity, uint64_t *out_bytes,
                         void *workspace, uint64_t workspace_bytes,
                         hipStream_t stream) {
+  CallScope scope;
   const int l = log2_block(block_elems);
   if (l < 0 || l < kHashMinLog2B) return CIERA_EUNSUPPORTED;
   if (!out || (n_elems && (!w_new || !hash_in || !hash_out)))
@@ -325,6 +357,7 @@ int ciera_decode_gathered(const void *gathered, uint64_t gathered_bytes,
                           uint32_t block_elems, uint32_t flags, uint16_t *out,
                           uint8_t *exp_cache, void *workspace,
                           uint64_t workspace_bytes, hipStream_t stream) {
+  CallScope scope;
   DecArgs a;
   bool vec = false;
   const int rc = decode_args(gathered, gathered_bytes, shard_offsets, nshards,
@@ -348,6 +381,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
                        uint64_t n_elems, uint32_t block_elems, uint32_t flags,
                        void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream) {
+  CallScope scope;
   const int l = log2_block(block_elems);
   if (l < 0) return CIERA_EUNSUPPORTED;
   if (flags & ~CIERA_FP16) return CIERA_EINVAL;
@@ -382,6 +416,7 @@ int ciera_update_cache(uint8_t *exp_cache, const void *encoded,
 int ciera_ans_code(void *encoded, uint64_t n_elems, uint32_t block_elems,
                    uint64_t *out_bytes, void *workspace,
                    uint64_t workspace_bytes, hipStream_t stream) {
+  CallScope scope;
   const int l = log2_block(block_elems);
   if (l < 0 || l < kAnsMinLog2B) return CIERA_EUNSUPPORTED;
   if (!encoded || !workspace) return CIERA_EINVAL;
@@ -417,6 +452,7 @@ int ciera_decode_gathered_noalloc(const void *gathered,
                                   uint32_t block_elems, uint32_t flags,
                                   uint16_t *out, uint8_t *exp_cache,
                                   uint32_t *err, hipStream_t stream) {
+  CallScope scope;
   DecArgs a;
   bool vec = false;
   const int rc = decode_args(gathered, gathered_bytes, shard_offsets, nshards,

@@ -4,7 +4,8 @@
 
 #include <stdint.h>
 
-#include <hip/hip_runtime_api.h>
+#include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 namespace ciera {
 
@@ -82,11 +83,24 @@ constexpr uint64_t kEncChunk = 4096;
 // exception pass keeps in flight, and the number of waves it aims for (each
 // wave takes a run of exc_tiles_per_wave tiles)
 constexpr uint32_t kExcBatch = 4;
-constexpr uint64_t kExcRowWaves = 16384;
+// the same when the exception pass copies from the updated cache (8 bytes
+// per lane and row instead of 16)
+#ifndef CIERA_EXC_BATCH_C
+#define CIERA_EXC_BATCH_C 4
+#endif
+constexpr uint32_t kExcBatchCache = CIERA_EXC_BATCH_C;
+#ifndef CIERA_EXC_ROW_WAVES
+#define CIERA_EXC_ROW_WAVES 16384
+#endif
+constexpr uint64_t kExcRowWaves = CIERA_EXC_ROW_WAVES;
 // 16-byte bitmap words per thread that a workgroup counting the flagged
-// blocks in front of it loads at once (the encode's row-wise exception pass,
-// the decode without a prefix pass)
+// blocks in front of it loads at once (the decode without a prefix pass; the
+// encode's exception pass: kExcGroupLoads)
 constexpr uint32_t kGroupLoads = 2;
+#ifndef CIERA_EXC_GROUP_LOADS
+#define CIERA_EXC_GROUP_LOADS 2
+#endif
+constexpr uint32_t kExcGroupLoads = CIERA_EXC_GROUP_LOADS;
 inline uint32_t exc_tiles_per_wave(uint64_t tiles) {
   const uint64_t t = (tiles + kExcRowWaves - 1) / kExcRowWaves;
   return uint32_t(t ? t : 1);
@@ -204,6 +218,44 @@ struct AnsEncArgs {
 };
 
 // Launchers (ciera_kernels.hip). Each returns the launch status.
+// Kernel-level timing of one library call (ciera_time_next_call): the first
+// kernel the call launches stamps `start` with its start, the call's last
+// kernel stamps `stop` with its end. Per host thread; cleared when the call
+// returns. Kernels in between carry no event: an event bound to a kernel
+// holds the next one back by a few microseconds.
+struct LaunchTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+LaunchTiming &launch_timing();
+
+// Every kernel launch of the library goes through klaunch, and the last one
+// of each call through klaunch_end.
+template <bool END, typename F, typename... Args>
+inline void klaunch_at(F kernel, dim3 grid, dim3 block, uint32_t shmem,
+                       hipStream_t s, Args... args) {
+  LaunchTiming &t = launch_timing();
+  hipEvent_t stop = END ? t.stop : nullptr;
+  if (t.start || stop) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, t.start, stop, 0u,
+                          args...);
+    t.start = nullptr;
+    if (END) t.stop = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+  }
+}
+template <typename F, typename... Args>
+inline void klaunch(F kernel, dim3 grid, dim3 block, uint32_t shmem,
+                    hipStream_t s, Args... args) {
+  klaunch_at<false>(kernel, grid, block, shmem, s, args...);
+}
+template <typename F, typename... Args>
+inline void klaunch_end(F kernel, dim3 grid, dim3 block, uint32_t shmem,
+                        hipStream_t s, Args... args) {
+  klaunch_at<true>(kernel, grid, block, shmem, s, args...);
+}
+
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
 // pass 1 with the hash detector only: a.hash_out receives every block's hash
 hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s);
@@ -214,6 +266,8 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s);
 // ciera_ans.hip
 hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s);
 hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s);
-hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s);
+// `last`: the fill is the call's last kernel (ciera_workspace_init)
+hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s,
+                            bool last = false);
 
 }  // namespace ciera

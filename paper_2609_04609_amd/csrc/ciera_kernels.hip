@@ -729,8 +729,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_counts_kernel(
 
 // This thread's share of the flagged blocks in bitmap bytes [0, nbytes):
 // every load is issued before the first add (clamped addresses, no
-// branches), so a workgroup's count costs one round trip per kGroupLoads
-// 16-byte words per thread. Sum it over the workgroup with block_sum.
+// branches), so a workgroup's count costs one round trip per L 16-byte
+// words per thread. Sum it over the workgroup with block_sum.
+template <uint32_t L>
 __device__ __forceinline__ uint32_t popc_bytes_part(const uint8_t *bmp,
                                                     uint64_t nbytes) {
   if (!nbytes) return 0u;
@@ -739,15 +740,15 @@ __device__ __forceinline__ uint32_t popc_bytes_part(const uint8_t *bmp,
   const uint32_t tb = bmp[ti < nbytes ? ti : nbytes - 1];
   const uint4 *b4 = reinterpret_cast<const uint4 *>(bmp);
   uint32_t c = 0;
-  for (uint64_t i0 = 0; i0 < full16; i0 += kGroupLoads * kThreads) {
-    uint4 v[kGroupLoads];
+  for (uint64_t i0 = 0; i0 < full16; i0 += L * kThreads) {
+    uint4 v[L];
 #pragma unroll
-    for (uint32_t j = 0; j < kGroupLoads; ++j) {
+    for (uint32_t j = 0; j < L; ++j) {
       const uint64_t i = i0 + j * kThreads + threadIdx.x;
       v[j] = b4[i < full16 ? i : full16 - 1];
     }
 #pragma unroll
-    for (uint32_t j = 0; j < kGroupLoads; ++j) {
+    for (uint32_t j = 0; j < L; ++j) {
       const uint64_t i = i0 + j * kThreads + threadIdx.x;
       const uint32_t w = __popc(v[j].x) + __popc(v[j].y) + __popc(v[j].z) +
                          __popc(v[j].w);
@@ -909,7 +910,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
 template <bool VEC, bool F16, bool FROMC>
 __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   using Src = ExcSrc<VEC, F16, FROMC>;
-  constexpr uint32_t D = kExcBatch;
+  constexpr uint32_t D = FROMC ? kExcBatchCache : kExcBatch;
   __shared__ uint32_t s_red[4];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t n = a.n;
@@ -971,7 +972,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
     const uint64_t sb = min(t0, bm);  // + the sibling runs in front
     const uint64_t si = gb + lane;
     const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
-    const uint32_t cg = popc_bytes_part(bmp, gb);
+    const uint32_t cg = popc_bytes_part<kExcGroupLoads>(bmp, gb);
     uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
     for (uint64_t i = si + 64; i < sb; i += 64)  // runs of > 21 tiles
       cs += __popc(uint32_t(bmp[i]));
@@ -1098,7 +1099,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
     const uint64_t sb = min(t0 * bpt, bm);  // + the sibling runs in front
     const uint64_t si = gb + lane;
     const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
-    const uint32_t cg = popc_bytes_part(bmp, gb);
+    const uint32_t cg = popc_bytes_part<kExcGroupLoads>(bmp, gb);
     uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
     for (uint64_t i = si + 64; i < sb; i += 64)
       cs += __popc(uint32_t(bmp[i]));
@@ -1779,7 +1780,7 @@ template <bool ELEMS, typename Pick>
 void launch_exc(dim3 grid, const EncArgs &a, bool vec, bool f16, bool fromc,
                 hipStream_t s, Pick pick) {
   auto go = [&](auto v, auto f, auto c) {
-    hipLaunchKernelGGL(pick(v, f, c), grid, dim3(kThreads), 0, s, a);
+    klaunch_end(pick(v, f, c), grid, dim3(kThreads), 0, s, a);
   };
   auto with_c = [&](auto v, auto f) {
     if (fromc) go(v, f, bool_c<true>{}); else go(v, f, bool_c<false>{});
@@ -1801,10 +1802,10 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     constexpr bool V = decltype(v)::value, E = decltype(e)::value,
                    F = decltype(f)::value;
     if (fromc)
-      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, true>), grid,
+      klaunch((encode_pass_kernel<V, E, kDetExact, F, true>), grid,
                          block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, false>),
+      klaunch((encode_pass_kernel<V, E, kDetExact, F, false>),
                          grid, block, 0, s, a);
   };
   if (elems) {
@@ -1815,17 +1816,17 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     else exact(bool_c<false>{}, bool_c<false>{}, bool_c<true>{});
   } else if (a.hashed) {
     if (vec)
-      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHash>), grid,
+      klaunch((encode_pass_kernel<true, false, kDetHash>), grid,
                          block, 0, s, a);
     else
-      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHash>), grid,
+      klaunch((encode_pass_kernel<false, false, kDetHash>), grid,
                          block, 0, s, a);
   } else {
     if (vec) exact(bool_c<true>{}, bool_c<false>{}, bool_c<false>{});
     else exact(bool_c<false>{}, bool_c<false>{}, bool_c<false>{});
   }
   if (elems || a.scan_prefix)
-    hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
+    klaunch(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
   if (elems) {
     launch_exc<true>(grid, a, vec, false, fromc, s, [](auto v, auto, auto c) {
@@ -1860,10 +1861,10 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
 hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s) {
   const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
   if (vec)
-    hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHashOnly>), grid,
+    klaunch_end((encode_pass_kernel<true, false, kDetHashOnly>), grid,
                        block, 0, s, a);
   else
-    hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHashOnly>), grid,
+    klaunch_end((encode_pass_kernel<false, false, kDetHashOnly>), grid,
                        block, 0, s, a);
   return hipGetLastError();
 }
@@ -1876,11 +1877,11 @@ hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
   uint64_t blocks = (octets + kThreads - 1) / kThreads;
   if (blocks == 0) blocks = 1;
   if (vec)
-    hipLaunchKernelGGL((encode_raw_kernel<true>), dim3(uint32_t(blocks)),
+    klaunch_end((encode_raw_kernel<true>), dim3(uint32_t(blocks)),
                        dim3(kThreads), 0, s, w, n, B, out, out_bytes,
                        dtype);
   else
-    hipLaunchKernelGGL((encode_raw_kernel<false>), dim3(uint32_t(blocks)),
+    klaunch_end((encode_raw_kernel<false>), dim3(uint32_t(blocks)),
                        dim3(kThreads), 0, s, w, n, B, out, out_bytes,
                        dtype);
   return hipGetLastError();
@@ -1893,76 +1894,81 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
   const bool upd = a.out == nullptr;
   if (a.log2B == 0) {
     const dim3 cgrid(uint32_t((tiles + 3) / 4), a.nshards);
-    hipLaunchKernelGGL(count_tile_bits_kernel, cgrid, block, 0, s, a,
+    klaunch(count_tile_bits_kernel, cgrid, block, 0, s, a,
                        uint32_t(tiles));
-    hipLaunchKernelGGL(scan_counts_kernel, dim3(a.nshards),
+    klaunch(scan_counts_kernel, dim3(a.nshards),
                        dim3(kScanThreads), 0, s, a.tile_excl, uint32_t(tiles),
                        dec_count_stride(tiles));
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
-        hipLaunchKernelGGL((decode_elems_kernel<O, true, true>), grid, block,
+        klaunch_end((decode_elems_kernel<O, true, true>), grid, block,
                            0, s, a);
       else
-        hipLaunchKernelGGL((decode_elems_kernel<O, false, true>), grid, block,
+        klaunch_end((decode_elems_kernel<O, false, true>), grid, block,
                            0, s, a);
     } else {
       if (vec)
-        hipLaunchKernelGGL((decode_elems_kernel<O, true, false>), grid, block,
+        klaunch_end((decode_elems_kernel<O, true, false>), grid, block,
                            0, s, a);
       else
-        hipLaunchKernelGGL((decode_elems_kernel<O, false, false>), grid,
+        klaunch_end((decode_elems_kernel<O, false, false>), grid,
                            block, 0, s, a);
     }
     return hipGetLastError();
   }
   if (a.prefix_pass)
-    hipLaunchKernelGGL(tile_prefix_kernel, dim3(a.nshards), dim3(kScanThreads),
+    klaunch(tile_prefix_kernel, dim3(a.nshards), dim3(kScanThreads),
                        0, s, a);
   if (a.f16) {
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
-        hipLaunchKernelGGL((decode_kernel<O, true, true, true>), grid, block,
+        klaunch_end((decode_kernel<O, true, true, true>), grid, block,
                            0, s, a);
       else
-        hipLaunchKernelGGL((decode_kernel<O, false, true, true>), grid, block,
+        klaunch_end((decode_kernel<O, false, true, true>), grid, block,
                            0, s, a);
     } else {
       if (vec)
-        hipLaunchKernelGGL((decode_kernel<O, true, false, true>), grid, block,
+        klaunch_end((decode_kernel<O, true, false, true>), grid, block,
                            0, s, a);
       else
-        hipLaunchKernelGGL((decode_kernel<O, false, false, true>), grid,
+        klaunch_end((decode_kernel<O, false, false, true>), grid,
                            block, 0, s, a);
     }
     return hipGetLastError();
   }
   if (upd) {
     if (vec)
-      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, true>), grid,
+      klaunch_end((decode_kernel<int(kDecOct), true, true>), grid,
                          block, 0, s, a);
     else
-      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, true>), grid,
+      klaunch_end((decode_kernel<int(kDecOct), false, true>), grid,
                          block, 0, s, a);
   } else {
     if (vec)
-      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, false>), grid,
+      klaunch_end((decode_kernel<int(kDecOct), true, false>), grid,
                          block, 0, s, a);
     else
-      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, false>), grid,
+      klaunch_end((decode_kernel<int(kDecOct), false, false>), grid,
                          block, 0, s, a);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s) {
+hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s,
+                            bool last) {
   const uint64_t words = bytes / 4;
   if (words == 0) return hipSuccess;
   uint64_t blocks = (words + kThreads - 1) / kThreads;
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads),
-                     0, s, static_cast<uint32_t *>(p), words);
+  if (last)
+    klaunch_end(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads), 0,
+                s, static_cast<uint32_t *>(p), words);
+  else
+    klaunch(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads), 0, s,
+            static_cast<uint32_t *>(p), words);
   return hipGetLastError();
 }
 
