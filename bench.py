@@ -20,11 +20,11 @@ rANS and overlap variants, the small configurations and one layer of the
 mixed model step.
 
 Inputs are resident in HBM before timing starts. Phase times come from HIP
-events on the stream the kernels run on, stamped by the library's kernels
-themselves (ciera_time_next_call: the start of a call's first kernel, the
-end of its last), so that the timed steps run back to back with no marker
-packet between encode and decode. The CPU oracle is timed on the host cores
-as a reported baseline, on the same bytes, streamed shard by shard.
+timing events recorded on the stream the kernels run on, right before and
+after each library call, created without the system-scope fence a default
+event makes (its L2 write-back idles the stream for microseconds). The CPU
+oracle is timed on the host cores as a reported baseline, on the same bytes,
+streamed shard by shard.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--block B]
 """
@@ -115,29 +115,18 @@ class TimingEvent:
             self._hip.hipEventDestroy(self._h)
 
 
-# Phase times: by default the library's own kernels stamp the events
-# (ciera_time_next_call: the first kernel of a call its start, the last its
-# end), so no marker packet sits between the timed calls; with marker
-# timing, events are recorded on the stream around each call instead.
-KERNEL_STAMPS = True
-
-
 class Span:
-    """The time one library call's kernels take on their stream."""
+    """The time one library call takes on its stream: timing events recorded
+    right before and right after it."""
 
     def __init__(self):
         self.a, self.b = TimingEvent(), TimingEvent()
 
     def arm(self, stream):
-        if KERNEL_STAMPS:
-            from paper_2609_04609_amd import ciera
-            ciera.ciera_time_next_call(self.a._h, self.b._h)
-        else:
-            self.a.record(stream)
+        self.a.record(stream)
 
     def close(self, stream):
-        if not KERNEL_STAMPS:
-            self.b.record(stream)
+        self.b.record(stream)
 
     def us(self):
         return self.a.elapsed_time(self.b) * 1e3
@@ -941,12 +930,10 @@ def run(args):
             "note": "a plain 2 GiB device copy (torch copy_), read + write "
                     "bytes per second"},
         "verified": rec["verified"],
-        "timing": ("HIP events stamped by the first and last kernel of each "
-                   "library call (hipExtLaunchKernel), on the kernels' stream"
-                   if KERNEL_STAMPS else
-                   "HIP events recorded on the kernels' stream around each "
-                   "call (" + ("fenced" if TimingEvent.fenced else
-                              "hipEventDisableSystemFence") + ")"),
+        "timing": ("HIP events recorded on the kernels' stream right "
+                   "before and after each call (" +
+                   ("default, fenced" if TimingEvent.fenced else
+                    "hipEventDisableSystemFence") + ")"),
     }
     if args.cpu_baseline:
         log("timing the CPU oracle")
@@ -1015,17 +1002,10 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three 1 GiB device copies (counter "
                          "calibration for rocprofv3 --pmc runs)")
-    ap.add_argument("--marker-events", action="store_true",
-                    help="time the library calls with events recorded on "
-                         "the stream around them instead of events stamped "
-                         "by their kernels")
     ap.add_argument("--fenced-events", action="store_true",
-                    help="with --marker-events: default HIP events (a "
-                         "system-scope release at every event) instead of "
-                         "fence-free ones")
+                    help="time with default HIP events (a system-scope "
+                         "release at every event) instead of fence-free ones")
     args = ap.parse_args()
-    global KERNEL_STAMPS
-    KERNEL_STAMPS = not args.marker_events
     TimingEvent.fenced = args.fenced_events
     if args.gpus != 1:
         print("bench.py measures one GPU: the codec is rank-local and the "

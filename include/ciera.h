@@ -151,17 +151,6 @@ int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
 int ciera_workspace_error(void *workspace, uint32_t *err, int clear,
                           hipStream_t stream);
 
-/* Measurement aid (not part of the method). The next GPU call of this
- * library made from the calling host thread launches its first kernel with
- * `start` and every kernel with `stop` as hipExtLaunchKernel events, so that
- * hipEventElapsedTime(start, stop) is the span from the start of the call's
- * first kernel to the end of its last, with no marker packet between calls
- * (an event recorded between two calls idles the stream for a few us).
- * Either event may be NULL. The request ends when that call returns, also
- * when the call fails or enqueues nothing (its events then stay
- * unrecorded). Events: created by the caller, on the call's device. */
-int ciera_time_next_call(hipEvent_t start, hipEvent_t stop);
-
 /* Sender side of Algorithm 1 for one shard (Section 3.1). flags: any of
  * CIERA_ENC_RAW, CIERA_FP16, CIERA_ENC_UPDATE_CACHE (not with RAW).
  *   w_new      n bf16 values as 16-bit patterns.

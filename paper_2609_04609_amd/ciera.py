@@ -51,7 +51,6 @@ _vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctype
 _SIGS = {
     "ciera_encoded_bound": (_u64, [_u64, _u32, _u32]),
     "ciera_workspace_bytes": (_u64, [_u64, _u32, _u32, _u32]),
-    "ciera_time_next_call": (_i32, [_vp, _vp]),
     "ciera_workspace_init": (_i32, [_vp, _u64, _vp]),
     "ciera_workspace_error": (_i32, [_vp, ctypes.POINTER(_u32), _i32, _vp]),
     "ciera_encode": (_i32, [_vp, _vp, _u64, _u32, _u32, _vp, _u64, _vp, _vp,
@@ -110,12 +109,6 @@ def ciera_encoded_bound(n_elems, block_elems, flags=0):
 
 def ciera_workspace_bytes(n_elems, nshards, block_elems, flags=0):
     return lib().ciera_workspace_bytes(n_elems, nshards, block_elems, flags)
-
-
-def ciera_time_next_call(start_event, stop_event):
-    """hipEvent_t handles (or None) for the next library call's kernels."""
-    _check("ciera_time_next_call",
-           lib().ciera_time_next_call(start_event, stop_event))
 
 
 def ciera_workspace_init(workspace, workspace_bytes, stream):

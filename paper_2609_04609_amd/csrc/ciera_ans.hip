@@ -501,11 +501,11 @@ hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s) {
   // every histogram workgroup adds its bins to the same few hot counters at
   // the end: 256 workgroups measured 15.3 us against 19.3 us for 1024
   const uint32_t gh = g < 256u ? g : 256u;
-  klaunch(ans_hist_kernel, dim3(gh), dim3(kThreads), 0, s, a);
-  klaunch(ans_table_kernel, dim3(1), dim3(kThreads), 0, s, a);
-  klaunch(ans_encode_kernel, dim3(g), dim3(kThreads), 0, s, a);
-  klaunch(ans_finalize_kernel, dim3(1), dim3(kThreads), 0, s, a);
-  klaunch_end(ans_copy_kernel, dim3(g), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_hist_kernel, dim3(gh), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_table_kernel, dim3(1), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_encode_kernel, dim3(g), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_finalize_kernel, dim3(1), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_copy_kernel, dim3(g), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -517,7 +517,7 @@ hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s) {
   const uint64_t need = (kmax + kWaves - 1) / kWaves;
   if (g > need) g = need;
   if (g == 0) g = 1;
-  klaunch(ans_decode_kernel, dim3(uint32_t(g), a.nshards),
+  hipLaunchKernelGGL(ans_decode_kernel, dim3(uint32_t(g), a.nshards),
                      dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }

@@ -17,25 +17,16 @@
 // that hipGetSymbolAddress returns for the current device (noalloc_scratch).
 static __device__ __align__(256) uint8_t scratch[CIERA_NOALLOC_SCRATCH_BYTES];
 
-namespace ciera {
-LaunchTiming &launch_timing() {
-  static thread_local LaunchTiming t;
-  return t;
-}
-}  // namespace ciera
-
 namespace {
 
 using namespace ciera;
 
-// The scope of one GPU call. On entry it clears a HIP error that earlier
+// The scope of one GPU call: on entry it clears a HIP error that earlier
 // work left pending on this thread, so that the hipGetLastError after the
-// call's launches reports the call's own failures only; on return it ends a
-// timing request (ciera_time_next_call).
+// call's launches reports the call's own failures only.
 struct CallScope {
   CallScope() { (void)hipGetLastError(); }
   CallScope(const CallScope &) = delete;
-  ~CallScope() { launch_timing() = LaunchTiming{}; }
 };
 
 // B = 1 or a power of two in [16, 4096]; returns log2(B) or -1.
@@ -82,11 +73,8 @@ constexpr uint64_t kPrefixPassBytes = uint64_t(128) << 20;
 // of tiles) counts the bitmap in front of it, half the bitmap on average.
 bool use_count_scan(uint64_t n, uint32_t l) {
   if (l == 0) return false;
-#ifdef CIERA_FORCE_COUNT_SCAN
-  return true;
-#endif
   const uint64_t tiles = enc_tiles(n, l);
-  const uint64_t per_group = 4 * uint64_t(exc_tiles_per_wave(tiles));
+  const uint64_t per_group = 4 * uint64_t(exc_tiles_per_wave(tiles, l));
   const uint64_t groups = (tiles + per_group - 1) / per_group;
   return groups * bitmap_bytes(n, l) / 2 > kPrefixPassBytes;
 }
@@ -113,7 +101,7 @@ uint64_t ciera_workspace_bytes(uint64_t n_elems, uint32_t nshards,
   const int l = log2_block(block_elems);
   if (l < 0 || (flags & ~CIERA_WS_ANS)) return 0;
   // encode: one count per tile plus the total
-  const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n_elems, uint32_t(l)) + 1);
+  const uint64_t enc = enc_ws_bytes(n_elems, uint32_t(l));
   // decode: the offset of every tile of every shard
   const uint32_t ns = nshards ? nshards : 1;
   const uint64_t dec = dec_ws_bytes(n_elems, ns);
@@ -162,20 +150,13 @@ uint8_t *ans_lists_of(void *workspace, uint64_t bytes, uint64_t n,
 }
 }  // namespace
 
-int ciera_time_next_call(hipEvent_t start, hipEvent_t stop) {
-  LaunchTiming &t = launch_timing();
-  t.start = start;
-  t.stop = stop;
-  return CIERA_OK;
-}
-
 int ciera_workspace_init(void *workspace, uint64_t workspace_bytes,
                          hipStream_t stream) {
   CallScope scope;
   if (!workspace || workspace_bytes < kWsCtlBytes || !aligned(workspace, 16))
     return CIERA_EINVAL;
-  return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream,
-                          true) == hipSuccess
+  return launch_fill_zero(workspace, workspace_bytes & ~uint64_t(3), stream) ==
+                 hipSuccess
              ? CIERA_OK
              : CIERA_EHIP;
 }
@@ -206,7 +187,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
                       bool hashed, bool f16) {
   if (!workspace || !aligned(workspace, 16)) return CIERA_EINVAL;
   const uint64_t tiles = enc_tiles(n_elems, l);
-  if (workspace_bytes < kWsCtlBytes + 4 * (tiles + 1)) return CIERA_ENOSPC;
+  if (workspace_bytes < enc_ws_bytes(n_elems, l)) return CIERA_ENOSPC;
   EncArgs a{};
   a.w = w_new;
   a.cache = exp_cache;
@@ -225,7 +206,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   a.hashed = hashed;
   a.f16 = f16;
   a.scan_prefix = use_count_scan(n_elems, l);
-  a.exc_tiles_per_wave = exc_tiles_per_wave(tiles);
+  a.exc_tiles_per_wave = exc_tiles_per_wave(tiles, l);
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }

@@ -4,8 +4,7 @@
 
 #include <stdint.h>
 
-#include <hip/hip_runtime.h>
-#include <hip/hip_ext.h>
+#include <hip/hip_runtime_api.h>
 
 namespace ciera {
 
@@ -79,30 +78,27 @@ static_assert((kDecTile & (kDecTile - 1)) == 0 && kDecTile >= 4096,
 // lane) when B <= 512, and 8 blocks (8B values, several chunks) when B > 512,
 // so that every tile owns whole bitmap bytes.
 constexpr uint64_t kEncChunk = 4096;
-// B >= 16: the wave instructions of W' re-reads that one wave of the
-// exception pass keeps in flight, and the number of waves it aims for (each
-// wave takes a run of exc_tiles_per_wave tiles)
+// B >= 16: the rows (B >= 512) or wave instructions (B < 512) of changed
+// exponents that one wave of the exception pass keeps in flight, and the
+// number of waves it aims for (each wave takes a run of exc_tiles_per_wave
+// tiles). B >= 512 aims for 8192 waves, all resident at once on 256 CUs at
+// 8 waves per SIMD; when a wave's run then spans several tiles and the pass
+// copies from the updated cache (8 bytes per lane and row), the wave keeps
+// kExcBatchDeep rows in flight. On the DeepSeek-style shard (21,504 tiles)
+// that took the pass from 15.5 us (16384 waves of 4 rows) to 13.8 us; a
+// deeper batch with 8 bitmap loads per thread in the offset count lost
+// occupancy (74 VGPRs, 6 waves per SIMD) and took 15.6 us.
 constexpr uint32_t kExcBatch = 4;
-// the same when the exception pass copies from the updated cache (8 bytes
-// per lane and row instead of 16)
-#ifndef CIERA_EXC_BATCH_C
-#define CIERA_EXC_BATCH_C 4
-#endif
-constexpr uint32_t kExcBatchCache = CIERA_EXC_BATCH_C;
-#ifndef CIERA_EXC_ROW_WAVES
-#define CIERA_EXC_ROW_WAVES 16384
-#endif
-constexpr uint64_t kExcRowWaves = CIERA_EXC_ROW_WAVES;
+constexpr uint32_t kExcBatchDeep = 8;
+constexpr uint64_t kExcBlockWaves = 16384;
+constexpr uint64_t kExcRowWaves = 8192;
 // 16-byte bitmap words per thread that a workgroup counting the flagged
-// blocks in front of it loads at once (the decode without a prefix pass; the
-// encode's exception pass: kExcGroupLoads)
+// blocks in front of it loads at once (the encode's exception pass, the
+// decode without a prefix pass)
 constexpr uint32_t kGroupLoads = 2;
-#ifndef CIERA_EXC_GROUP_LOADS
-#define CIERA_EXC_GROUP_LOADS 2
-#endif
-constexpr uint32_t kExcGroupLoads = CIERA_EXC_GROUP_LOADS;
-inline uint32_t exc_tiles_per_wave(uint64_t tiles) {
-  const uint64_t t = (tiles + kExcRowWaves - 1) / kExcRowWaves;
+inline uint32_t exc_tiles_per_wave(uint64_t tiles, uint32_t log2B) {
+  const uint64_t waves = log2B >= 9 ? kExcRowWaves : kExcBlockWaves;
+  const uint64_t t = (tiles + waves - 1) / waves;
   return uint32_t(t ? t : 1);
 }
 inline uint64_t enc_tile_elems(uint32_t log2B) {
@@ -186,10 +182,14 @@ struct AnsCtl {
 static_assert(sizeof(AnsCtl) == 4096, "rANS control block is 4 KB");
 constexpr int kAnsMinLog2B = 4;  // rANS-coded sections need B >= 16
 inline uint64_t ans_kmax(uint64_t n) { return (n + kAnsChunk - 1) / kAnsChunk; }
+// encode: the control block and a count per tile plus the total
+inline uint64_t enc_ws_bytes(uint64_t n, uint32_t log2B) {
+  return kWsCtlBytes + 4 * (enc_tiles(n, log2B) + 1);
+}
 // past the control block, the encode counts and the decode tile offsets of
 // nshards shards
 inline uint64_t ans_ws_offset(uint64_t n, uint32_t log2B, uint32_t nshards) {
-  const uint64_t enc = kWsCtlBytes + 4 * (enc_tiles(n, log2B) + 1);
+  const uint64_t enc = enc_ws_bytes(n, log2B);
   const uint64_t dec = dec_ws_bytes(n, nshards);
   return ((enc > dec ? enc : dec) + 255) & ~uint64_t(255);
 }
@@ -218,44 +218,6 @@ struct AnsEncArgs {
 };
 
 // Launchers (ciera_kernels.hip). Each returns the launch status.
-// Kernel-level timing of one library call (ciera_time_next_call): the first
-// kernel the call launches stamps `start` with its start, the call's last
-// kernel stamps `stop` with its end. Per host thread; cleared when the call
-// returns. Kernels in between carry no event: an event bound to a kernel
-// holds the next one back by a few microseconds.
-struct LaunchTiming {
-  hipEvent_t start = nullptr;
-  hipEvent_t stop = nullptr;
-};
-LaunchTiming &launch_timing();
-
-// Every kernel launch of the library goes through klaunch, and the last one
-// of each call through klaunch_end.
-template <bool END, typename F, typename... Args>
-inline void klaunch_at(F kernel, dim3 grid, dim3 block, uint32_t shmem,
-                       hipStream_t s, Args... args) {
-  LaunchTiming &t = launch_timing();
-  hipEvent_t stop = END ? t.stop : nullptr;
-  if (t.start || stop) {
-    hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, t.start, stop, 0u,
-                          args...);
-    t.start = nullptr;
-    if (END) t.stop = nullptr;
-  } else {
-    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
-  }
-}
-template <typename F, typename... Args>
-inline void klaunch(F kernel, dim3 grid, dim3 block, uint32_t shmem,
-                    hipStream_t s, Args... args) {
-  klaunch_at<false>(kernel, grid, block, shmem, s, args...);
-}
-template <typename F, typename... Args>
-inline void klaunch_end(F kernel, dim3 grid, dim3 block, uint32_t shmem,
-                        hipStream_t s, Args... args) {
-  klaunch_at<true>(kernel, grid, block, shmem, s, args...);
-}
-
 hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s);
 // pass 1 with the hash detector only: a.hash_out receives every block's hash
 hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s);
@@ -266,8 +228,6 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s);
 // ciera_ans.hip
 hipError_t launch_ans_code(const AnsEncArgs &a, hipStream_t s);
 hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s);
-// `last`: the fill is the call's last kernel (ciera_workspace_init)
-hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s,
-                            bool last = false);
+hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s);
 
 }  // namespace ciera

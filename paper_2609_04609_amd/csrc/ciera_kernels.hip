@@ -903,14 +903,13 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
 // changed or unchanged as a whole, and the exceptions of the changed rows
 // follow one another in row order: the k-th changed row's exponents start at
 // 512 k in the list. A tile (8 blocks) is one bitmap byte. Each wave takes a
-// run of a.exc_tiles_per_wave tiles and copies its changed rows kExcBatch at
-// a time, so that that many re-reads of W' are in flight per wave; the first
-// batch is issued before the offset of the run (the changed blocks in front
-// of it) is counted, and the two overlap.
-template <bool VEC, bool F16, bool FROMC>
+// run of a.exc_tiles_per_wave tiles and copies its changed rows D at a time,
+// so that that many reads of the rows' exponents are in flight per wave; the
+// first batch is issued before the offset of the run (the changed blocks in
+// front of it) is counted, and the two overlap.
+template <bool VEC, bool F16, bool FROMC, uint32_t D>
 __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   using Src = ExcSrc<VEC, F16, FROMC>;
-  constexpr uint32_t D = FROMC ? kExcBatchCache : kExcBatch;
   __shared__ uint32_t s_red[4];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t n = a.n;
@@ -972,7 +971,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
     const uint64_t sb = min(t0, bm);  // + the sibling runs in front
     const uint64_t si = gb + lane;
     const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
-    const uint32_t cg = popc_bytes_part<kExcGroupLoads>(bmp, gb);
+    const uint32_t cg = popc_bytes_part<kGroupLoads>(bmp, gb);
     uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
     for (uint64_t i = si + 64; i < sb; i += 64)  // runs of > 21 tiles
       cs += __popc(uint32_t(bmp[i]));
@@ -1099,7 +1098,7 @@ __global__ __launch_bounds__(kThreads) void encode_exc_blocks_kernel(
     const uint64_t sb = min(t0 * bpt, bm);  // + the sibling runs in front
     const uint64_t si = gb + lane;
     const uint32_t sv = bm ? bmp[min(si, bm - 1)] : 0u;
-    const uint32_t cg = popc_bytes_part<kExcGroupLoads>(bmp, gb);
+    const uint32_t cg = popc_bytes_part<kGroupLoads>(bmp, gb);
     uint32_t cs = si < sb ? uint32_t(__popc(sv)) : 0u;
     for (uint64_t i = si + 64; i < sb; i += 64)
       cs += __popc(uint32_t(bmp[i]));
@@ -1780,7 +1779,7 @@ template <bool ELEMS, typename Pick>
 void launch_exc(dim3 grid, const EncArgs &a, bool vec, bool f16, bool fromc,
                 hipStream_t s, Pick pick) {
   auto go = [&](auto v, auto f, auto c) {
-    klaunch_end(pick(v, f, c), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(pick(v, f, c), grid, dim3(kThreads), 0, s, a);
   };
   auto with_c = [&](auto v, auto f) {
     if (fromc) go(v, f, bool_c<true>{}); else go(v, f, bool_c<false>{});
@@ -1802,10 +1801,10 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     constexpr bool V = decltype(v)::value, E = decltype(e)::value,
                    F = decltype(f)::value;
     if (fromc)
-      klaunch((encode_pass_kernel<V, E, kDetExact, F, true>), grid,
+      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, true>), grid,
                          block, 0, s, a);
     else
-      klaunch((encode_pass_kernel<V, E, kDetExact, F, false>),
+      hipLaunchKernelGGL((encode_pass_kernel<V, E, kDetExact, F, false>),
                          grid, block, 0, s, a);
   };
   if (elems) {
@@ -1816,17 +1815,17 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     else exact(bool_c<false>{}, bool_c<false>{}, bool_c<true>{});
   } else if (a.hashed) {
     if (vec)
-      klaunch((encode_pass_kernel<true, false, kDetHash>), grid,
+      hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHash>), grid,
                          block, 0, s, a);
     else
-      klaunch((encode_pass_kernel<false, false, kDetHash>), grid,
+      hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHash>), grid,
                          block, 0, s, a);
   } else {
     if (vec) exact(bool_c<true>{}, bool_c<false>{}, bool_c<false>{});
     else exact(bool_c<false>{}, bool_c<false>{}, bool_c<false>{});
   }
   if (elems || a.scan_prefix)
-    klaunch(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
+    hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
   if (elems) {
     launch_exc<true>(grid, a, vec, false, fromc, s, [](auto v, auto, auto c) {
@@ -1848,12 +1847,19 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
                                                         decltype(f)::value,
                                                         decltype(c)::value>;
                       });
+  else if (fromc && r.exc_tiles_per_wave >= 2)
+    launch_exc<false>(rgrid, r, vec, r.f16, fromc, s,
+                      [](auto v, auto f, auto c) {
+                        return encode_exc_rows_kernel<
+                            decltype(v)::value, decltype(f)::value,
+                            decltype(c)::value, kExcBatchDeep>;
+                      });
   else
     launch_exc<false>(rgrid, r, vec, r.f16, fromc, s,
                       [](auto v, auto f, auto c) {
-                        return encode_exc_rows_kernel<decltype(v)::value,
-                                                      decltype(f)::value,
-                                                      decltype(c)::value>;
+                        return encode_exc_rows_kernel<
+                            decltype(v)::value, decltype(f)::value,
+                            decltype(c)::value, kExcBatch>;
                       });
   return hipGetLastError();
 }
@@ -1861,10 +1867,10 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
 hipError_t launch_hash_blocks(const EncArgs &a, bool vec, hipStream_t s) {
   const dim3 grid((a.num_tiles + 3) / 4), block(kThreads);
   if (vec)
-    klaunch_end((encode_pass_kernel<true, false, kDetHashOnly>), grid,
+    hipLaunchKernelGGL((encode_pass_kernel<true, false, kDetHashOnly>), grid,
                        block, 0, s, a);
   else
-    klaunch_end((encode_pass_kernel<false, false, kDetHashOnly>), grid,
+    hipLaunchKernelGGL((encode_pass_kernel<false, false, kDetHashOnly>), grid,
                        block, 0, s, a);
   return hipGetLastError();
 }
@@ -1877,11 +1883,11 @@ hipError_t launch_encode_raw(const uint16_t *w, uint64_t n, uint32_t B,
   uint64_t blocks = (octets + kThreads - 1) / kThreads;
   if (blocks == 0) blocks = 1;
   if (vec)
-    klaunch_end((encode_raw_kernel<true>), dim3(uint32_t(blocks)),
+    hipLaunchKernelGGL((encode_raw_kernel<true>), dim3(uint32_t(blocks)),
                        dim3(kThreads), 0, s, w, n, B, out, out_bytes,
                        dtype);
   else
-    klaunch_end((encode_raw_kernel<false>), dim3(uint32_t(blocks)),
+    hipLaunchKernelGGL((encode_raw_kernel<false>), dim3(uint32_t(blocks)),
                        dim3(kThreads), 0, s, w, n, B, out, out_bytes,
                        dtype);
   return hipGetLastError();
@@ -1894,81 +1900,76 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
   const bool upd = a.out == nullptr;
   if (a.log2B == 0) {
     const dim3 cgrid(uint32_t((tiles + 3) / 4), a.nshards);
-    klaunch(count_tile_bits_kernel, cgrid, block, 0, s, a,
+    hipLaunchKernelGGL(count_tile_bits_kernel, cgrid, block, 0, s, a,
                        uint32_t(tiles));
-    klaunch(scan_counts_kernel, dim3(a.nshards),
+    hipLaunchKernelGGL(scan_counts_kernel, dim3(a.nshards),
                        dim3(kScanThreads), 0, s, a.tile_excl, uint32_t(tiles),
                        dec_count_stride(tiles));
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
-        klaunch_end((decode_elems_kernel<O, true, true>), grid, block,
+        hipLaunchKernelGGL((decode_elems_kernel<O, true, true>), grid, block,
                            0, s, a);
       else
-        klaunch_end((decode_elems_kernel<O, false, true>), grid, block,
+        hipLaunchKernelGGL((decode_elems_kernel<O, false, true>), grid, block,
                            0, s, a);
     } else {
       if (vec)
-        klaunch_end((decode_elems_kernel<O, true, false>), grid, block,
+        hipLaunchKernelGGL((decode_elems_kernel<O, true, false>), grid, block,
                            0, s, a);
       else
-        klaunch_end((decode_elems_kernel<O, false, false>), grid,
+        hipLaunchKernelGGL((decode_elems_kernel<O, false, false>), grid,
                            block, 0, s, a);
     }
     return hipGetLastError();
   }
   if (a.prefix_pass)
-    klaunch(tile_prefix_kernel, dim3(a.nshards), dim3(kScanThreads),
+    hipLaunchKernelGGL(tile_prefix_kernel, dim3(a.nshards), dim3(kScanThreads),
                        0, s, a);
   if (a.f16) {
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
-        klaunch_end((decode_kernel<O, true, true, true>), grid, block,
+        hipLaunchKernelGGL((decode_kernel<O, true, true, true>), grid, block,
                            0, s, a);
       else
-        klaunch_end((decode_kernel<O, false, true, true>), grid, block,
+        hipLaunchKernelGGL((decode_kernel<O, false, true, true>), grid, block,
                            0, s, a);
     } else {
       if (vec)
-        klaunch_end((decode_kernel<O, true, false, true>), grid, block,
+        hipLaunchKernelGGL((decode_kernel<O, true, false, true>), grid, block,
                            0, s, a);
       else
-        klaunch_end((decode_kernel<O, false, false, true>), grid,
+        hipLaunchKernelGGL((decode_kernel<O, false, false, true>), grid,
                            block, 0, s, a);
     }
     return hipGetLastError();
   }
   if (upd) {
     if (vec)
-      klaunch_end((decode_kernel<int(kDecOct), true, true>), grid,
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, true>), grid,
                          block, 0, s, a);
     else
-      klaunch_end((decode_kernel<int(kDecOct), false, true>), grid,
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, true>), grid,
                          block, 0, s, a);
   } else {
     if (vec)
-      klaunch_end((decode_kernel<int(kDecOct), true, false>), grid,
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), true, false>), grid,
                          block, 0, s, a);
     else
-      klaunch_end((decode_kernel<int(kDecOct), false, false>), grid,
+      hipLaunchKernelGGL((decode_kernel<int(kDecOct), false, false>), grid,
                          block, 0, s, a);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s,
-                            bool last) {
+hipError_t launch_fill_zero(void *p, uint64_t bytes, hipStream_t s) {
   const uint64_t words = bytes / 4;
   if (words == 0) return hipSuccess;
   uint64_t blocks = (words + kThreads - 1) / kThreads;
   if (blocks > 4096) blocks = 4096;
-  if (last)
-    klaunch_end(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads), 0,
-                s, static_cast<uint32_t *>(p), words);
-  else
-    klaunch(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads), 0, s,
-            static_cast<uint32_t *>(p), words);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(uint32_t(blocks)), dim3(kThreads),
+                     0, s, static_cast<uint32_t *>(p), words);
   return hipGetLastError();
 }
 

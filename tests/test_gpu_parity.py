@@ -60,13 +60,15 @@ def test_encode_rows_random_sizes(gu, orc, B):
     assert ws.error() == 0
 
 
-@pytest.mark.parametrize("B", [64, 512])
-@pytest.mark.parametrize("n", [16384 * 4096, 16384 * 4096 + 1,
-                               16384 * 4096 + 4097])
-def test_encode_rows_run_boundary(gu, orc, n, B):
+@pytest.mark.parametrize("B,waves", [(64, 16384), (512, 8192)])
+@pytest.mark.parametrize("extra", [0, 1, 4097])
+def test_encode_rows_run_boundary(gu, orc, B, waves, extra):
     """Shards around the size where the exception pass goes from one tile
-    per wave to two (16,384 tiles of 4096 values): the last run may hold a
-    single, partial tile."""
+    per wave to two (16,384 tiles of 4096 values at B < 512, 8192 at
+    B >= 512, where runs of two tiles or more also take the deeper batch
+    when the cache is brought forward): the last run may hold a single,
+    partial tile. Plain and fused-update encodes match the oracle."""
+    n = waves * 4096 + extra
     w, w2 = gu.pair(n, 9300 + n % 7, c=0.0005)
     cache_h = orc.split(gu.host_u16(w))[0]
     del w
@@ -74,17 +76,19 @@ def test_encode_rows_run_boundary(gu, orc, n, B):
     expect = orc.encode(gu.host_u16(w2), cache_h, B)
     assert total == expect.size
     np.testing.assert_array_equal(gu.host_u8(out)[:total], expect)
+    del out
+    gu.check_fused_update(orc, w2, cache_h, B, expect, ws, msg="fused")
     assert ws.error() == 0
 
 
 def test_encode_rows_with_count_scan(gu, orc):
-    """A 310,000,005-value shard at B = 512: the row-wise exception pass gives
-    each wave a run of 5 tiles, and its workgroups' counting would re-read
-    about 143 MB of bitmap, so the offsets come from pass 1's per-tile counts
+    """A 600,000,005-value shard at B = 512: the row-wise exception pass gives
+    each wave a run of 18 tiles, and its workgroups' counting would re-read
+    about 149 MB of bitmap, so the offsets come from pass 1's per-tile counts
     and the scan. bf16 and fp16 match the oracle byte for byte; a small call
     first must not leak its counts into the big one."""
     from paper_2609_04609_amd import ciera, synth
-    n, B = 310_000_005, 512
+    n, B = 600_000_005, 512
     ws = ciera.Workspace(n, 1, B)
     w, w2 = gu.pair(n, 3131, c=0.0002)
     wh, w2h = gu.host_u16(w), gu.host_u16(w2)
@@ -116,8 +120,8 @@ def test_encode_rows_with_count_scan(gu, orc):
 
 def test_encode_rows_several_chunks(gu, orc):
     """A 600,000,003-value shard at B = 4096: each wave of the row-wise
-    exception pass takes two tiles, 128 rows of 512 values, so it walks its
-    run in two chunks of 64 rows. Matches the oracle byte for byte."""
+    exception pass takes three tiles, 192 rows of 512 values, so it walks its
+    run in three chunks of 64 rows. Matches the oracle byte for byte."""
     n, B = 600_000_003, 4096
     w, w2 = gu.pair(n, 3434, c=0.00002)
     cache_h = orc.split(gu.host_u16(w))[0]
