@@ -286,12 +286,16 @@ int ciera_encode_hashed(const uint16_t *w_new, const uint64_t *hash_in,
  *   Comm(x) = alpha + (R - 1) x / bw
  *   g = Comm(S) - (Comm(S_{s+m} + S_bm + q S_e + header) + T_hash + T_cmp
  *                  + T_decmp)
- * with S = 2n, S_e = S_{s+m} = n bytes for bf16, S_bm = ceil(ceil(n/B)/8).
+ * with S = 2n, S_e = S_{s+m} = n bytes for bf16 (fp16: S_{s+m} = n +
+ * 3 ceil(n/8), S_e = 5 ceil(n/8), the fp16 wire sections), S_bm =
+ * ceil(ceil(n/B)/8).
  * T_hash and T_cmp count as zero when `overlapped` (compression runs on its
  * own stream beside the Allgather). A shard is compressed iff g > 0. */
 typedef struct {
   uint64_t n_elems;     /* values in one rank's shard */
   uint32_t block_elems; /* B */
+  uint32_t flags;       /* 0 (bf16) or CIERA_FP16: S_{s+m} = n + 3 ceil(n/8)
+                           and S_e = 5 ceil(n/8) bytes (the fp16 sections) */
   double q;             /* measured fraction of changed blocks, in [0, 1] */
 } ciera_shard_stats;
 

@@ -814,22 +814,48 @@ int oracle_decode_f16(const uint8_t *enc, uint64_t n, uint8_t *cache,
 
 /* Section 3.2 gain:
  *   g = Comm(S) - (Comm(S_{s+m} + S_bm + q S_e) + T_hash + T_cmp + T_decmp)
- * with S = 2n, S_e = n, S_{s+m} = n for bf16 and the fixed header added to
- * the compressed payload (a reading: the header is part of what is sent).
- * When compression is overlapped with communication, T_hash and T_cmp leave
- * the critical path and count as zero. */
-double oracle_gain(uint64_t n, uint64_t B, double q, uint64_t R, double alpha_s,
-                   double bw_Bps, double t_hash_s, double t_cmp_s,
-                   double t_decmp_s, int overlapped, double header_bytes) {
-  double S = 2.0 * (double)n;
-  double S_e = (double)n;
-  double S_sm = S - S_e;
+ * for a shard whose raw bytes are S, whose sign+mantissa section is S_sm
+ * bytes and whose exponents take S_e bytes when every block changed; the
+ * fixed header is added to the compressed payload (a reading: the header is
+ * part of what is sent). When compression is overlapped with communication,
+ * T_hash and T_cmp leave the critical path and count as zero. */
+static double gain_of_sections(double S, double S_sm, double S_e, uint64_t n,
+                               uint64_t B, double q, uint64_t R,
+                               double alpha_s, double bw_Bps, double t_hash_s,
+                               double t_cmp_s, double t_decmp_s,
+                               int overlapped, double header_bytes) {
   double S_bm = (double)bitmap_bytes(n, B);
   double comm_raw = alpha_s + (double)(R - 1) * S / bw_Bps;
   double payload = S_sm + S_bm + q * S_e + header_bytes;
   double comm_cmp = alpha_s + (double)(R - 1) * payload / bw_Bps;
   double sender = overlapped ? 0.0 : (t_hash_s + t_cmp_s);
   return comm_raw - (comm_cmp + sender + t_decmp_s);
+}
+
+/* bf16: S = 2n, S_e = n (one exponent byte per value), S_{s+m} = n. */
+double oracle_gain(uint64_t n, uint64_t B, double q, uint64_t R, double alpha_s,
+                   double bw_Bps, double t_hash_s, double t_cmp_s,
+                   double t_decmp_s, int overlapped, double header_bytes) {
+  double S = 2.0 * (double)n;
+  double S_e = (double)n;
+  double S_sm = S - S_e;
+  return gain_of_sections(S, S_sm, S_e, n, B, q, R, alpha_s, bw_Bps, t_hash_s,
+                          t_cmp_s, t_decmp_s, overlapped, header_bytes);
+}
+
+/* fp16 (Table 2's precision; the wire layout of the fp16 encoder above):
+ * S = 2n, S_{s+m} = n + 3 ceil(n/8) (the low mantissa bytes and three bit
+ * planes of sign and high mantissa bits per octet), S_e = 5 ceil(n/8) (five
+ * exponent bit planes per octet), so q S_e counts 5/8 of a byte per
+ * exponent. */
+double oracle_gain_f16(uint64_t n, uint64_t B, double q, uint64_t R,
+                       double alpha_s, double bw_Bps, double t_hash_s,
+                       double t_cmp_s, double t_decmp_s, int overlapped,
+                       double header_bytes) {
+  double octets = (double)((n + 7u) / 8u);
+  return gain_of_sections(2.0 * (double)n, (double)n + 3.0 * octets,
+                          5.0 * octets, n, B, q, R, alpha_s, bw_Bps, t_hash_s,
+                          t_cmp_s, t_decmp_s, overlapped, header_bytes);
 }
 
 uint64_t oracle_select(const double *gain, const double *mem, uint64_t count,

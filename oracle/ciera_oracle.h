@@ -130,6 +130,13 @@ double oracle_gain(uint64_t n, uint64_t B, double q, uint64_t R, double alpha_s,
                    double bw_Bps, double t_hash_s, double t_cmp_s,
                    double t_decmp_s, int overlapped, double header_bytes);
 
+/* The Section 3.2 gain of an fp16 shard (its sections are n + 3 ceil(n/8)
+ * sign+mantissa bytes and 5 ceil(n/8) exponent bytes). */
+double oracle_gain_f16(uint64_t n, uint64_t B, double q, uint64_t R,
+                       double alpha_s, double bw_Bps, double t_hash_s,
+                       double t_cmp_s, double t_decmp_s, int overlapped,
+                       double header_bytes);
+
 /* Section 3.2 ranking: keep shards with g > 0, sort by g/M descending (ties by
  * index), take them greedily while the cache budget allows. Writes 1/0 into
  * selected[i]; returns the number selected. stop_at_first_misfit != 0 stops

@@ -57,13 +57,12 @@ def _bind(lib):
                                            ctypes.c_uint64, _u16p, _u8p]
     lib.oracle_update_cache.restype = ctypes.c_int
     lib.oracle_update_cache.argtypes = [_u8p, _u8p, ctypes.c_uint64]
-    lib.oracle_gain.restype = ctypes.c_double
-    lib.oracle_gain.argtypes = [ctypes.c_uint64, ctypes.c_uint64,
-                                ctypes.c_double, ctypes.c_uint64,
-                                ctypes.c_double, ctypes.c_double,
-                                ctypes.c_double, ctypes.c_double,
-                                ctypes.c_double, ctypes.c_int,
-                                ctypes.c_double]
+    for fn in (lib.oracle_gain, lib.oracle_gain_f16):
+        fn.restype = ctypes.c_double
+        fn.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double,
+                       ctypes.c_uint64, ctypes.c_double, ctypes.c_double,
+                       ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                       ctypes.c_int, ctypes.c_double]
     lib.oracle_select.restype = ctypes.c_uint64
     lib.oracle_select.argtypes = [_f64p, _f64p, ctypes.c_uint64,
                                   ctypes.c_double, ctypes.c_int, _u8p]
@@ -191,10 +190,10 @@ class Oracle:
     def gain(self, n: int, B: int, q: float, R: int, alpha_s: float,
              bus_bw_Bps: float, t_hash_s: float = 0.0, t_cmp_s: float = 0.0,
              t_decmp_s: float = 0.0, overlapped: bool = True,
-             header_bytes: float = HEADER_BYTES) -> float:
-        return float(self._lib.oracle_gain(n, B, q, R, alpha_s, bus_bw_Bps,
-                                           t_hash_s, t_cmp_s, t_decmp_s,
-                                           int(overlapped), header_bytes))
+             header_bytes: float = HEADER_BYTES, fp16: bool = False) -> float:
+        fn = self._lib.oracle_gain_f16 if fp16 else self._lib.oracle_gain
+        return float(fn(n, B, q, R, alpha_s, bus_bw_Bps, t_hash_s, t_cmp_s,
+                        t_decmp_s, int(overlapped), header_bytes))
 
     def should_compress(self, *args, **kw) -> bool:
         """Section 3.2: keep a shard only when its gain is positive."""

@@ -37,7 +37,7 @@ class CieraError(RuntimeError):
 
 class ShardStats(ctypes.Structure):
     _fields_ = [("n_elems", ctypes.c_uint64), ("block_elems", ctypes.c_uint32),
-                ("q", ctypes.c_double)]
+                ("flags", ctypes.c_uint32), ("q", ctypes.c_double)]
 
 
 class CostModel(ctypes.Structure):
@@ -177,9 +177,10 @@ def ciera_encode_hashed(w_new, hash_in, hash_out, n_elems, block_elems, out,
 
 def ciera_should_compress(n_elems, block_elems, q, world_size, alpha_s,
                           bus_bw_Bps, t_hash_s=0.0, t_cmp_s=0.0, t_decmp_s=0.0,
-                          header_bytes=float(HEADER_BYTES), overlapped=True):
+                          header_bytes=float(HEADER_BYTES), overlapped=True,
+                          fp16=False):
     """Returns (decision 0/1, gain in seconds)."""
-    st = ShardStats(n_elems, block_elems, q)
+    st = ShardStats(n_elems, block_elems, FP16 if fp16 else 0, q)
     cm = CostModel(world_size, alpha_s, bus_bw_Bps, t_hash_s, t_cmp_s,
                    t_decmp_s, header_bytes, int(overlapped))
     g = ctypes.c_double(0.0)

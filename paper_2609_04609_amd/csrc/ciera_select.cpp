@@ -27,10 +27,15 @@ int ciera_should_compress(const ciera_shard_stats *stats,
   if (B == 0 || (B & (B - 1)) != 0) return CIERA_EUNSUPPORTED;
   if (!(stats->q >= 0.0 && stats->q <= 1.0)) return CIERA_EINVAL;
   if (model->world_size == 0 || !(model->bus_bw_Bps > 0.0)) return CIERA_EINVAL;
+  if (stats->flags & ~CIERA_FP16) return CIERA_EINVAL;
+  const bool f16 = stats->flags & CIERA_FP16;
   const double n = double(stats->n_elems);
-  const double S = 2.0 * n;     // bf16 bytes
-  const double S_e = n;         // one exponent byte per value
-  const double S_sm = S - S_e;  // one sign+mantissa byte per value
+  const double octets = double((stats->n_elems + 7) / 8);
+  const double S = 2.0 * n;  // 16-bit values
+  // bf16: one exponent byte and one sign+mantissa byte per value; fp16: five
+  // exponent bit planes, and the low mantissa byte plus three bit planes
+  const double S_e = f16 ? 5.0 * octets : n;
+  const double S_sm = f16 ? n + 3.0 * octets : n;
   const uint64_t blocks = (stats->n_elems + B - 1) / B;
   const double S_bm = double((blocks + 7) / 8);
   const double hops = double(model->world_size - 1);

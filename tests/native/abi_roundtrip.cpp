@@ -147,7 +147,7 @@ int main() {
 
   // the selection rule on this shard's measured change rate, with a slow
   // inter-node link where compression pays
-  ciera_shard_stats st = {n, B, 0.0};
+  ciera_shard_stats st = {n, B, 0u, 0.0};
   {
     const uint64_t nblk = (n + B - 1) / B;
     uint64_t changed = 0;

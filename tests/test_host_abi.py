@@ -214,6 +214,35 @@ def test_gain_hand_computed(cl, orc):
                                      rel_tol=1e-9)
 
 
+def test_gain_fp16_hand_computed(cl, orc):
+    """The same shard in fp16 (CIERA_FP16): its sections are S_{s+m} =
+    n + 3 ceil(n/8) and S_e = 5 ceil(n/8) bytes. By hand, n = 1e6 (125,000
+    octets), B = 512, q = 0.2, R = 16, alpha = 10 us, bw = 8 GB/s,
+    T_decmp = 1 ms, overlapped, 64-byte header:
+      payload  = 1,375,000 + 245 + 0.2 * 625,000 + 64 = 1,500,309 B
+      Comm(P)  = 1e-5 + 15 * 1,500,309 / 8e9          = 0.002823079375 s
+      g        = 0.00376 - 0.002823079375 - 0.001     = -0.000063079375 s
+    The bf16 shard of the same size gains (above); the fp16 one does not."""
+    dec, g = cl.ciera_should_compress(1_000_000, 512, 0.2, 16, 10e-6, 8e9,
+                                      t_decmp_s=1e-3, fp16=True)
+    assert dec == 0
+    assert math.isclose(g, -0.000063079375, rel_tol=1e-12)
+    go = orc.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_decmp_s=1e-3,
+                  fp16=True)
+    assert math.isclose(go, -0.000063079375, rel_tol=1e-12)
+    # a ragged n: ceil(n/8) octets; library and oracle agree over q
+    for q in np.linspace(0, 1, 11):
+        a = cl.ciera_should_compress(1_000_003, 64, float(q), 8, 5e-6, 50e9,
+                                     t_decmp_s=2e-5, fp16=True)[1]
+        b = orc.gain(1_000_003, 64, float(q), 8, 5e-6, 50e9, t_decmp_s=2e-5,
+                     fp16=True)
+        assert math.isclose(a, b, rel_tol=1e-12, abs_tol=1e-15)
+    # unknown flags are refused
+    st = cl.ShardStats(1000, 512, 0x80, 0.1)
+    cm = cl.CostModel(16, 1e-5, 8e9, 0.0, 0.0, 0.0, 64.0, 1)
+    assert cl.lib().ciera_should_compress(st, cm, None) == cl.EINVAL
+
+
 def test_gain_qualitative(cl, orc):
     n, B, R = 25_165_824, 512, 16
     qs = np.linspace(0, 1, 41)

@@ -74,6 +74,10 @@ MUTANTS = [
      "double sender = 0.0;"),
     ("gain drops the decode time", "return comm_raw - (comm_cmp + sender + t_decmp_s);",
      "return comm_raw - (comm_cmp + sender);"),
+    ("fp16 gain counts bf16 exponent bytes", "5.0 * octets, n, B, q, R,",
+     "8.0 * octets, n, B, q, R,"),
+    ("fp16 gain drops the bit planes", "(double)n + 3.0 * octets,",
+     "(double)n,"),
     ("hash word index off by one", "(j + 1u) * OR_SM64_GAMMA",
      "j * OR_SM64_GAMMA"),
     ("hash decision reads one half",
@@ -230,8 +234,11 @@ def _pins(o):
         g = o.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_decmp_s=1e-3)
         g2 = o.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_hash_s=2e-4,
                     t_cmp_s=4e-4, t_decmp_s=1e-3, overlapped=False)
+        g3 = o.gain(1_000_000, 512, 0.2, 16, 10e-6, 8e9, t_decmp_s=1e-3,
+                    fp16=True)
         return (abs(g - 0.000499420625) < 1e-12
-                and abs(g2 - (0.000499420625 - 6e-4)) < 1e-12)
+                and abs(g2 - (0.000499420625 - 6e-4)) < 1e-12
+                and abs(g3 + 0.000063079375) < 1e-12)
     check("gain", gain_hand)
 
     def hash_pins():
