@@ -438,7 +438,6 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
     ring[64 + lane] = block(1);
     uint32_t pre = block(2);      // the block after the window
     uint32_t next = 3, base = 0;  // word index of the window's first word
-    uint32_t wlim = nwords;       // words left in the stream from base
     __builtin_amdgcn_wave_barrier();
     bool bad = x < kAnsL;
     uint32_t rd = 0;
@@ -463,8 +462,9 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
       const uint32_t rel = __builtin_amdgcn_mbcnt_hi(
           uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), rd - base));
       // word base + rel of the stream sits at (base + rel) mod 256 of the ring
+      // a lane that reads past the stream's last word takes a word of
+      // padding or of the next block, and the check after the chunk fails
       const uint32_t w = ring16[(base + rel) & 255u];
-      bad = bad || (need && rel >= wlim);
       x = need ? ((x << 16) | w) : x;
       rd += uint32_t(__popcll(m));
       if (rd - base >= 128u) {  // uniform: slide the window by one block
@@ -473,14 +473,14 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
         __builtin_amdgcn_wave_barrier();
         pre = block(next++);
         base += 128u;
-        wlim = nwords > base ? nwords - base : 0u;
       }
     };
     const uint32_t full = len / 64;
     for (uint32_t t = 0; t < full; ++t)
       step(t, std::integral_constant<bool, false>{});
     if (len % 64) step(full, std::integral_constant<bool, true>{});
-    // every state back at L, the words used up, only zero padding after
+    // every state back at L, the words used up exactly (none read past the
+    // stream's end), only zero padding after
     bad = bad || x != kAnsL;
     const uint32_t used = 256u + 2u * rd;
     if (((used + 3u) & ~3u) != end - start) bad = true;

@@ -123,8 +123,9 @@ def test_update_cache_on_coded_shards(gu, orc, B):
 
 def test_ans_error_paths(gu, orc):
     """A coded shard met by a workspace without rANS room, and coded sections
-    with a wrong frequency table or a flipped stream byte: the device error
-    word says so and every access stays in bounds."""
+    with a wrong frequency table, a flipped stream byte or a stream cut
+    short: the device error word says so and every access stays in
+    bounds."""
     from paper_2609_04609_amd import ciera
     B, n = 512, 70001
     ws = ciera.Workspace(n, 1, B, ans=True)
@@ -164,6 +165,16 @@ def test_ans_error_paths(gu, orc):
     K = int(enc[sec:sec + 4].view(np.uint32)[0])
     bad = enc.copy()
     bad[sec + 520 + 4 * K + 4 * 7 + 1] ^= 0x40
+    ciera.decode_gathered_t(gu.dev_u8(bad), offs_t, n, B, out,
+                            gu.dev_u8(cache_h), ws)
+    torch.cuda.synchronize()
+    assert ws.error() & ciera.DEVERR_FORMAT
+    # the first chunk's stream cut 4 bytes short: its decoder needs words
+    # past the new end (taking padding or the next chunk's words instead)
+    assert K >= 2
+    bad = enc.copy()
+    ends = bad[sec + 520:sec + 520 + 4 * K].view(np.uint32)
+    ends[0] -= 4
     ciera.decode_gathered_t(gu.dev_u8(bad), offs_t, n, B, out,
                             gu.dev_u8(cache_h), ws)
     torch.cuda.synchronize()
