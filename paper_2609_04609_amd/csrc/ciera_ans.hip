@@ -30,6 +30,11 @@ namespace ciera {
 namespace {
 
 constexpr int kWaves = kThreads / 64;
+#ifndef CIERA_ANS_DEC_THREADS
+#define CIERA_ANS_DEC_THREADS 1024
+#endif
+// threads per rANS decode workgroup: its waves share one slot table
+constexpr int kAnsDecThreads = CIERA_ANS_DEC_THREADS;
 
 __device__ __forceinline__ void set_err(uint32_t *err, uint32_t bits) {
   __hip_atomic_fetch_or(err, bits, __ATOMIC_RELAXED,
@@ -356,12 +361,15 @@ __global__ __launch_bounds__(kThreads) void ans_copy_kernel(AnsEncArgs a) {
 // written over the block the window leaves. Any inconsistency sets
 // CIERA_DEVERR_FORMAT; every access stays inside the section and the shard's
 // exception list.
-__global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
+template <int NT>
+__global__ __launch_bounds__(NT) void ans_decode_kernel(DecArgs a) {
+  constexpr int NW = NT / 64;
+  static_assert(NT >= 256 && NT % 256 == 0, "a thread per symbol at least");
   __shared__ uint32_t s_slot[kAnsM];
   __shared__ uint32_t s_freq[256];
   __shared__ uint32_t s_cum[256];
-  __shared__ uint32_t s_red[kWaves];
-  __shared__ uint32_t s_ring[kWaves][128];  // two blocks of 128 words a wave
+  __shared__ uint32_t s_red[4];
+  __shared__ uint32_t s_ring[NW][128];  // two blocks of 128 words a wave
   const uint32_t j = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   // wave-uniform, so that the chunk loop and its lengths stay scalar
@@ -392,17 +400,35 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   const uint64_t want_k = (E + kAnsChunk - 1) / kAnsChunk;
   bool ok = K == want_k && ld32(sec + 4) == kAnsChunk &&
             C >= kAnsFixed + 4ull * K;
-  s_freq[tid] = reinterpret_cast<const uint16_t *>(sec + 8)[tid];
-  uint32_t total = 0;
-  const uint32_t cum = block_excl_scan32(s_freq[tid], s_red, &total);
-  s_cum[tid] = cum;
+  // the 256 frequencies (the first four waves), their total and exclusive
+  // prefix sums
+  uint32_t f = 0, inc = 0;
+  if (tid < 256) {
+    f = reinterpret_cast<const uint16_t *>(sec + 8)[tid];
+    s_freq[tid] = f;
+    inc = f;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t t = __shfl_up(inc, d, 64);
+      if (lane >= d) inc += t;
+    }
+    if (lane == 63) s_red[wave] = inc;
+  }
+  __syncthreads();
+  uint32_t before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) before += s_red[w];
+    total += s_red[w];
+  }
+  if (tid < 256) s_cum[tid] = before + inc - f;
   ok = ok && total == kAnsM;
   if (!ok) {
     if (blockIdx.x == 0 && tid == 0) set_err(a.err, CIERA_DEVERR_FORMAT);
     return;
   }
   __syncthreads();
-  for (uint32_t slot = uint32_t(tid); slot < kAnsM; slot += kThreads) {
+  for (uint32_t slot = uint32_t(tid); slot < kAnsM; slot += NT) {
     uint32_t lo = 0, hi = 255;  // largest s with cum[s] <= slot
     while (lo < hi) {
       const uint32_t mid = (lo + hi + 1) >> 1;
@@ -415,8 +441,8 @@ __global__ __launch_bounds__(kThreads) void ans_decode_kernel(DecArgs a) {
   const uint8_t *streams = sec + kAnsFixed + 4ull * K;
   const uint64_t avail = C - kAnsFixed - 4ull * K;
   uint8_t *const list = a.ans_exc + uint64_t(j) * a.ans_stride;
-  for (uint32_t c = blockIdx.x * kWaves + uint32_t(wave); c < K;
-       c += gridDim.x * kWaves) {
+  for (uint32_t c = blockIdx.x * NW + uint32_t(wave); c < K;
+       c += gridDim.x * NW) {
     const uint32_t start = c ? ends[c - 1] : 0u;
     const uint32_t end = ends[c];
     if (!(start <= end && end <= avail && ((start | end) & 3u) == 0 &&
@@ -513,12 +539,15 @@ hipError_t launch_ans_decode(const DecArgs &a, hipStream_t s) {
   if (a.ans_exc == nullptr || a.nshards == 0) return hipSuccess;
   const uint64_t kmax = ans_kmax(a.n);
   if (kmax == 0) return hipSuccess;
-  uint64_t g = (2048 + a.nshards - 1) / a.nshards;
-  const uint64_t need = (kmax + kWaves - 1) / kWaves;
+  // about 8192 waves over all shards
+  constexpr int NT = kAnsDecThreads;
+  constexpr uint32_t kGroups = 8192u / (NT / 64);
+  uint64_t g = (kGroups + a.nshards - 1) / a.nshards;
+  const uint64_t need = (kmax + NT / 64 - 1) / (NT / 64);
   if (g > need) g = need;
   if (g == 0) g = 1;
-  hipLaunchKernelGGL(ans_decode_kernel, dim3(uint32_t(g), a.nshards),
-                     dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(ans_decode_kernel<NT>, dim3(uint32_t(g), a.nshards),
+                     dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
