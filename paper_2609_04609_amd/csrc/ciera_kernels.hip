@@ -207,10 +207,23 @@ __device__ __forceinline__ uint32_t octet_valid(uint64_t elem, uint64_t n) {
 }
 
 // ------------------------------------------------------ wave/block sums ----
-__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+// Inclusive scan over the wave's 64 lanes with DPP moves (no LDS): shifts
+// by 1, 2, 4 and 8 lanes inside each row of 16 (lanes shifted in from
+// outside the row read 0), then row 15's last lane added into row 1 and
+// row 3, then lane 31 into rows 2 and 3.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x112, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x114, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x118, 0xF, 0xF, true));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x142, 0xA, 0xF, false));
+  v += uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x143, 0xC, 0xF, false));
   return v;
+}
+
+// The wave's sum, in every lane (lane 63 of the inclusive scan).
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+  return __builtin_amdgcn_readlane(wave_incl_scan(v), 63);
 }
 
 __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *s_red) {
@@ -223,15 +236,6 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *s_red) {
   return v;
 }
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t t = __shfl_up(v, d, 64);
-    if (lane >= d) v += t;
-  }
-  return v;
-}
 
 // Bit i set iff byte i of a and b differ (i = 0..3).
 __device__ __forceinline__ uint32_t bytes_ne4(uint32_t a, uint32_t b) {
