@@ -49,15 +49,15 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
 # scaled by what the counters read for a 1 GiB copy) for the kernel source
 # with this sha256; see profiles/hbm_traffic_*.md. Reported only while the
 # source is unchanged.
-_SRC_SHA = "4f3e2ccc33c96f9e23c26e54138f1f99679b69564517faf5c633536e5f288dd1"
+_SRC_SHA = "7e5e3300fe66aa558a1c83c045d67d15fef71df91be76207532b6519714d9fe0"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48941110471,
-                                  "encode": 423481321},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925493811,
+                                  "encode": 423388314},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1780000627,
-                                        "encode": 123684204},
+                                        "decode": 1780197091,
+                                        "encode": 123667677},
 }
 
 
