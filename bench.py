@@ -714,8 +714,8 @@ def cpu_baseline(S, budget_s=20.0):
     its receiver cache split from W just before use): the encode of rank 0's
     shard on one thread; the decode of gathered shards on one thread, shard
     after shard, for about a third of the budget; and the decode of every
-    one of the R shards with one shard per thread on up to 16 cores (the
-    host's share on the GPU machine), in rounds of one shard per thread. The step
+    one of the R shards with one shard per thread on up to 16 cores (a
+    host's share of cores per GPU), in rounds of one shard per thread. The step
     rate is encode + that all-core decode of all R shards."""
     import concurrent.futures as cf
     from oracle import oracle
