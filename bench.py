@@ -43,34 +43,43 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, 8 TB/s
 COPY_CAL_BYTES = 1 << 30
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_04609_amd", "csrc",
-                          "ciera_kernels.hip")
+# the kernels and their launch configuration (grids, tile orders, passes)
+KERNEL_SRC = [os.path.join(ROOT, "paper_2609_04609_amd", "csrc", f)
+              for f in ("ciera_kernels.hip", "ciera_internal.h",
+                        "ciera_api.cpp")]
 # HBM bytes per call measured with rocprofv3 FETCH_SIZE + WRITE_SIZE (each
-# scaled by what the counters read for a 1 GiB copy) for the kernel source
-# with this sha256; see profiles/hbm_traffic_*.md. Reported only while the
-# source is unchanged.
-_SRC_SHA = "7e5e3300fe66aa558a1c83c045d67d15fef71df91be76207532b6519714d9fe0"
+# scaled by what the counters read for a 1 GiB copy) for the sources whose
+# concatenation has this sha256; see profiles/hbm_traffic_*.md. Reported only
+# while those sources are unchanged.
+_SRC_SHA = "f15874ebf57f578ca5aeabcb7f99d7296a3384bd8810b4b1dd6081da83af268f"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925493811,
-                                  "encode": 423388314},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925855689,
+                                  "encode": 423374080},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1780197091,
-                                        "encode": 123667677},
+                                        "decode": 1778687596,
+                                        "encode": 123655069},
 }
 
 
 def measured_traffic(name, B, dtype="bf16"):
     """{"decode": bytes, "encode": bytes} of the current kernel source, or
     None when no counter run covers it."""
-    import hashlib
     rec = MEASURED_TRAFFIC.get((name, B, dtype))
     if rec is None:
         return None
-    with open(KERNEL_SRC, "rb") as f:
-        digest = hashlib.sha256(f.read()).hexdigest()
-    return rec if digest == rec["sha"] else None
+    return rec if source_digest() == rec["sha"] else None
+
+
+def source_digest():
+    """sha256 of the kernel and launch sources, concatenated in order."""
+    import hashlib
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 METRIC = ("encode & N-shard decode GB/s (bf16 weights), % HBM peak, "
