@@ -299,7 +299,12 @@ def _decode_case(gu, orc, R, n_s, B, raw_mask, seed):
 
 @pytest.mark.parametrize("B", [1, 16, 64, 512, 4096])
 @pytest.mark.parametrize("R,n_s", [(1, 1), (3, 16385), (4, 40000),
-                                   (5, 7777), (16, 16384), (2, 100003)])
+                                   (5, 7777), (16, 16384), (2, 100003),
+                                   # 310 decode tiles of 16384 values, the
+                                   # last of each shard ragged: runs of 32
+                                   # tiles per XCD over the first 256, the
+                                   # rest in order
+                                   (5, 1_000_003)])
 def test_decode_gathered_matches_oracle(gu, orc, B, R, n_s):
     from paper_2609_04609_amd import ciera
     raw_mask = [(j % 3) == 2 for j in range(R)]
