@@ -811,6 +811,84 @@ def spread(v):
     return [round(float(x), 2) for x in np.percentile(v, [10, 50, 90])]
 
 
+_PROBE = None
+
+
+def probe_lib():
+    """libciera_probe.so (built beside libciera.so by build()): the encode-
+    and decode-shaped stream probes."""
+    global _PROBE
+    if _PROBE is None:
+        import ctypes
+        path = os.path.join(ROOT, "paper_2609_04609_amd", "libciera_probe.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: run build() first")
+        lib = ctypes.CDLL(path)
+        for f in (lib.ciera_probe_encode_shaped, lib.ciera_probe_decode_shaped):
+            f.restype = ctypes.c_int
+            f.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_uint64,
+                                                  ctypes.c_void_p]
+        _PROBE = lib
+    return _PROBE
+
+
+def time_stream_ceiling(S, steps, stream, start):
+    """The codec step's access patterns with none of its arithmetic, timed in
+    the codec's own slots: `steps` more codec steps (continuing the W <-> W'
+    alternation from step `start`), each with the decode-shaped probe right
+    after its encode and the encode-shaped probe right after its decode.
+    encode-shaped: read 2n + n bytes, write n (the streaming pass's pattern);
+    decode-shaped: read R n + R n bytes, write 2 R n (the merge's)."""
+    import torch
+    from paper_2609_04609_amd import ciera
+    n, B, R = S.n, S.B, S.R
+    lib = probe_lib()
+    h = torch.cuda.current_stream().cuda_stream
+    scratch = torch.empty(n, dtype=torch.uint8, device=S.dev)
+    sm = S.gA[:R * n] if S.gA.numel() >= R * n else None
+    pe, pd = [], []
+    for i in range(steps + 2):
+        s = start + i
+        even = s % 2 == 0
+        w_in = S.W2[:n] if even else S.W[:n]
+        g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
+        ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
+                       update_cache=True)
+        sd = Span()
+        if sm is not None:
+            sd.arm(stream)
+            rc = lib.ciera_probe_decode_shaped(sm.data_ptr(), S.cache.data_ptr(),
+                                               S.out.data_ptr(), R * n, h)
+            sd.close(stream)
+            if rc:
+                raise RuntimeError("decode-shaped probe failed")
+        ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
+        se = Span()
+        se.arm(stream)
+        rc = lib.ciera_probe_encode_shaped(w_in.data_ptr(),
+                                           S.send_cache.data_ptr(),
+                                           scratch.data_ptr(), n, h)
+        se.close(stream)
+        if rc:
+            raise RuntimeError("encode-shaped probe failed")
+        if i >= 2:
+            pe.append(se)
+            if sm is not None:
+                pd.append(sd)
+    torch.cuda.synchronize()
+    last_even = (start + steps + 1) % 2 == 0
+    if not torch.equal(S.out, S.W2 if last_even else S.W):
+        raise RuntimeError("codec steps around the probes are not exact")
+    t_e = float(np.mean([x.us() for x in pe])) / 1e6
+    out = {"encode_shaped_us": round(t_e * 1e6, 2),
+           "encode_shaped_gbps": round(4 * n / t_e / 1e9, 1)}
+    if pd:
+        t_d = float(np.mean([x.us() for x in pd])) / 1e6
+        out["decode_shaped_us"] = round(t_d * 1e6, 2)
+        out["decode_shaped_gbps"] = round(4 * R * n / t_d / 1e9, 1)
+    return out
+
+
 def measure_layer(S, args, stream, decide_link_bps=8e9):
     """The timed codec steps of one Setup and their figures: per-phase times,
     algorithmic bytes and HBM fractions (decode and encode rooflines), the
@@ -835,6 +913,10 @@ def measure_layer(S, args, stream, decide_link_bps=8e9):
                                        start=args.warmup)
     t_enc = float(np.mean(enc_us)) / 1e6
     t_dec = float(np.mean(dec_us)) / 1e6
+    # an even number of steps (with the two warm-up ones) leaves the caches
+    # on the side the timed steps left them
+    ceil = time_stream_ceiling(S, 2 * max(1, args.steps // 4), stream,
+                               args.warmup + args.steps)
     t_upd = time_update_cache(S, args.steps, stream)
     # exponents that changed in rank 0's shard: the fused cache update's bytes
     d0 = ((S.W[:n].to(torch.int32) ^ S.W2[:n].to(torch.int32)) >> 7) & 0xFF
@@ -885,6 +967,18 @@ def measure_layer(S, args, stream, decide_link_bps=8e9):
                             "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                             "frac": round(enc_gbps / HBM_PEAK_GBPS, 4),
                             "traffic": tr["encode"] if tr else None},
+        "stream_ceiling": {
+            **ceil,
+            "encode_frac_of_stream": round(
+                enc_gbps / ceil["encode_shaped_gbps"], 4),
+            **({"decode_frac_of_stream": round(
+                dec_gbps / ceil["decode_shaped_gbps"], 4)}
+               if "decode_shaped_gbps" in ceil else {}),
+            "note": ("stream probes with the codec's access patterns and no "
+                     "codec arithmetic, timed in its slots of the step: "
+                     "encode-shaped after the decode (4n bytes), "
+                     "decode-shaped after the encode (4Rn bytes); the "
+                     "fractions compare algorithmic GB/s")},
         "wire_ratio": round(sum(S.totA) / (2.0 * R * n), 5),
         "q_blocks": round(q, 5),
         "exceptions_local": E_A[0],
@@ -949,6 +1043,7 @@ def run(args):
                 rec["encode"]["hbm_gbps"] / copy_gbps, 4),
             "note": "a plain 2 GiB device copy (torch copy_), read + write "
                     "bytes per second"},
+        "stream_ceiling": rec["stream_ceiling"],
         "verified": rec["verified"],
         "timing": ("HIP events recorded on the kernels' stream right "
                    "before and after each call (" +

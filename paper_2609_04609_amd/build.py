@@ -1,4 +1,5 @@
-"""Build libciera.so in-tree for gfx950 (hipcc cross-compiles without a GPU).
+"""Build libciera.so in-tree for gfx950 (hipcc cross-compiles without a GPU),
+and libciera_probe.so, the benchmark's stream probes (not part of the codec).
 
     python -m paper_2609_04609_amd.build
 """
@@ -12,6 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libciera.so")
+PROBE_LIB = os.path.join(PKG, "libciera_probe.so")
+PROBE_SOURCE = "stream_probe.hip"
 SOURCES = ["ciera_kernels.hip", "ciera_ans.hip", "ciera_api.cpp",
            "ciera_select.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -44,7 +47,19 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    build_probe(verbose)
     return LIB
+
+
+def build_probe(verbose: bool = False) -> str:
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, "-shared",
+           os.path.join(CSRC, PROBE_SOURCE), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":
