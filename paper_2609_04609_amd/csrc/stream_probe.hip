@@ -9,7 +9,9 @@
 //     update, one wave per 4096 values.
 //   decode-shaped: per value read 1 byte (sign|mantissa) and 1 byte (the
 //     exponent), write 2 bytes, all non-temporal: the access pattern of the
-//     merge, one 256-thread workgroup per 16384 values.
+//     merge, one 256-thread workgroup per 16384 values, the tiles walked in
+//     runs of 32 per XCD as the merge walks them (1-2.5% faster than in
+//     order on the DeepSeek-style layer's buffers).
 //
 // n must be a multiple of 8 and every pointer 16-byte aligned (checked on
 // the host; the call returns hipErrorInvalidValue otherwise).
@@ -73,7 +75,15 @@ __global__ __launch_bounds__(256) void encode_shaped_kernel(
 __global__ __launch_bounds__(256) void decode_shaped_kernel(
     const uint8_t *sm, const uint8_t *c, uint16_t *out, uint64_t n) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint64_t base = uint64_t(blockIdx.x) * kDecTile;
+  // workgroup L = 8k + x (XCD x, its k-th) takes tile
+  // (k / 32) 256 + 32 x + k mod 32; the tail short of 256 tiles keeps its
+  // place
+  uint64_t L = blockIdx.x;
+  if (L < ((uint64_t(gridDim.x) >> 8) << 8)) {
+    const uint64_t k = L >> 3;
+    L = ((k >> 5) << 8) | ((L & 7u) << 5) | (k & 31u);
+  }
+  const uint64_t base = L * kDecTile;
   uint2 sv[8], ev[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) {

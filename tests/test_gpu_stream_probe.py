@@ -21,7 +21,8 @@ def test_probe_library_exports_its_two_calls():
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("n", [8, 4096, 16384 * 3 + 8, 1 << 20])
+@pytest.mark.parametrize("n", [8, 4096, 16384 * 3 + 8, 1 << 20,
+                               16384 * 300 + 8])  # 301 tiles: runs and tail
 def test_probes_compute_their_byte_maps(n):
     import torch
     import bench
