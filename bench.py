@@ -349,10 +349,11 @@ def time_small_configs(B, dev, steps, stream):
     return out
 
 
-def time_mixed_layer(B, dev, steps, stream):
+def time_mixed_layer(B, dev, steps, stream, warmup_regime=False):
     """One layer of the mixed model step (attention q/k/v/o, router, two
     layer norms and the 64-expert group, 16 shards each) at the steady
-    per-type change rates. The Section 3.2 rule decides per tensor on an
+    per-type change rates, or in the warm-up regime (30% of every tensor's
+    exponents change). The Section 3.2 rule decides per tensor on an
     xGMI-class link (alpha 10 us, 150 GB/s per peer) from the block change
     rate of this step's data, with a modelled decode time; the selected
     tensors form one compressed group and the rest one raw group, and the
@@ -371,7 +372,8 @@ def time_mixed_layer(B, dev, steps, stream):
                 n, 0.02, synth.seed_for("mixed", 0, name, j), dev)
             W[j * n:(j + 1) * n] = w
             W2[j * n:(j + 1) * n] = synth.forced_bernoulli_bits(
-                w, synth.STEADY_RATE[kind],
+                w, synth.WARMUP_RATE if warmup_regime else
+                synth.STEADY_RATE[kind],
                 synth.seed_for("mixed", 0, name, "u", j))
         e1 = (W.view(R, n).to(torch.int32) >> 7) & 0xFF
         e2 = (W2.view(R, n).to(torch.int32) >> 7) & 0xFF
@@ -387,8 +389,9 @@ def time_mixed_layer(B, dev, steps, stream):
         del e1, e2, d
     res = {"workload": ("mixed model step, one of 16 identical layers: "
                         "q/k/v/o 2048x2048, router 2048x64, 2 layer norms "
-                        "of 2048, 64 experts x 3 matrices; R=16, steady "
-                        "per-type rates"),
+                        "of 2048, 64 experts x 3 matrices; R=16, " +
+                        ("warm-up regime, 30% of exponents change"
+                         if warmup_regime else "steady per-type rates")),
            "compressed": sorted(k for k, v in dec.items() if v),
            "raw": sorted(k for k, v in dec.items() if not v)}
     total_us, vals = 0.0, 0
@@ -1084,6 +1087,16 @@ def run(args):
                                                   stream)
         res["mixed_layer"] = time_mixed_layer(512, dev,
                                               min(args.steps, 20), stream)
+        res["mixed_layer_warmup"] = time_mixed_layer(
+            512, dev, min(args.steps, 20), stream, warmup_regime=True)
+        # the OLMoE layer's other forced change rates (1% and 5%)
+        for name in ("olmoe_layer_c1", "olmoe_layer_c5"):
+            Sr = Setup(synth.WORKLOADS[name], 512, dev)
+            rr = measure_layer(Sr, args, stream)
+            rr.pop("_cache_is_w2")
+            res[name] = rr
+            del Sr
+            torch.cuda.empty_cache()
     if args.copy_calibration:
         # a plain device copy of a known size, for scaling the HBM byte
         # counters of a rocprofv3 --pmc run of this same command
