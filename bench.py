@@ -265,6 +265,47 @@ class Setup:
         return g, off_t, totals
 
 
+def codec_step(S, s, stream, se=None, sd=None):
+    """Step s of the codec on a Setup: rank 0's encode (bringing its cache
+    forward; raw groups encode raw), then the gathered decode. Even steps go
+    W -> W', odd steps back. se and sd (Spans) time the two calls."""
+    from paper_2609_04609_amd import ciera
+    n, B = S.n, S.B
+    even = (s % 2) == 0
+    w_in = S.W2[:n] if even else S.W[:n]
+    g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
+    if se is not None:
+        se.arm(stream)
+    if S.raw:
+        ciera.encode_t(w_in, None, B, S.ws_enc, S.tmp, raw=True)
+    else:
+        ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
+                       update_cache=True)
+    if se is not None:
+        se.close(stream)
+        sd.arm(stream)
+    ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
+    if sd is not None:
+        sd.close(stream)
+
+
+def check_last_step(S, last):
+    """The encoded bytes, decoded values and caches after step `last`, bit
+    for bit, and no device error; raises otherwise."""
+    import torch
+    n = S.n
+    last_even = last % 2 == 0
+    expect = S.W2 if last_even else S.W
+    ok = bool(torch.equal(S.out, expect))
+    if not S.raw:
+        g, t = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
+        ok = ok and bool(torch.equal(S.cache[:n], S.send_cache)) and \
+            bool(torch.equal(S.tmp[:t], g[:t]))
+    errs = S.ws_enc.error() | S.ws_dec.error()
+    if not ok or errs:
+        raise RuntimeError(f"codec steps are not exact (err={errs})")
+
+
 def timed_steps(S, warmup, steps, stream, decide=None, start=0):
     """The codec step on a Setup (rank 0's encode, bringing its cache
     forward, then the gathered decode; raw groups encode raw), alternating
@@ -275,28 +316,11 @@ def timed_steps(S, warmup, steps, stream, decide=None, start=0):
     time per step (s). The last step's encoded bytes, decoded values and
     caches are checked bit for bit."""
     import torch
-    from paper_2609_04609_amd import ciera
-    n, B = S.n, S.B
 
     def one(s, se, sd):
-        even = (s % 2) == 0
-        w_in = S.W2[:n] if even else S.W[:n]
-        g, off = (S.gA, S.offA) if even else (S.gB, S.offB)
         if decide is not None:
             decide(s)
-        if se is not None:
-            se.arm(stream)
-        if S.raw:
-            ciera.encode_t(w_in, None, B, S.ws_enc, S.tmp, raw=True)
-        else:
-            ciera.encode_t(w_in, S.send_cache, B, S.ws_enc, S.tmp,
-                           update_cache=True)
-        if se is not None:
-            se.close(stream)
-            sd.arm(stream)
-        ciera.decode_gathered_t(g, off, n, B, S.out, S.cache, S.ws_dec)
-        if sd is not None:
-            sd.close(stream)
+        codec_step(S, s, stream, se, sd)
 
     for s in range(warmup):
         one(start + s, None, None)
@@ -307,16 +331,7 @@ def timed_steps(S, warmup, steps, stream, decide=None, start=0):
         one(start + warmup + s, *spans[s])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
-    last_even = (start + warmup + steps - 1) % 2 == 0
-    expect = S.W2 if last_even else S.W
-    ok = bool(torch.equal(S.out, expect))
-    if not S.raw:
-        g, t = (S.gA, S.totA[0]) if last_even else (S.gB, S.totB[0])
-        ok = ok and bool(torch.equal(S.cache[:n], S.send_cache)) and \
-            bool(torch.equal(S.tmp[:t], g[:t]))
-    errs = S.ws_enc.error() | S.ws_dec.error()
-    if not ok or errs:
-        raise RuntimeError(f"codec steps are not exact (err={errs})")
+    check_last_step(S, start + warmup + steps - 1)
     enc = [se.us() for se, _ in spans]
     dec = [sd.us() for _, sd in spans]
     return enc, dec, wall
@@ -328,22 +343,63 @@ def codec_steps(S, warmup, steps, stream):
     return float(np.mean(enc)) / 1e6, float(np.mean(dec)) / 1e6, wall
 
 
+def graph_steps(S, reps, start):
+    """The codec step from a HIP graph: steps start and start + 1 (one each
+    way, so that replays continue the alternation) captured once, then
+    replayed `reps` times between two events on the current stream; the
+    library's calls launch kernels only, so they capture as they are.
+    Returns us per step; the state after the last replay is checked bit for
+    bit."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # one eager pair on a side stream first
+        codec_step(S, start, side)
+        codec_step(S, start + 1, side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cap = torch.cuda.current_stream()
+        codec_step(S, start, cap)
+        codec_step(S, start + 1, cap)
+    graph.replay()  # the first replay uploads the graph
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    check_last_step(S, start + 1)
+    us = a.elapsed_time(b) * 1e3 / (2 * reps)
+    del graph
+    return us
+
+
 def time_small_configs(B, dev, steps, stream):
     """The tiny tensor and the single OLMoE expert (natural update, and 1%
-    of exponents forced), R shards each: the codec step as for the layer.
-    These sizes measure launch latency more than bandwidth."""
+    of exponents forced), R shards each: the codec step as for the layer,
+    called from Python, and the same step replayed from a HIP graph
+    (us_per_step_graph). These sizes measure launch latency more than
+    bandwidth."""
     from paper_2609_04609_amd import synth
     out = {}
     for name in ("tiny", "olmoe_expert", "olmoe_expert_forced"):
         wl = synth.WORKLOADS[name]
         S = Setup(wl, B, dev)
         t_enc, t_dec, wall = codec_steps(S, 10, steps, stream)
+        us_graph = graph_steps(S, max(steps, 10), 10 + steps)
         n, R = S.n, S.R
         out[name] = {"workload": describe(wl, B),
                      "us_per_step": round(wall * 1e6, 2),
                      "encode_us": round(t_enc * 1e6, 2),
                      "decode_us": round(t_dec * 1e6, 2),
                      "bf16_gbps": round((2 * n + 2 * R * n) / wall / 1e9, 1),
+                     "us_per_step_graph": round(us_graph, 2),
+                     "bf16_gbps_graph": round((2 * n + 2 * R * n) /
+                                              (us_graph * 1e-6) / 1e9, 1),
                      "wire_ratio": round(sum(S.totA) / (2.0 * R * n), 5)}
         del S
     return out
