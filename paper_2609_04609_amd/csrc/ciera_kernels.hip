@@ -11,17 +11,18 @@
 //                sign+mantissa plane, the bitmap and a changed-block count
 //                per tile, streaming at copy speed;
 //            (2) the exponents of the changed blocks, in block order, read
-//                back from W' for those blocks only, and the header:
-//                encode_exc_blocks_kernel (B = 16 ... 256, lanes over the
-//                changed blocks), encode_exc_rows_kernel (B >= 512, over the
-//                changed 512-value rows), encode_exc_elems_kernel (B = 1).
-//                A workgroup finds its first exception by counting the
-//                bitmap bits in front of it (the bitmap is 1/(8B) of the
-//                shard and stays in L2); at B = 1, and where that count
-//                would re-read too much, a scan_counts_kernel over pass 1's
-//                per-tile counts stands in for it.
+//                back for those blocks only (from the cache pass 1 brought
+//                forward with the fused cache update, else from W'), and
+//                the header: encode_exc_blocks_kernel (B = 16 ... 256, lanes
+//                over the changed blocks), encode_exc_rows_kernel (B >= 512,
+//                over the changed 512-value rows), encode_exc_elems_kernel
+//                (B = 1). A workgroup finds its first exception by counting
+//                the bitmap bits in front of it (the bitmap is 1/(8B) of the
+//                shard and stays in L2), or at B = 1 by adding up pass 1's
+//                per-tile counts in front of it; where either would re-read
+//                too much, a scan_counts_kernel over those counts stands in.
 //            No workgroup ever waits on another: compacting the exception
-//            list costs one re-read of the changed blocks (2 bytes per
+//            list costs one re-read of the changed blocks (1 or 2 bytes per
 //            changed value) instead of a cross-workgroup scan whose waits
 //            would hold every tile's slot behind its slowest predecessor.
 //   decode   for all R gathered shards at once: ExpCache patch + Merge. Each
@@ -851,29 +852,59 @@ __device__ void exc_finish(const EncArgs &a, uint64_t total_changed,
   for (uint64_t i = S_exc + lane; i < pad16(S_exc); i += 64) exc_out[i] = 0;
 }
 
+// This thread's share of the 32-bit counts c[0, count) (c 16-byte
+// aligned): every load issued before the first add, as in popc_bytes_part.
+// Sum it over the workgroup with block_sum.
+template <uint32_t L>
+__device__ __forceinline__ uint32_t sum_words_part(const uint32_t *c,
+                                                   uint64_t count) {
+  if (!count) return 0u;
+  const uint64_t full4 = count >> 2;
+  const uint64_t ti = (full4 << 2) + threadIdx.x;  // < 4 tail words
+  const uint32_t tw = c[ti < count ? ti : count - 1];
+  const uint4 *c4 = reinterpret_cast<const uint4 *>(c);
+  uint32_t s = 0;
+  for (uint64_t i0 = 0; i0 < full4; i0 += L * kThreads) {
+    uint4 v[L];
+#pragma unroll
+    for (uint32_t j = 0; j < L; ++j) {
+      const uint64_t i = i0 + j * kThreads + threadIdx.x;
+      v[j] = c4[i < full4 ? i : full4 - 1];
+    }
+#pragma unroll
+    for (uint32_t j = 0; j < L; ++j) {
+      const uint64_t i = i0 + j * kThreads + threadIdx.x;
+      s += i < full4 ? v[j].x + v[j].y + v[j].z + v[j].w : 0u;
+    }
+  }
+  return s + (ti < count ? tw : 0u);
+}
+
 // Pass 2 for B = 1: the tile's changed values, at the tile's offset in the
-// list (from the scanned per-tile counts of pass 1); the last tile writes
-// the header. W' is read again only where the bitmap says so.
+// list: the per-tile counts of pass 1 in front of the tile, summed here by
+// the workgroup, or (a.scan_prefix) read from their scan. The last tile
+// writes the header. W' is read again only where the bitmap says so.
 template <bool VEC, bool FROMC>
 __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
     EncArgs a) {
   using Src = ExcSrc<VEC, false, FROMC>;
+  __shared__ uint32_t s_red[4];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t nt = a.num_tiles;
   const uint32_t tile = blockIdx.x * 4u + wave;
-  if (tile >= a.num_tiles) return;
+  const bool live = tile < nt;  // every wave takes part in the count
   const uint64_t n = a.n;
   const uint64_t tbase = uint64_t(tile) * a.tile_elems;
   const uint64_t n16 = pad16(sm_bytes(n, false));
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
   uint8_t *const exc_out =
       a.out + kHeaderBytes + n16 + pad16(bitmap_bytes(n, 0));
-  const uint32_t prefix = a.counts[tile];
   uint32_t mask[8], excl[8];
   uint32_t run = 0;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
-    const uint32_t valid = octet_valid(elem, n);
+    const uint32_t valid = live ? octet_valid(elem, n) : 0u;
     mask[u] = valid ? uint32_t(bmp[elem >> 3]) & ((1u << valid) - 1u) : 0u;
     const uint32_t c = __popc(mask[u]);
     const uint32_t incl = wave_incl_scan(c);
@@ -886,6 +917,17 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
     const uint64_t elem = tbase + (uint64_t(u) * 64 + lane) * 8;
     if (mask[u]) wv[u] = Src::load(a, elem, octet_valid(elem, n));
   }
+  uint32_t prefix;
+  if (a.scan_prefix) {
+    prefix = live ? a.counts[tile] : 0u;
+  } else {
+    const uint32_t g0 = min(blockIdx.x * 4u, nt);
+    const uint32_t cg = sum_words_part<kGroupLoads>(a.counts, g0);
+    const uint32_t cs =
+        (lane < wave && g0 + lane < nt) ? a.counts[g0 + lane] : 0u;
+    prefix = block_sum(cg, s_red) + wave_sum(cs);
+  }
+  if (!live) return;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     uint32_t mm = mask[u];
@@ -899,8 +941,10 @@ __global__ __launch_bounds__(kThreads) void encode_exc_elems_kernel(
       mm &= mm - 1u;
     }
   }
-  if (tile == a.num_tiles - 1)
-    exc_finish<true, false>(a, uint64_t(a.counts[a.num_tiles]), lane);
+  if (tile == nt - 1)
+    exc_finish<true, false>(
+        a, a.scan_prefix ? uint64_t(a.counts[nt]) : uint64_t(prefix) + run,
+        lane);
 }
 
 // Pass 2 for B >= 512. A row of 512 values lies inside one block, so it is
@@ -1828,7 +1872,7 @@ hipError_t launch_encode(const EncArgs &a, bool vec, hipStream_t s) {
     if (vec) exact(bool_c<true>{}, bool_c<false>{}, bool_c<false>{});
     else exact(bool_c<false>{}, bool_c<false>{}, bool_c<false>{});
   }
-  if (elems || a.scan_prefix)
+  if (a.scan_prefix)
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(kScanThreads), 0, s,
                        a.counts, a.num_tiles, uint64_t(0));
   if (elems) {
