@@ -51,15 +51,15 @@ KERNEL_SRC = [os.path.join(ROOT, "paper_2609_04609_amd", "csrc", f)
 # scaled by what the counters read for a 1 GiB copy) for the sources whose
 # concatenation has this sha256; see profiles/hbm_traffic_*.md. Reported only
 # while those sources are unchanged.
-_SRC_SHA = "f15874ebf57f578ca5aeabcb7f99d7296a3384bd8810b4b1dd6081da83af268f"
+_SRC_SHA = "2efe8aae0dd2f8b9fb1b4127d7cdaf90de25cd7e214f141862976c07602fc2c2"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925855689,
-                                  "encode": 423374080},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925217130,
+                                  "encode": 423520205},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1778687596,
-                                        "encode": 123655069},
+                                        "decode": 1778735340,
+                                        "encode": 123681411},
 }
 
 
