@@ -128,14 +128,22 @@ bool dec_workspace_ok(uint64_t n, uint32_t nshards, uint64_t bytes) {
 // Every decode tile needs the flagged blocks in front of it. Counting them in
 // the tile re-reads half the shard's bitmap per tile on average, which grows
 // with tiles x bitmap; past about 20 us of such reads (128 MB) one prefix
-// pass over the bitmaps is cheaper than its extra launch.
+// pass over the bitmaps is cheaper than its extra launch. At B = 1 a count
+// kernel takes every tile's bitmap bits first, and each merge workgroup adds
+// up the 32-bit counts in front of its tile (tiles x tiles x 2 bytes per
+// shard) unless that passes 128 MB, where a scan of the counts runs instead:
+// 16 shards of 25.2M values (1,536 tiles each, 75 MB) decode in 294-298 us
+// that way against 303-306 us with the scan (three processes, libraries
+// taking turns on the same buffers).
 // The gathered decode walks its tiles in runs of 32 per XCD, with or
 // without the prefix pass (measured with libraries taking turns on the same
 // buffers: 3-7% faster than in order on the DeepSeek-style layer, 0.5% on
 // the OLMoE layer; runs of 8 to 128 within 0.5% of 32).
 constexpr uint32_t kXcdRunLog2 = 5;
 bool use_prefix_pass(uint64_t n, uint32_t nshards, int l) {
-  if (l == 0) return false;
+  if (l == 0)
+    return uint64_t(nshards) * dec_tiles(n) * dec_tiles(n) * 2 >
+           kPrefixPassBytes;
   const uint64_t inline_bytes = uint64_t(nshards) * dec_tiles(n) *
                                 bitmap_bytes(n, uint32_t(l)) / 2;
   return inline_bytes > kPrefixPassBytes;

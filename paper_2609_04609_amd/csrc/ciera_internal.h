@@ -153,7 +153,10 @@ struct DecArgs {
   // per shard and decode tile: the flagged blocks (B >= 16) or changed values
   // (B = 1) in front of the tile, dec_count_stride(tiles) words per shard
   uint32_t *tile_excl;
-  bool prefix_pass;  // B >= 16: tile_excl was filled by tile_prefix_kernel
+  // B >= 16: tile_excl was filled by tile_prefix_kernel; B = 1: the per-tile
+  // counts in tile_excl are scanned (scan_counts_kernel) before the merge,
+  // which otherwise adds up the counts in front of each tile itself
+  bool prefix_pass;
   uint32_t xcd_run_log2;  // B >= 16: log2 of the tiles per XCD turn (0: in order)
 };
 

@@ -28,8 +28,10 @@
 //   decode   for all R gathered shards at once: ExpCache patch + Merge. Each
 //            tile finds its first exception by counting the bitmap bits in
 //            front of it (the bitmap is 1/(8B) of the shard and stays in L2),
-//            so decode tiles never wait on each other. At B = 1 a count and a
-//            scan kernel give every tile its first exception.
+//            so decode tiles never wait on each other. At B = 1 a count
+//            kernel takes every tile's bitmap bits first, and each tile adds
+//            up the counts in front of it (or, past 128 MB of such reads, a
+//            scan of the counts runs in between).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -1642,7 +1644,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecArgs a) {
 // byte o, and the exception list holds the changed exponent bytes in value
 // order (the encoder is encode_pass_kernel<..., true, ...>). Within a decode tile
 // the octets are ranked by a wave scan per 64-octet segment and a scan of the
-// segment totals; a per-shard scan of per-tile counts gives the tile start.
+// segment totals; the per-tile counts in front of the tile (added up by the
+// tile's workgroup, or scanned per shard) give the tile start.
 
 // Exclusive rank of this lane's octet among the set bits of its tile, for
 // every u; returns the tile total. `cnt[u]` are the per-octet bit counts.
@@ -1702,11 +1705,13 @@ __global__ __launch_bounds__(kThreads) void count_tile_bits_kernel(
   if (lane == 0) a.tile_excl[uint64_t(j) * dec_count_stride(tiles) + t] = c;
 }
 
-// Decode, B = 1, step 3: patch and merge (UPDATE_ONLY: patch only).
+// Decode, B = 1, step 2 (step 3 after a scan of the counts): patch and merge
+// (UPDATE_ONLY: patch only).
 template <int OCT, bool VEC, bool UPDATE_ONLY>
 __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
   constexpr uint32_t T = kThreads * 8 * OCT;
   __shared__ uint32_t s_seg[4 * OCT + 1];
+  __shared__ uint32_t s_red[4];
 
   const uint32_t j = blockIdx.y;
   const uint32_t t = blockIdx.x;
@@ -1741,8 +1746,6 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
   const uint8_t *const bmp = sm_in + pad16(n);
   const uint8_t *const exc = bmp + pad16((n + 7) / 8);
   const uint32_t tiles = uint32_t(dec_tiles(n));
-  const uint32_t tile_first =
-      a.tile_excl[uint64_t(j) * dec_count_stride(tiles) + t];
   const bool full = VEC && base + T <= n;
 
   uint32_t mask[OCT], cnt[OCT];
@@ -1769,6 +1772,13 @@ __global__ __launch_bounds__(kThreads) void decode_elems_kernel(DecArgs a) {
       }
     }
   }
+  // the changed values in front of the tile: scanned, or the counts in
+  // front of it added up here, its loads behind the tile's own
+  const uint32_t *const counts =
+      a.tile_excl + uint64_t(j) * dec_count_stride(tiles);
+  const uint32_t tile_first =
+      a.prefix_pass ? counts[t]
+                    : block_sum(sum_words_part<kGroupLoads>(counts, t), s_red);
   uint32_t excl[OCT];
   rank_octets<OCT>(cnt, excl, s_seg);
 
@@ -1950,9 +1960,10 @@ hipError_t launch_decode(const DecArgs &a, bool vec, hipStream_t s) {
     const dim3 cgrid(uint32_t((tiles + 3) / 4), a.nshards);
     hipLaunchKernelGGL(count_tile_bits_kernel, cgrid, block, 0, s, a,
                        uint32_t(tiles));
-    hipLaunchKernelGGL(scan_counts_kernel, dim3(a.nshards),
-                       dim3(kScanThreads), 0, s, a.tile_excl, uint32_t(tiles),
-                       dec_count_stride(tiles));
+    if (a.prefix_pass)
+      hipLaunchKernelGGL(scan_counts_kernel, dim3(a.nshards),
+                         dim3(kScanThreads), 0, s, a.tile_excl,
+                         uint32_t(tiles), dec_count_stride(tiles));
     constexpr int O = int(kDecOct);
     if (upd) {
       if (vec)
