@@ -413,8 +413,9 @@ def time_mixed_layer(B, dev, steps, stream, warmup_regime=False):
     xGMI-class link (alpha 10 us, 150 GB/s per peer) from the block change
     rate of this step's data, with a modelled decode time; the selected
     tensors form one compressed group and the rest one raw group, and the
-    layer's codec step is both groups' steps. All 16 layers of the model
-    have this shape and these rates."""
+    layer's codec step is both groups' steps, called from Python and also
+    replayed from HIP graphs. All 16 layers of the model have this shape
+    and these rates."""
     import torch
     from paper_2609_04609_amd import ciera, synth
     R = synth.MIXED_SHARDS
@@ -450,7 +451,7 @@ def time_mixed_layer(B, dev, steps, stream, warmup_regime=False):
                          if warmup_regime else "steady per-type rates")),
            "compressed": sorted(k for k, v in dec.items() if v),
            "raw": sorted(k for k, v in dec.items() if not v)}
-    total_us, vals = 0.0, 0
+    total_us, total_graph_us, vals = 0.0, 0.0, 0
     for raw in (False, True):
         names = [nm for nm, _, _ in synth.MIXED_TENSORS
                  if bool(dec[nm]) != raw]
@@ -468,17 +469,22 @@ def time_mixed_layer(B, dev, steps, stream, warmup_regime=False):
                 off += n
         S = Setup.from_tensors(Wf, W2f, R, n_flat, B, dev, raw=raw)
         t_enc, t_dec, wall = codec_steps(S, 5, steps, stream)
+        us_graph = graph_steps(S, max(steps, 10), 5 + steps)
         key = "raw_group" if raw else "compressed_group"
         res[key] = {"values_per_shard": n_flat,
                     "us_per_step": round(wall * 1e6, 2),
                     "encode_us": round(t_enc * 1e6, 2),
                     "decode_us": round(t_dec * 1e6, 2),
+                    "us_per_step_graph": round(us_graph, 2),
                     "wire_ratio": round(sum(S.totA) / (2.0 * R * n_flat), 5)}
         total_us += wall * 1e6
+        total_graph_us += us_graph
         vals += R * n_flat
         del S, Wf, W2f
     res["us_per_layer"] = round(total_us, 2)
     res["bf16_gbps"] = round(2 * vals / (total_us * 1e-6) / 1e9, 1)
+    # the same two group steps, each replayed from a HIP graph
+    res["us_per_layer_graph"] = round(total_graph_us, 2)
     return res
 
 
