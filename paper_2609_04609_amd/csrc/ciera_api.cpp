@@ -140,6 +140,17 @@ bool dec_workspace_ok(uint64_t n, uint32_t nshards, uint64_t bytes) {
 // buffers: 3-7% faster than in order on the DeepSeek-style layer, 0.5% on
 // the OLMoE layer; runs of 8 to 128 within 0.5% of 32).
 constexpr uint32_t kXcdRunLog2 = 5;
+// Pass 1 of the encode walks its workgroups in runs of 32 per XCD when the
+// exception pass gives each wave several tiles (B >= 16). With one tile a
+// wave (and always at B = 1) the exception pass's workgroup w covers pass
+// 1's workgroup w's tiles on the same XCD, whose L2 still holds the cache
+// bytes it reads back, and runs would break that. Libraries taking turns on
+// the same buffers: the DeepSeek-style shard (three tiles a wave) encodes
+// in 68.2-68.4 us with runs against 68.8-69.1 us in order; the OLMoE shard
+// (one tile a wave) in 25.2 us with runs against 23.5 us in order.
+bool enc_xcd_runs(uint64_t tiles, int l) {
+  return l > 0 && exc_tiles_per_wave(tiles, uint32_t(l)) >= 2;
+}
 bool use_prefix_pass(uint64_t n, uint32_t nshards, int l) {
   if (l == 0)
     return uint64_t(nshards) * dec_tiles(n) * dec_tiles(n) * 2 >
@@ -219,6 +230,7 @@ int encode_compressed(const uint16_t *w_new, const uint8_t *exp_cache,
   a.f16 = f16;
   a.scan_prefix = use_count_scan(n_elems, l);
   a.exc_tiles_per_wave = exc_tiles_per_wave(tiles, l);
+  a.xcd_run_log2 = enc_xcd_runs(tiles, l) ? kXcdRunLog2 : 0u;
   const bool vec = aligned(w_new, 16) && aligned(exp_cache, 8);
   return launch_encode(a, vec, stream) == hipSuccess ? CIERA_OK : CIERA_EHIP;
 }

@@ -350,7 +350,19 @@ __global__ __launch_bounds__(kThreads) void encode_pass_kernel(EncArgs a) {
   static_assert(!(HASH && ELEMS), "the block hash needs B >= 16");
   static_assert(!(F16 && (HASH || ELEMS)), "fp16: exact compare, B >= 16");
   const uint32_t lane = threadIdx.x & 63;
-  const uint32_t tile = blockIdx.x * 4u + (threadIdx.x >> 6);
+  // Workgroup L = 8k + x runs on XCD x as its k-th. With runs of
+  // G = 2^a.xcd_run_log2 workgroups it takes the tiles of workgroup
+  // (k / G) 8G + x G + k mod G, so each XCD streams G neighbouring
+  // workgroups' tiles at a time; the tail short of 8G keeps the plain order.
+  uint32_t grp = blockIdx.x;
+  if (a.xcd_run_log2) {
+    const uint32_t g = a.xcd_run_log2;
+    if (grp < ((gridDim.x >> (g + 3)) << (g + 3))) {
+      const uint32_t k = grp >> 3;
+      grp = ((k >> g) << (g + 3)) | ((grp & 7u) << g) | (k & ((1u << g) - 1u));
+    }
+  }
+  const uint32_t tile = grp * 4u + (threadIdx.x >> 6);
   if (tile >= a.num_tiles) return;
   const uint64_t n = a.n;
   const uint32_t log2B = a.log2B;
