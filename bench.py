@@ -51,15 +51,15 @@ KERNEL_SRC = [os.path.join(ROOT, "paper_2609_04609_amd", "csrc", f)
 # scaled by what the counters read for a 1 GiB copy) for the sources whose
 # concatenation has this sha256; see profiles/hbm_traffic_*.md. Reported only
 # while those sources are unchanged.
-_SRC_SHA = "5ea3eccaf1b8cce559eefa4d68c515bc98000c9eedd72dd34a80766b75d17642"
+_SRC_SHA = "a094dfc5361fbb82361c08040d3051964513af641967d91806d0561ab564bb56"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925384926,
-                                  "encode": 423494037},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48918941394,
+                                  "encode": 423463447},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1778733090,
-                                        "encode": 123672637},
+                                        "decode": 1778682501,
+                                        "encode": 123682914},
 }
 
 
