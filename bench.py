@@ -891,10 +891,27 @@ def probe_lib():
         lib = ctypes.CDLL(path)
         for f in (lib.ciera_probe_encode_shaped, lib.ciera_probe_decode_shaped):
             f.restype = ctypes.c_int
-            f.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_uint64,
-                                                  ctypes.c_void_p]
+        lib.ciera_probe_encode_shaped.argtypes = (
+            [ctypes.c_void_p] * 3 + [ctypes.c_uint64, ctypes.c_int,
+                                     ctypes.c_void_p])
+        lib.ciera_probe_decode_shaped.argtypes = (
+            [ctypes.c_void_p] * 3 + [ctypes.c_uint64, ctypes.c_void_p])
         _PROBE = lib
     return _PROBE
+
+
+def encode_xcd_runs(n, B):
+    """Whether the encode's streaming pass walks its workgroups in runs of 32
+    per XCD at this shard size and block size: the library's own rule (the
+    exception pass gives each wave two tiles or more, B >= 16), restated so
+    that the encode-shaped probe takes the same order."""
+    if B < 16:
+        return False
+    l = B.bit_length() - 1
+    tile = 4096 if l <= 9 else 8 << l
+    tiles = max(1, -(-n // tile))
+    waves = 8192 if l >= 9 else 16384
+    return -(-tiles // waves) >= 2
 
 
 def time_stream_ceiling(S, steps, stream, start):
@@ -910,6 +927,7 @@ def time_stream_ceiling(S, steps, stream, start):
     lib = probe_lib()
     h = torch.cuda.current_stream().cuda_stream
     scratch = torch.empty(n, dtype=torch.uint8, device=S.dev)
+    runs = int(encode_xcd_runs(n, B))
     sm = S.gA[:R * n] if S.gA.numel() >= R * n else None
     pe, pd = [], []
     for i in range(steps + 2):
@@ -932,7 +950,7 @@ def time_stream_ceiling(S, steps, stream, start):
         se.arm(stream)
         rc = lib.ciera_probe_encode_shaped(w_in.data_ptr(),
                                            S.send_cache.data_ptr(),
-                                           scratch.data_ptr(), n, h)
+                                           scratch.data_ptr(), n, runs, h)
         se.close(stream)
         if rc:
             raise RuntimeError("encode-shaped probe failed")

@@ -6,7 +6,9 @@
 //   encode-shaped: per value read 2 bytes (a bf16 value, non-temporal) and
 //     1 byte (its cached exponent, plain), write 1 byte (non-temporal): the
 //     access pattern of the encode's streaming pass with the fused cache
-//     update, one wave per 4096 values.
+//     update, one wave per 4096 values, the workgroups walked in order or
+//     (runs != 0) in runs of 32 per XCD, whichever that pass takes at the
+//     caller's shape.
 //   decode-shaped: per value read 1 byte (sign|mantissa) and 1 byte (the
 //     exponent), write 2 bytes, all non-temporal: the access pattern of the
 //     merge, one 256-thread workgroup per 16384 values, the tiles walked in
@@ -46,9 +48,16 @@ constexpr uint64_t kEncTile = 4096;   // values per wave
 constexpr uint64_t kDecTile = 16384;  // values per workgroup
 
 __global__ __launch_bounds__(256) void encode_shaped_kernel(
-    const uint16_t *w, const uint8_t *c, uint8_t *out, uint64_t n) {
+    const uint16_t *w, const uint8_t *c, uint8_t *out, uint64_t n, int runs) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint64_t tbase = (uint64_t(blockIdx.x) * 4u + wave) * kEncTile;
+  // workgroup L = 8k + x (XCD x, its k-th) takes the values of workgroup
+  // (k / 32) 256 + 32 x + k mod 32; the tail short of 256 keeps its place
+  uint32_t grp = blockIdx.x;
+  if (runs && grp < ((gridDim.x >> 8) << 8)) {
+    const uint32_t k = grp >> 3;
+    grp = ((k >> 5) << 8) | ((grp & 7u) << 5) | (k & 31u);
+  }
+  const uint64_t tbase = (uint64_t(grp) * 4u + wave) * kEncTile;
   if (tbase >= n) return;
   uint4 wv[8];
   uint2 cv[8];
@@ -114,14 +123,15 @@ bool ok16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 extern "C" {
 
-// out[k] = (w[k] >> 8) ^ c[k] for k < n.
+// out[k] = (w[k] >> 8) ^ c[k] for k < n; runs: the workgroup order above.
 int ciera_probe_encode_shaped(const uint16_t *w, const uint8_t *c,
-                              uint8_t *out, uint64_t n, hipStream_t stream) {
+                              uint8_t *out, uint64_t n, int runs,
+                              hipStream_t stream) {
   if (n % 8 || !ok16(w) || !ok16(c) || !ok16(out)) return hipErrorInvalidValue;
   if (n == 0) return hipSuccess;
   const uint64_t groups = (n + 4 * kEncTile - 1) / (4 * kEncTile);
   hipLaunchKernelGGL(encode_shaped_kernel, dim3(uint32_t(groups)), dim3(256),
-                     0, stream, w, c, out, n);
+                     0, stream, w, c, out, n, runs);
   return hipGetLastError();
 }
 

@@ -22,7 +22,8 @@ def test_probe_library_exports_its_two_calls():
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("n", [8, 4096, 16384 * 3 + 8, 1 << 20,
-                               16384 * 300 + 8])  # 301 tiles: runs and tail
+                               16384 * 300 + 8,  # 301 tiles: runs and tail
+                               16384 * 700 + 8])  # 701 workgroups (encode)
 def test_probes_compute_their_byte_maps(n):
     import torch
     import bench
@@ -37,16 +38,19 @@ def test_probes_compute_their_byte_maps(n):
     o8 = torch.empty(n, dtype=torch.uint8, device="cuda")
     o16 = torch.empty(n, dtype=torch.int16, device="cuda")
     h = torch.cuda.current_stream().cuda_stream
-    assert lib.ciera_probe_encode_shaped(dw.data_ptr(), dc.data_ptr(),
-                                         o8.data_ptr(), n, h) == 0
+    for runs in (0, 1):  # workgroups in order, and in runs of 32 per XCD
+        o8.fill_(0)
+        assert lib.ciera_probe_encode_shaped(dw.data_ptr(), dc.data_ptr(),
+                                             o8.data_ptr(), n, runs, h) == 0
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(o8.cpu().numpy(),
+                                      ((w >> 8).astype(np.uint8) ^ c))
     assert lib.ciera_probe_decode_shaped(dsm.data_ptr(), dc.data_ptr(),
                                          o16.data_ptr(), n, h) == 0
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(o8.cpu().numpy(),
-                                  ((w >> 8).astype(np.uint8) ^ c))
     np.testing.assert_array_equal(
         o16.cpu().numpy().view(np.uint16),
         (c.astype(np.uint16) << 8) | sm.astype(np.uint16))
     # a length that is not a multiple of 8 is refused before any launch
     assert lib.ciera_probe_encode_shaped(dw.data_ptr(), dc.data_ptr(),
-                                         o8.data_ptr(), n - 1, h) != 0
+                                         o8.data_ptr(), n - 1, 0, h) != 0
