@@ -55,11 +55,11 @@ _SRC_SHA = "a094dfc5361fbb82361c08040d3051964513af641967d91806d0561ab564bb56"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48918941394,
-                                  "encode": 423463447},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925607934,
+                                  "encode": 423467590},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1778682501,
-                                        "encode": 123682914},
+                                        "decode": 1778721212,
+                                        "encode": 123695062},
 }
 
 
