@@ -127,7 +127,8 @@ struct EncArgs {
   bool scan_prefix;
   // B >= 16: tiles per wave of the exception pass
   uint32_t exc_tiles_per_wave;
-  // pass 1: log2 of the workgroups per XCD turn (0: in order)
+  // pass 1 and the row-wise exception pass: log2 of the workgroups per XCD
+  // turn (0: in order)
   uint32_t xcd_run_log2;
   bool f16;  // fp16 values (B >= 16)
   // block-hash detector (B >= 16) in place of exact compare with `cache`

@@ -982,7 +982,16 @@ __global__ __launch_bounds__(kThreads) void encode_exc_rows_kernel(EncArgs a) {
   const uint8_t *const bmp = a.out + kHeaderBytes + n16;
   uint8_t *const exc_out = a.out + kHeaderBytes + n16 + pad16(bm);
   const uint64_t nt = a.num_tiles, tpw = a.exc_tiles_per_wave;
-  const uint64_t g0 = min(uint64_t(blockIdx.x) * 4u * tpw, nt);
+  // the workgroups in runs per XCD where pass 1 takes them (as there)
+  uint32_t grp = blockIdx.x;
+  if (a.xcd_run_log2) {
+    const uint32_t g = a.xcd_run_log2;
+    if (grp < ((gridDim.x >> (g + 3)) << (g + 3))) {
+      const uint32_t k = grp >> 3;
+      grp = ((k >> g) << (g + 3)) | ((grp & 7u) << g) | (k & ((1u << g) - 1u));
+    }
+  }
+  const uint64_t g0 = min(uint64_t(grp) * 4u * tpw, nt);
   const uint64_t t0 = min(g0 + wave * tpw, nt);
   const uint64_t t1 = min(t0 + tpw, nt);
   const uint64_t rows = (n + 511) >> 9;
