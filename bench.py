@@ -51,15 +51,15 @@ KERNEL_SRC = [os.path.join(ROOT, "paper_2609_04609_amd", "csrc", f)
 # scaled by what the counters read for a 1 GiB copy) for the sources whose
 # concatenation has this sha256; see profiles/hbm_traffic_*.md. Reported only
 # while those sources are unchanged.
-_SRC_SHA = "a094dfc5361fbb82361c08040d3051964513af641967d91806d0561ab564bb56"
+_SRC_SHA = "af9052628ae3d84f8ef73c869c5cab68544f0451f31ad7e535ecdd7522c7e00d"
 MEASURED_TRAFFIC = {
     # ciera_decode_gathered (tile_prefix_kernel + decode_kernel) and the
     # fused-update ciera_encode (encode_pass_kernel + encode_exc_rows_kernel)
-    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48925607934,
-                                  "encode": 423467590},
+    ("dsv3_layer", 512, "bf16"): {"sha": _SRC_SHA, "decode": 48928094659,
+                                  "encode": 423501392},
     ("olmoe_layer_c0.1", 512, "bf16"): {"sha": _SRC_SHA,
-                                        "decode": 1778721212,
-                                        "encode": 123695062},
+                                        "decode": 1778761534,
+                                        "encode": 123671142},
 }
 
 
