@@ -154,3 +154,26 @@ def test_hashed_chain_keeps_caches_in_step(gu, orc, B):
         np.testing.assert_array_equal(_host_u64(h),
                                       orc.hash_blocks(gu.host_u16(nxt), B))
         cur = nxt
+
+
+@pytest.mark.parametrize("B,n", [(512, 40_000_017), (64, 70_000_003)])
+def test_encode_hashed_large_shards(gu, orc, B, n):
+    """Shards large enough for the exception pass to take two tiles a wave
+    or more, where the streaming pass walks its workgroups in runs per XCD:
+    hashed and exact-compare encodes against the oracle."""
+    from paper_2609_04609_amd import ciera
+    w, w2 = gu.pair(n, 900 + B, c=0.001)
+    wh, w2h = gu.host_u16(w), gu.host_u16(w2)
+    h_old = orc.hash_blocks(wh, B)
+    expect, h_new = orc.encode_hashed(w2h, h_old, B)
+    cache_h, _ = orc.split(wh)
+    np.testing.assert_array_equal(expect, orc.encode(w2h, cache_h, B))
+    ws = ciera.Workspace(n, 1, B)
+    got, total, hout = _gpu_encode_hashed(gu, w2, h_old, B, ws)
+    assert total == expect.size
+    np.testing.assert_array_equal(got[:total], expect)
+    np.testing.assert_array_equal(hout, h_new)
+    out, total, _ = gu.gpu_encode(w2, gu.dev_u8(cache_h), B, ws)
+    assert total == expect.size
+    np.testing.assert_array_equal(gu.host_u8(out[:total]), expect)
+    assert ws.error() == 0
