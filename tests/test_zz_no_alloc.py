@@ -2,8 +2,9 @@
 its tile offsets live in the library's device scratch array) against
 ciera_decode_gathered with a workspace, through the C ABI, bit for bit: two
 calls in a row on the same scratch, the second with a smaller input, for the
-paths that use the scratch (B = 1 per-tile counts, B >= 16 with the prefix
-pass) and one that does not; then the error word of a call with a bad shard,
+paths that use the scratch (B = 1 per-tile counts, added up in the merge or
+scanned first on large layers; B >= 16 with the prefix pass) and one that
+does not; then the error word of a call with a bad shard,
 and of the clean call after it."""
 import numpy as np
 import pytest
@@ -58,7 +59,8 @@ def _both(lib, g, o, n, B, cache0):
 
 
 @pytest.mark.parametrize("B,first,second", [
-    (1, (4, 1_000_003), (2, 70_001)),          # per-tile counts and scan
+    (1, (4, 1_000_003), (2, 70_001)),          # per-tile counts summed
+    (1, (3, 90_000_007), (2, 70_001)),         # counts scanned, then summed
     (16, (16, 6_000_008), (3, 100_000)),       # prefix pass, then without
     (512, (3, 300_007), (2, 16_385)),          # counts in the tile
 ])
